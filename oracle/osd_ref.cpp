@@ -1,0 +1,444 @@
+/*
+ * osd_ref.cpp -- plain fp64 CPU oracle (test infrastructure only).
+ *
+ * Restates, loop by loop, what the verification and distillation steps of
+ * online speculative decoding compute (arXiv:2310.07177).  Nothing here is
+ * blocked, fused or reordered: each function follows the definition it
+ * cites, so that a reader can check it against the paper by eye.  It shares
+ * no code with the HIP library.
+ *
+ * Readings of points the paper leaves open are stated where they are used:
+ *   - acceptance is "u < p(y)/q(y)" with u in [0,1) (Appendix A.1 writes
+ *     u <= p/q; the two agree except on a set of u of measure zero);
+ *   - the extra token is drawn by inverse CDF over ascending token id with a
+ *     strict ">" so that zero-mass tokens are never drawn (Eq. 5 names the
+ *     distribution, not the sampler);
+ *   - the same temperature scales target and draft logits (Section 4.1);
+ *   - temperature 0 means greedy verification: accept while the draft token
+ *     equals the target argmax (lowest index on ties), emit that argmax;
+ *   - the gradient is the exact derivative with respect to the raw student
+ *     logits, including the 1/tau factor of the temperature softmax.
+ */
+#include "osd_ref.h"
+
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+namespace {
+
+const double kInf = std::numeric_limits<double>::infinity();
+const double kNaN = std::numeric_limits<double>::quiet_NaN();
+
+/* One logit, converted exactly to fp64. */
+double load_logit(const void* base, int dtype, int64_t idx) {
+    if (dtype == OSD_REF_F32) {
+        return (double)((const float*)base)[idx];
+    }
+    if (dtype == OSD_REF_BF16) {
+        uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;
+        float f;
+        std::memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+    return ((const double*)base)[idx];
+}
+
+/* A row of V logits starting at element offset `off`. */
+std::vector<double> load_row(const void* base, int dtype, int64_t off, int V) {
+    std::vector<double> z((size_t)V);
+    for (int j = 0; j < V; ++j) z[(size_t)j] = load_logit(base, dtype, off + j);
+    return z;
+}
+
+/*
+ * Temperature softmax, softmax(z / T), and its log (Section 4.1 uses a
+ * tunable temperature on the logits before the softmax).  The maximum is
+ * subtracted before exponentiating; that leaves the value unchanged in exact
+ * arithmetic.  Returns false when the row has no finite logit (every
+ * probability would be 0/0).
+ */
+bool temperature_softmax(const std::vector<double>& z, double T,
+                         std::vector<double>& prob,
+                         std::vector<double>& logprob) {
+    const size_t V = z.size();
+    double m = -kInf;
+    for (size_t j = 0; j < V; ++j) {
+        double x = z[j] / T;
+        if (x > m) m = x;
+    }
+    if (!(m > -kInf) || !std::isfinite(m)) return false;
+    double s = 0.0;
+    for (size_t j = 0; j < V; ++j) s += std::exp(z[j] / T - m);
+    double lse = m + std::log(s);
+    prob.assign(V, 0.0);
+    logprob.assign(V, 0.0);
+    for (size_t j = 0; j < V; ++j) {
+        prob[j] = std::exp(z[j] / T - m) / s;
+        logprob[j] = z[j] / T - lse;
+    }
+    return true;
+}
+
+/*
+ * Inverse-CDF draw from the unnormalised weights r (all >= 0) with total Z:
+ * the smallest j whose running sum C_j exceeds c = u * Z, walking ascending
+ * token ids.  If rounding leaves c at or beyond the last running sum, the
+ * last token with r_j > 0 is taken.  *margin receives
+ * min(C_j - c, c - C_{j-1}), the distance in probability mass from c to the
+ * nearer edge of the chosen interval.
+ */
+int inverse_cdf(const std::vector<double>& r, double Z, float u,
+                double* margin) {
+    const double c = (double)u * Z;
+    double C = 0.0;
+    for (size_t j = 0; j < r.size(); ++j) {
+        double prev = C;
+        C += r[j];
+        if (C > c) {
+            double a = C - c, b = c - prev;
+            *margin = a < b ? a : b;
+            return (int)j;
+        }
+    }
+    for (size_t j = r.size(); j-- > 0;) {
+        if (r[j] > 0.0) {
+            *margin = 0.0;
+            return (int)j;
+        }
+    }
+    *margin = 0.0;
+    return -1;
+}
+
+/* Greedy reading: the target argmax, lowest index on ties.  -1 if the row has
+ * no finite logit. */
+int row_argmax(const std::vector<double>& z) {
+    int best = -1;
+    double bv = -kInf;
+    for (size_t j = 0; j < z.size(); ++j) {
+        if (z[j] > bv) {
+            bv = z[j];
+            best = (int)j;
+        }
+    }
+    if (best >= 0 && !std::isfinite(bv)) return -1;
+    return best;
+}
+
+void mark_invalid(int b, int K, int32_t* accepted_len, int32_t* out_tokens,
+                  uint8_t* reject_mask) {
+    accepted_len[b] = -1;
+    for (int i = 0; i <= K; ++i) out_tokens[(size_t)b * (K + 1) + i] = -1;
+    if (reject_mask)
+        for (int i = 0; i < K; ++i) reject_mask[(size_t)b * K + i] = 0;
+}
+
+}  // namespace
+
+extern "C" int osd_ref_verify(const void* target, const void* draft, int dtype,
+                              int B, int K, int V,
+                              const int32_t* draft_tokens,
+                              const int32_t* draft_len,
+                              const float* u_accept, const float* u_resample,
+                              float temperature, int32_t* accepted_len,
+                              int32_t* out_tokens, uint8_t* reject_mask,
+                              double* margin_accept, double* margin_cdf,
+                              int32_t* z_fallback) {
+    if (!target || !draft_tokens || !accepted_len || !out_tokens) return -1;
+    if (B <= 0 || K <= 0 || V <= 0) return -1;
+    if (dtype != OSD_REF_F32 && dtype != OSD_REF_BF16 && dtype != OSD_REF_F64)
+        return -1;
+    if (!(temperature >= 0.0f) || std::isinf(temperature)) return -1;
+    const bool greedy = temperature == 0.0f;
+    if (!greedy && (!draft || !u_accept || !u_resample)) return -1;
+    const double T = (double)temperature;
+    const int64_t tstride = (int64_t)(K + 1) * V, dstride = (int64_t)K * V;
+
+    for (int b = 0; b < B; ++b) {
+        if (margin_accept)
+            for (int i = 0; i < K; ++i) margin_accept[(size_t)b * K + i] = kNaN;
+        if (margin_cdf) margin_cdf[b] = kNaN;
+        if (z_fallback) z_fallback[b] = 0;
+        if (reject_mask)
+            for (int i = 0; i < K; ++i) reject_mask[(size_t)b * K + i] = 0;
+
+        /* Ragged proposals: k_b tokens were proposed; target row k_b is the
+         * bonus row.  Anything past k_b is padding and is never read. */
+        const int kb = draft_len ? draft_len[b] : K;
+        if (kb < 1 || kb > K) {
+            mark_invalid(b, K, accepted_len, out_tokens, reject_mask);
+            continue;
+        }
+        const int32_t* y = draft_tokens + (size_t)b * K;
+        bool ok = true;
+        for (int i = 0; i < kb; ++i)
+            if (y[i] < 0 || y[i] >= V) ok = false;
+        if (!ok) {
+            mark_invalid(b, K, accepted_len, out_tokens, reject_mask);
+            continue;
+        }
+
+        int a = kb;       /* number of accepted draft tokens */
+        int extra = -1;   /* the one additional token */
+
+        if (greedy) {
+            /* Accept while the proposal equals the target argmax; the extra
+             * token is the target argmax at the first mismatch, or at the
+             * bonus row. */
+            for (int i = 0; i <= kb && ok; ++i) {
+                std::vector<double> t =
+                    load_row(target, dtype, b * tstride + (int64_t)i * V, V);
+                int g = row_argmax(t);
+                if (g < 0) {
+                    ok = false;
+                    break;
+                }
+                if (i == kb || y[i] != g) {
+                    a = i;
+                    extra = g;
+                    break;
+                }
+            }
+        } else {
+            /* Appendix A.1: with i rising from 1 to k, accept y_i if
+             * u < p(y_i)/q(y_i); otherwise stop.  Rows are 0-based here:
+             * row i scores proposal y[i]. */
+            std::vector<double> P, logP, Q, logQ;
+            bool rejected = false;
+            for (int i = 0; i < kb; ++i) {
+                std::vector<double> t =
+                    load_row(target, dtype, b * tstride + (int64_t)i * V, V);
+                std::vector<double> d =
+                    load_row(draft, dtype, b * dstride + (int64_t)i * V, V);
+                if (!temperature_softmax(t, T, P, logP) ||
+                    !temperature_softmax(d, T, Q, logQ)) {
+                    ok = false;
+                    break;
+                }
+                const double py = P[(size_t)y[i]], qy = Q[(size_t)y[i]];
+                double ratio;
+                if (qy > 0.0)
+                    ratio = py / qy;
+                else
+                    ratio = py > 0.0 ? kInf : 0.0;
+                const float u = u_accept[(size_t)b * K + i];
+                if (margin_accept)
+                    margin_accept[(size_t)b * K + i] = std::fabs((double)u - ratio);
+                if (!((double)u < ratio)) {
+                    a = i;
+                    rejected = true;
+                    break;
+                }
+            }
+            if (ok) {
+                /* Eq. 5: after a rejection at a the extra token comes from
+                 * norm(max(0, p - q)) at row a; after k_b acceptances it
+                 * comes from p at the bonus row k_b. */
+                std::vector<double> r((size_t)V);
+                double Z = 0.0;
+                if (rejected) {
+                    for (int j = 0; j < V; ++j) {
+                        double diff = P[(size_t)j] - Q[(size_t)j];
+                        r[(size_t)j] = diff > 0.0 ? diff : 0.0;
+                    }
+                    for (int j = 0; j < V; ++j) Z += r[(size_t)j];
+                    if (!(Z > 0.0)) {
+                        /* Exact arithmetic rules this out (a rejection needs
+                         * p(y) < q(y), so some other p_j > q_j); under
+                         * rounding the draw falls back to p. */
+                        r = P;
+                        Z = 0.0;
+                        for (int j = 0; j < V; ++j) Z += r[(size_t)j];
+                        if (z_fallback) z_fallback[b] = 1;
+                    }
+                } else {
+                    std::vector<double> t =
+                        load_row(target, dtype, b * tstride + (int64_t)kb * V, V);
+                    if (!temperature_softmax(t, T, P, logP)) {
+                        ok = false;
+                    } else {
+                        r = P;
+                        for (int j = 0; j < V; ++j) Z += r[(size_t)j];
+                    }
+                }
+                if (ok) {
+                    double margin = 0.0;
+                    extra = inverse_cdf(r, Z, u_resample[b], &margin);
+                    if (margin_cdf) margin_cdf[b] = margin;
+                    if (extra < 0) ok = false;
+                }
+            }
+        }
+
+        if (!ok) {
+            mark_invalid(b, K, accepted_len, out_tokens, reject_mask);
+            if (margin_cdf) margin_cdf[b] = kNaN;
+            continue;
+        }
+        /* Emit y_1..y_a and the extra token (Algorithm 1: a + 1 new tokens);
+         * record the error index a when a proposal was rejected. */
+        accepted_len[b] = a;
+        int32_t* out = out_tokens + (size_t)b * (K + 1);
+        for (int i = 0; i <= K; ++i) out[i] = -1;
+        for (int i = 0; i < a; ++i) out[i] = y[i];
+        out[a] = extra;
+        if (reject_mask && a < kb) reject_mask[(size_t)b * K + a] = 1;
+    }
+    return 0;
+}
+
+extern "C" int osd_ref_distill_loss_grad(const void* teacher,
+                                         int64_t teacher_batch_stride,
+                                         const void* student,
+                                         int64_t student_batch_stride,
+                                         int dtype, int B, int K, int V,
+                                         const uint8_t* mask, int kind,
+                                         double beta, double tau,
+                                         double* loss_out, double* row_loss,
+                                         double* grad) {
+    if (!teacher || !student || !loss_out) return -1;
+    if (B <= 0 || K <= 0 || V <= 0) return -1;
+    if (dtype != OSD_REF_F32 && dtype != OSD_REF_BF16 && dtype != OSD_REF_F64)
+        return -1;
+    if (kind != OSD_REF_FKL && kind != OSD_REF_RKL && kind != OSD_REF_JSD)
+        return -1;
+    if (!(tau > 0.0) || std::isinf(tau)) return -1;
+    if (!(beta >= 0.0 && beta <= 1.0)) return -1;
+
+    double loss_sum = 0.0, count = 0.0;
+    std::vector<double> P, logP, Q, logQ;
+    for (int b = 0; b < B; ++b) {
+        for (int i = 0; i < K; ++i) {
+            const size_t n = (size_t)b * K + i;
+            double* g = grad ? grad + n * (size_t)V : nullptr;
+            const bool on = mask ? mask[n] != 0 : true;
+            if (!on) {
+                if (row_loss) row_loss[n] = 0.0;
+                if (g)
+                    for (int j = 0; j < V; ++j) g[j] = 0.0;
+                continue;
+            }
+            std::vector<double> t = load_row(
+                teacher, dtype, b * teacher_batch_stride + (int64_t)i * V, V);
+            std::vector<double> s = load_row(
+                student, dtype, b * student_batch_stride + (int64_t)i * V, V);
+            double D = kNaN;
+            bool ok = temperature_softmax(t, tau, P, logP) &&
+                      temperature_softmax(s, tau, Q, logQ);
+            if (ok && kind == OSD_REF_FKL) {
+                /* Eq. 3: KL(p || q) = sum_j p_j (log p_j - log q_j), with
+                 * 0 log 0 = 0.  d/ds_j = (q_j - p_j) / tau. */
+                D = 0.0;
+                for (int j = 0; j < V; ++j)
+                    if (P[(size_t)j] > 0.0)
+                        D += P[(size_t)j] * (logP[(size_t)j] - logQ[(size_t)j]);
+                if (g)
+                    for (int j = 0; j < V; ++j)
+                        g[j] = (Q[(size_t)j] - P[(size_t)j]) / tau;
+            } else if (ok && kind == OSD_REF_RKL) {
+                /* Eq. 3: KL(q || p).  d/ds_j = q_j (log q_j - log p_j - KL) / tau. */
+                D = 0.0;
+                for (int j = 0; j < V; ++j)
+                    if (Q[(size_t)j] > 0.0)
+                        D += Q[(size_t)j] * (logQ[(size_t)j] - logP[(size_t)j]);
+                if (g)
+                    for (int j = 0; j < V; ++j)
+                        g[j] = Q[(size_t)j] > 0.0
+                                   ? Q[(size_t)j] *
+                                         (logQ[(size_t)j] - logP[(size_t)j] - D) /
+                                         tau
+                                   : 0.0;
+            } else if (ok) {
+                /* Eq. 3: JSD[beta] = beta KL(p || m) + (1-beta) KL(q || m) with
+                 * m = beta p + (1-beta) q (beta weights the teacher).
+                 * d/ds_j = (1-beta) q_j (log q_j - log m_j - KL(q || m)) / tau. */
+                std::vector<double> logM((size_t)V);
+                for (int j = 0; j < V; ++j)
+                    logM[(size_t)j] =
+                        std::log(beta * P[(size_t)j] + (1.0 - beta) * Q[(size_t)j]);
+                double kl_pm = 0.0, kl_qm = 0.0;
+                for (int j = 0; j < V; ++j)
+                    if (P[(size_t)j] > 0.0)
+                        kl_pm += P[(size_t)j] * (logP[(size_t)j] - logM[(size_t)j]);
+                for (int j = 0; j < V; ++j)
+                    if (Q[(size_t)j] > 0.0)
+                        kl_qm += Q[(size_t)j] * (logQ[(size_t)j] - logM[(size_t)j]);
+                D = beta * kl_pm + (1.0 - beta) * kl_qm;
+                if (g)
+                    for (int j = 0; j < V; ++j)
+                        g[j] = Q[(size_t)j] > 0.0
+                                   ? (1.0 - beta) * Q[(size_t)j] *
+                                         (logQ[(size_t)j] - logM[(size_t)j] - kl_qm) /
+                                         tau
+                                   : 0.0;
+            } else if (g) {
+                for (int j = 0; j < V; ++j) g[j] = kNaN;
+            }
+            if (row_loss) row_loss[n] = D;
+            /* Eq. 2 averages over the batch; Eq. 4 sums over positions: the
+             * loss is reported as both, the gradient is of the sum. */
+            loss_sum += D;
+            count += 1.0;
+        }
+    }
+    loss_out[0] = count > 0.0 ? loss_sum / count : 0.0;
+    loss_out[1] = loss_sum;
+    return 0;
+}
+
+namespace {
+
+/* Spacing of bf16 values around |x| (8 significant bits; the subnormal
+ * spacing below 2^-126). */
+double bf16_quantum(double x) {
+    int e;
+    std::frexp(x, &e); /* |x| = f * 2^e, f in [0.5, 1) */
+    double q = std::ldexp(1.0, e - 8);
+    double qmin = std::ldexp(1.0, -133);
+    return q > qmin ? q : qmin;
+}
+
+}  // namespace
+
+extern "C" void osd_ref_round_bf16(const double* x, uint16_t* out, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) {
+        double v = x[i];
+        float f;
+        if (std::isnan(v)) {
+            f = std::numeric_limits<float>::quiet_NaN();
+        } else if (std::isinf(v) || v == 0.0) {
+            f = (float)v;
+        } else {
+            double q = bf16_quantum(v);
+            /* nearbyint rounds half to even in the default mode */
+            double r = std::nearbyint(v / q) * q;
+            /* exact: r has at most 8 significant bits; a value that rounds
+             * up to 2^128 becomes infinity, as RNE to bf16 requires */
+            f = (float)r;
+        }
+        uint32_t bits;
+        std::memcpy(&bits, &f, sizeof bits);
+        out[i] = (uint16_t)(bits >> 16);
+    }
+}
+
+extern "C" void osd_ref_round_f32(const double* x, float* out, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) out[i] = (float)x[i];
+}
+
+extern "C" void osd_ref_bf16_midpoint_flags(const double* x, uint8_t* flag,
+                                            int64_t n, double rel) {
+    for (int64_t i = 0; i < n; ++i) {
+        double v = x[i];
+        if (!std::isfinite(v) || v == 0.0) {
+            flag[i] = 0;
+            continue;
+        }
+        double q = bf16_quantum(v);
+        double k = std::floor(v / q);
+        double mid = (k + 0.5) * q;
+        flag[i] = std::fabs(v - mid) <= rel * std::fabs(v) ? 1 : 0;
+    }
+}

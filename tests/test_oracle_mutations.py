@@ -1,0 +1,61 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case copies the oracle source, plants one mistake by text substitution,
+builds the copy with the host compiler into a temporary directory, and runs
+the pin suites against it in a child process; at least one pin must fail.
+Nothing here touches the GPU or the HIP library.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "osd_ref.cpp")
+
+MUTATIONS = {
+    "residual_without_q": ("double diff = P[(size_t)j] - Q[(size_t)j];",
+                           "double diff = P[(size_t)j];"),
+    "ratio_inverted": ("ratio = py / qy;", "ratio = qy / py;"),
+    "bonus_row_off_by_one": ("b * tstride + (int64_t)kb * V, V);",
+                             "b * tstride + (int64_t)(kb - 1) * V, V);"),
+    "cdf_non_strict": ("if (C > c) {", "if (C >= c) {"),
+    "accept_continues_after_reject": ("                    a = i;\n                    rejected = true;\n                    break;",
+                                      "                    a = i;\n                    rejected = true;"),
+    "rkl_grad_missing_kl_term": ("(logQ[(size_t)j] - logP[(size_t)j] - D) /",
+                                 "(logQ[(size_t)j] - logP[(size_t)j]) /"),
+    "jsd_mixture_swapped": ("std::log(beta * P[(size_t)j] + (1.0 - beta) * Q[(size_t)j]);",
+                            "std::log(beta * Q[(size_t)j] + (1.0 - beta) * P[(size_t)j]);"),
+    "fkl_grad_missing_tau": ("g[j] = (Q[(size_t)j] - P[(size_t)j]) / tau;",
+                             "g[j] = (Q[(size_t)j] - P[(size_t)j]);"),
+    "fkl_sign_flipped": ("D += P[(size_t)j] * (logP[(size_t)j] - logQ[(size_t)j]);",
+                         "D += P[(size_t)j] * (logQ[(size_t)j] - logP[(size_t)j]);"),
+    "verify_temperature_ignored": ("const double T = (double)temperature;",
+                                   "const double T = 1.0;"),
+    "distill_temperature_ignored": ("bool ok = temperature_softmax(t, tau, P, logP) &&\n                      temperature_softmax(s, tau, Q, logQ);",
+                                    "bool ok = temperature_softmax(t, 1.0, P, logP) &&\n                      temperature_softmax(s, 1.0, Q, logQ);"),
+    "argmax_last_on_ties": ("if (z[j] > bv) {", "if (z[j] >= bv) {"),
+    "bf16_round_truncates": ("double r = std::nearbyint(v / q) * q;",
+                             "double r = std::trunc(v / q) * q;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not found exactly once: {name}"
+    mutated = tmp_path / "osd_ref_mut.cpp"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "libosd_ref_mut.so"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-fPIC", "-shared", "-I",
+                    os.path.join(ROOT, "oracle"), "-o", str(lib), str(mutated)],
+                   check=True)
+    env = dict(os.environ, OSD_REF_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_verify_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_distill_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"
