@@ -1,0 +1,270 @@
+"""Throughput of the OSD logits path on one MI355X.
+
+A step is one pass of the whole hot path over one batch: osd_verify
+(speculative-sampling verification at T = 0.7) followed by
+osd_distill_loss_grad (JSD, beta = 0.5, tau = 0.7, with the bf16 gradient)
+on the T5-vocabulary workload: B = 64 sequences, k = 8 proposals, V = 32128,
+bf16 logits, target ~ N(0, 2.5^2), draft = 0.7 target + N(0, 1.5^2).
+
+Inputs are synthetic and seeded; R copies of the batch rotate through the
+timed loop so that consecutive launches never find their inputs in the 256 MB
+Infinity Cache.  Each kernel is also timed alone (HIP events on the stream the
+kernels are launched on) to report its achieved HBM bandwidth against the
+8 TB/s peak.  The CPU baseline is the fp64 oracle on the host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+import argparse
+import ctypes
+import glob
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+B, K, V = 64, 8, 32128
+T_VERIFY, TAU, BETA = 0.7, 0.7, 0.5
+INFINITY_CACHE = 256 << 20
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--kernel-iters", type=int, default=400)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--only", default=None,
+                   help="profiling aid: run just one kernel loop (verify|greedy|jsd|rkl|copy)")
+    return p.parse_args()
+
+
+def verify_bytes(B, K, V, elem=2, greedy=False):
+    """Algorithmic bytes of one osd_verify call with every k_b = K: each target
+    row 0..K and draft row 0..K-1 read once (greedy: target rows only), the
+    proposals and uniforms read once, the outputs written once."""
+    rows = B * (K + 1) + (0 if greedy else B * K)
+    small = 4 * B * K + (0 if greedy else 4 * B * K + 4 * B) + 4 * B + 4 * B * (K + 1) + B * K
+    return rows * V * elem + small
+
+
+def distill_bytes(B, K, V, masked_rows, elem=2):
+    """Algorithmic bytes of one osd_distill_loss_grad call: teacher and student
+    rows read once where the mask is 1, the whole gradient written once, the
+    mask read, the per-row and total losses written."""
+    return masked_rows * 2 * V * elem + B * K * V * elem + B * K + 4 * B * K + 8
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2310_07177_amd", "csrc", "*"))):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(kernel_key, per_launch_algo_bytes):
+    """Measured HBM bytes per launch from the committed PMC summary, if it was
+    taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except ValueError:
+        return None
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    k = d.get("kernels", {}).get(kernel_key)
+    if not k:
+        return None
+    return k.get("bytes_per_launch")
+
+
+def cpu_baseline():
+    """The fp64 oracle on the host: one full batch (64 sequences, 512
+    positions) of verification + JSD distillation, single-threaded."""
+    from oracle import ref
+    from paper_2310_07177_amd import synth
+    x = synth.config_t5_vocab(seed=0)
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        ref.verify(x["target"], x["draft"], x["tokens"], x["u_accept"], x["u_resample"], T_VERIFY)
+        ref.distill(x["target"], x["draft"], "jsd", beta=BETA, tau=TAU, mask=x["mask"], B=B, K=K,
+                    teacher_batch_stride=(K + 1) * V, student_batch_stride=K * V)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el > 10.0 or reps >= 3:
+            break
+    return {"value": reps * B * K / el, "unit": "positions/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} full batch(es) of B=64 k=8 V=32128 bf16 (verify T=0.7 + JSD "
+                      f"beta=0.5 tau=0.7 with gradient), {el:.1f} s single-threaded fp64"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the path shards by "
+              "sequence with no exchange, so multi-GPU throughput is N x the one-GPU figure; "
+              "no multi-GPU run is made.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2310_07177_amd as osd
+    from paper_2310_07177_amd import binding, synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = osd.lib()
+    x = synth.config_t5_vocab(seed=0)
+    xg = synth.config_t5_vocab(seed=0, greedy=True)
+
+    def t_(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    base = dict(target=t_(x["target"]), draft=t_(x["draft"]), tokens=t_(x["tokens"].astype(np.int32)),
+                ua=t_(x["u_accept"]), ur=t_(x["u_resample"]), mask=t_(x["mask"]),
+                gtokens=t_(xg["tokens"].astype(np.int32)))
+    per_set = (base["target"].numel() + base["draft"].numel() + B * K * V) * 2
+    R = max(8, math.ceil(2 * INFINITY_CACHE / per_set))
+    sets = []
+    for _ in range(R):
+        s = {k: v.clone() for k, v in base.items()}
+        s["acc"] = torch.empty(B, dtype=torch.int32, device=dev)
+        s["toks"] = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+        s["rmask"] = torch.empty(B, K, dtype=torch.uint8, device=dev)
+        s["loss"] = torch.empty(2, dtype=torch.float32, device=dev)
+        s["rows"] = torch.empty(B, K, dtype=torch.float32, device=dev)
+        s["grad"] = torch.empty(B, K, V, dtype=torch.bfloat16, device=dev)
+        sets.append(s)
+    stream = torch.cuda.current_stream(dev)
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    vws = torch.zeros(L.osd_verify_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+    dws = torch.zeros(L.osd_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    # Pre-marshalled argument tuples: the timed loops are pure C calls.
+    verify_args = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, B, K, V, P(s["tokens"]), None,
+                    P(s["ua"]), P(s["ur"]), ctypes.c_float(T_VERIFY), P(s["acc"]), P(s["toks"]),
+                    P(s["rmask"]), P(vws), vws.numel(), hs) for s in sets]
+    greedy_args = [(P(s["target"]), None, binding.OSD_BF16, B, K, V, P(s["gtokens"]), None,
+                    None, None, ctypes.c_float(0.0), P(s["acc"]), P(s["toks"]),
+                    P(s["rmask"]), P(vws), vws.numel(), hs) for s in sets]
+
+    def distill_args(kind):
+        return [(P(s["target"]), (K + 1) * V, P(s["draft"]), K * V, binding.OSD_BF16, B, K, V,
+                 P(s["mask"]), kind, ctypes.c_float(BETA), ctypes.c_float(TAU), P(s["loss"]),
+                 P(s["rows"]), P(s["grad"]), P(dws), dws.numel(), hs) for s in sets]
+
+    jsd_args, rkl_args = distill_args(binding.OSD_JSD), distill_args(binding.OSD_RKL)
+    fv, fd = L.osd_verify, L.osd_distill_loss_grad
+
+    def call(f, a):
+        st = f(*a)
+        if st != 0:
+            raise RuntimeError(L.osd_status_string(st).decode())
+
+    def step(r):
+        call(fv, verify_args[r % R])
+        call(fd, jsd_args[r % R])
+
+    def time_loop(fn, iters):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for r in range(iters):
+            fn(r)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters  # ms
+
+    if args.only:
+        loops = {"verify": lambda r: call(fv, verify_args[r % R]),
+                 "greedy": lambda r: call(fv, greedy_args[r % R]),
+                 "jsd": lambda r: call(fd, jsd_args[r % R]),
+                 "rkl": lambda r: call(fd, rkl_args[r % R])}
+        if args.only == "copy":
+            # a plain copy of known size, to calibrate the HBM byte counters
+            src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+            dst = torch.empty_like(src)
+            for _ in range(10):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+            print(json.dumps({"only": "copy", "bytes_read": src.numel(), "bytes_written": dst.numel()}))
+            return
+        fn = loops[args.only]
+        for r in range(args.warmup):
+            fn(r)
+        ms = time_loop(fn, args.kernel_iters)
+        print(json.dumps({"only": args.only, "us_per_launch": ms * 1e3}), flush=True)
+        return
+
+    for r in range(args.warmup):
+        step(r)
+    torch.cuda.synchronize()
+    print(f"# warmup done: {args.warmup} steps, R={R} rotating input sets", file=sys.stderr, flush=True)
+    ms_step = time_loop(step, args.steps)
+    print(f"# timed {args.steps} steps: {ms_step * 1e3:.2f} us/step", file=sys.stderr, flush=True)
+
+    kernels = {}
+    masked = int(x["mask"].sum())
+    for name, f, argl, nbytes in (
+            ("verify", fv, verify_args, verify_bytes(B, K, V)),
+            ("verify_greedy", fv, greedy_args, verify_bytes(B, K, V, greedy=True)),
+            ("distill_jsd", fd, jsd_args, distill_bytes(B, K, V, masked)),
+            ("distill_rkl", fd, rkl_args, distill_bytes(B, K, V, masked))):
+        for r in range(10):
+            call(f, argl[r % R])
+        ms = time_loop(lambda r: call(f, argl[r % R]), args.kernel_iters)
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        kernels[name] = {"us_per_launch": round(ms * 1e3, 3), "algorithmic_bytes": nbytes,
+                         "achieved_GBps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
+        print(f"# {name}: {ms * 1e3:.2f} us/launch, {gbs:.0f} GB/s ({100 * gbs / PEAK_HBM_GBS:.1f}% of peak)",
+              file=sys.stderr, flush=True)
+
+    # The dominant kernel of a step: the one with the longer launch.
+    dom = max(("verify", "distill_jsd"), key=lambda k: kernels[k]["us_per_launch"])
+    kd = kernels[dom]
+    traffic = traffic_from_profiles(dom, kd["algorithmic_bytes"])
+    positions_per_s = B * K / (ms_step * 1e-3)
+    out = {
+        "metric": "verified token positions/sec and achieved HBM GB/s (% of peak) at V=32128 bf16",
+        "value": round(positions_per_s, 1),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; target ~ N(0,2.5^2), draft = 0.7 target + N(0,1.5^2))",
+        "config": {"workload": "T5-vocab verify + JSD distill step", "B": B, "k": K, "V": V,
+                   "logits": "bf16", "T": T_VERIFY, "tau": TAU, "beta": BETA, "mask": "all ones",
+                   "rotating_input_sets": R},
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": kd["achieved_GBps"],
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kd["frac_of_peak"],
+                     "traffic": traffic},
+        "kernels": kernels,
+        "step_GBps": round((kernels["verify"]["algorithmic_bytes"] + kernels["distill_jsd"]["algorithmic_bytes"])
+                           / (ms_step * 1e-3) / 1e9, 1),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * osd.h -- C ABI of the MI355X (gfx950) library for the vocabulary-wide logits
+ * path of online speculative decoding (Liu et al., "Online Speculative
+ * Decoding", ICML 2024, arXiv:2310.07177).
+ *
+ * Two operations:
+ *   osd_verify             speculative-sampling verification of k proposed
+ *                          tokens against the target (Appendix A.1, Eq. 5;
+ *                          Algorithm 1, the verification step);
+ *   osd_distill_loss_grad  the distillation divergence of Eq. 3 (forward KL,
+ *                          reverse KL, JSD[beta]) and its gradient with
+ *                          respect to the draft (student) logits (Section 4.1,
+ *                          Eq. 2-4).
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or synchronises.  Work is enqueued on `stream`
+ *     (a hipStream_t passed as void*; NULL is the default stream) and the call
+ *     returns without waiting for it.
+ *   - Logit arrays are row-major with the vocabulary axis contiguous, in the
+ *     dtype given by `dtype` (OSD_F32: IEEE float; OSD_BF16: bfloat16 bit
+ *     patterns).  Rows whose byte address and length are multiples of 16 take
+ *     the vectorised path; others are accepted and read element by element.
+ *   - Host-checkable mistakes (null required pointer, non-positive sizes,
+ *     K > OSD_MAX_K, V above osd_max_vocab, NaN or out-of-range scalars, an
+ *     unknown enum, a workspace that is too small) return a negative status
+ *     and enqueue nothing.  A failed launch returns OSD_ERR_DEVICE.
+ *   - Workspaces: the caller allocates `*_workspace_bytes(...)` bytes of
+ *     device memory and fills them with zeros ONCE before first use; every
+ *     call leaves its workspace zeroed again when its kernels finish.  Calls
+ *     that may run concurrently need distinct workspaces.
+ *   - Thread-safe: the library holds no mutable global state.
+ */
+#ifndef OSD_H
+#define OSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    OSD_OK = 0,
+    OSD_ERR_INVALID_ARG = -1,
+    OSD_ERR_UNSUPPORTED = -2,
+    OSD_ERR_DEVICE = -3,
+    OSD_ERR_WORKSPACE = -4
+} osd_status;
+
+typedef enum { OSD_F32 = 0, OSD_BF16 = 1 } osd_dtype;
+
+typedef enum { OSD_FKL = 0, OSD_RKL = 1, OSD_JSD = 2 } osd_divergence;
+
+#define OSD_MAX_K 16
+
+/* Largest vocabulary size the row-resident kernels accept for `dtype`
+ * (0 for an unknown dtype). */
+int osd_max_vocab(int dtype);
+
+/* Human-readable name of a status code (static storage). */
+const char* osd_status_string(int status);
+
+/* Workspace needed by osd_verify for B sequences of up to K proposals. */
+size_t osd_verify_workspace_bytes(int B, int K);
+
+/*
+ * osd_verify -- one speculative-decoding verification step for B sequences
+ * (Appendix A.1: with i rising from 1 to k, accept proposal y_i when
+ * u < p(y_i)/q(y_i) and stop at the first rejection; Eq. 5: then draw one
+ * more token from norm(max(0, p - q)) at the rejected position, or from p at
+ * position k+1 when all k were accepted).
+ *
+ * target_logits [B, K+1, V]  row i (0-based) holds the target logits that
+ *                            score proposal i, row k_b is the bonus row
+ * draft_logits  [B, K, V]    row i holds the draft logits proposal i was
+ *                            drawn from; may be NULL when temperature == 0
+ * draft_tokens  [B, K] int32 the proposals y
+ * draft_len     [B] int32    k_b in 1..K (ragged proposals), or NULL for K;
+ *                            rows past k_b are padding and are never read
+ * u_accept      [B, K] fp32  acceptance uniforms in [0,1); NULL iff T == 0
+ * u_resample    [B] fp32     the uniform of the extra token; NULL iff T == 0
+ * temperature   T > 0: logits are divided by T before the softmax (the same T
+ *               for target and draft); T == 0: greedy verification, proposals
+ *               are accepted while they equal the target argmax (lowest index
+ *               on ties) and the extra token is that argmax
+ * accepted_len  out [B] int32      a_b in 0..k_b, or -1 for an invalid row
+ *                                  (k_b outside 1..K, a token outside [0,V),
+ *                                  or a row that is read and has no finite
+ *                                  logit)
+ * out_tokens    out [B, K+1] int32 y_1..y_a, the extra token, then -1
+ * reject_mask   out [B, K] uint8   nullable; 1 at i == a_b when a_b < k_b
+ *                                  (the error index recorded for
+ *                                  distillation), else 0
+ * workspace     osd_verify_workspace_bytes(B, K) zero-initialised bytes
+ *
+ * Decisions are taken in fp32 arithmetic with fp64 scalars; they agree with
+ * an exact computation except where u lies within about 1e-7 of p(y)/q(y) or
+ * u*Z within about 1e-7 (in probability mass) of a CDF edge.
+ */
+int osd_verify(const void* target_logits, const void* draft_logits, int dtype,
+               int B, int K, int V,
+               const int32_t* draft_tokens, const int32_t* draft_len,
+               const float* u_accept, const float* u_resample,
+               float temperature,
+               int32_t* accepted_len, int32_t* out_tokens,
+               uint8_t* reject_mask,
+               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace needed by osd_distill_loss_grad for B*K rows. */
+size_t osd_distill_workspace_bytes(int B, int K);
+
+/*
+ * osd_distill_loss_grad -- masked distillation divergence between teacher
+ * (target) and student (draft) distributions at temperature tau and its
+ * gradient with respect to the student logits (Section 4.1, Eq. 3):
+ *   FKL  KL(p || q)                 gradient (q - p) / tau
+ *   RKL  KL(q || p)                 gradient q (log q - log p - KL(q||p)) / tau
+ *   JSD  beta KL(p || m) + (1-beta) KL(q || m),  m = beta p + (1-beta) q,
+ *                                   gradient (1-beta) q (log q - log m - KL(q||m)) / tau
+ * with p = softmax(teacher / tau), q = softmax(student / tau), 0 log 0 = 0.
+ *
+ * teacher_logits  row (b, i) starts at element b*teacher_batch_stride + i*V
+ *                 (pass (K+1)*V to distil the first K rows of a verify target)
+ * student_logits  row (b, i) starts at element b*student_batch_stride + i*V
+ * mask            [B, K] uint8 0/1, or NULL for all ones
+ * kind            OSD_FKL / OSD_RKL / OSD_JSD;  beta in [0,1] weights the
+ *                 teacher in the JSD mixture;  tau > 0
+ * loss_out        out [2] fp32: {sum(mask*D)/sum(mask) (0 if the mask is
+ *                 empty), sum(mask*D)} (Eq. 2's batch mean and Eq. 4's sum);
+ *                 reduced in a fixed order in fp64, so bitwise deterministic
+ * row_loss_out    out [B, K] fp32, nullable: D per row, 0 where mask is 0
+ * grad_out        out [B, K, V] in `dtype`, contiguous, nullable: the
+ *                 gradient of sum(mask*D); rows with mask 0 are written as 0
+ * workspace       osd_distill_workspace_bytes(B, K) zero-initialised bytes
+ */
+int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stride,
+                          const void* student_logits, int64_t student_batch_stride,
+                          int dtype, int B, int K, int V,
+                          const uint8_t* mask, int kind, float beta, float tau,
+                          float* loss_out, float* row_loss_out, void* grad_out,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OSD_H */

@@ -1,0 +1,189 @@
+"""Thin Python binding of libosd (include/osd.h).
+
+The functions carry the C ABI's names and only marshal arguments: torch
+supplies device memory and the current stream, every computation happens in
+the HIP kernels behind the C ABI.  There is no fallback: if the library or a
+GPU is missing, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libosd.so")
+
+OSD_OK, OSD_ERR_INVALID_ARG, OSD_ERR_UNSUPPORTED, OSD_ERR_DEVICE, OSD_ERR_WORKSPACE = 0, -1, -2, -3, -4
+OSD_F32, OSD_BF16 = 0, 1
+OSD_FKL, OSD_RKL, OSD_JSD = 0, 1, 2
+OSD_MAX_K = 16
+KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
+
+EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify",
+           "osd_distill_workspace_bytes", "osd_distill_loss_grad")
+
+_lib = None
+_lock = threading.Lock()
+
+
+class OsdError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} failed: {lib().osd_status_string(status).decode()}")
+
+
+def lib():
+    """Load libosd.so (built in-tree by paper_2310_07177_amd.build)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                                   "`python -m paper_2310_07177_amd.build`")
+            L = ctypes.CDLL(LIB_PATH)
+            vp, i32, i64, f32, sz = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                     ctypes.c_float, ctypes.c_size_t)
+            L.osd_max_vocab.restype = i32
+            L.osd_max_vocab.argtypes = [i32]
+            L.osd_status_string.restype = ctypes.c_char_p
+            L.osd_status_string.argtypes = [i32]
+            L.osd_verify_workspace_bytes.restype = sz
+            L.osd_verify_workspace_bytes.argtypes = [i32, i32]
+            L.osd_verify.restype = i32
+            L.osd_verify.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32,
+                                     vp, vp, vp, vp, sz, vp]
+            L.osd_distill_workspace_bytes.restype = sz
+            L.osd_distill_workspace_bytes.argtypes = [i32, i32]
+            L.osd_distill_loss_grad.restype = i32
+            L.osd_distill_loss_grad.argtypes = [vp, i64, vp, i64, i32, i32, i32, i32, vp, i32,
+                                                f32, f32, vp, vp, vp, vp, sz, vp]
+            _lib = L
+    return _lib
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return OSD_BF16
+    if t.dtype == torch.float32:
+        return OSD_F32
+    raise TypeError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def _check_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("every tensor argument must live on the GPU")
+
+
+def _stream_handle(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+# Zero-initialised workspaces, one per (device, stream, kind, size): the kernels
+# leave them zeroed, so they are reused across calls on the same stream.
+_workspaces = {}
+
+
+def workspace(kind, nbytes, device):
+    torch = _torch()
+    stream = torch.cuda.current_stream(device).cuda_stream
+    key = (str(device), stream, kind)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
+def osd_max_vocab(dtype_code: int) -> int:
+    return lib().osd_max_vocab(dtype_code)
+
+
+def osd_verify(target_logits, draft_logits, draft_tokens, u_accept, u_resample, temperature,
+               draft_len=None, out=None):
+    """Speculative-sampling verification through the C ABI.
+
+    target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or fp32, on the
+    GPU; draft may be None for temperature 0), draft_tokens [B, K] int32,
+    u_accept [B, K] / u_resample [B] float32 (None for temperature 0),
+    draft_len [B] int32 or None.  Returns (accepted_len [B], out_tokens
+    [B, K+1], reject_mask [B, K]) as new (or the given `out`) GPU tensors."""
+    torch = _torch()
+    B, K1, V = target_logits.shape
+    K = K1 - 1
+    _check_cuda(target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len)
+    dev = target_logits.device
+    for t in (target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if draft_tokens.dtype != torch.int32 or (draft_len is not None and draft_len.dtype != torch.int32):
+        raise TypeError("draft_tokens and draft_len must be int32")
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, K + 1, dtype=torch.int32, device=dev),
+               torch.empty(B, K, dtype=torch.uint8, device=dev))
+    acc, toks, rmask = out
+    L = lib()
+    nbytes = L.osd_verify_workspace_bytes(B, K)
+    ws = workspace("verify", nbytes, dev)
+    st = L.osd_verify(_ptr(target_logits), _ptr(draft_logits), _dtype_code(target_logits), B, K, V,
+                      _ptr(draft_tokens), _ptr(draft_len), _ptr(u_accept), _ptr(u_resample),
+                      float(temperature), _ptr(acc), _ptr(toks), _ptr(rmask), _ptr(ws),
+                      ws.numel(), _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_verify", st)
+    return acc, toks, rmask
+
+
+def osd_distill_loss_grad(teacher_logits, student_logits, kind, beta=0.5, tau=1.0, mask=None,
+                          B=None, K=None, teacher_batch_stride=None, student_batch_stride=None,
+                          grad=True, row_loss=True, out=None):
+    """Masked distillation divergence and gradient through the C ABI.
+
+    By default teacher and student are [B, K, V]; pass B, K and explicit
+    batch strides (elements) to distil the first K rows of a [B, K+1, V]
+    target.  Returns (loss [2] fp32 = {mean, sum}, row_loss [B, K] fp32 or
+    None, grad [B, K, V] or None)."""
+    torch = _torch()
+    _check_cuda(teacher_logits, student_logits, mask)
+    dev = student_logits.device
+    V = student_logits.shape[-1]
+    if B is None:
+        B, K = student_logits.shape[0], student_logits.shape[1]
+    if teacher_batch_stride is None:
+        teacher_batch_stride = teacher_logits.stride(0)
+    if student_batch_stride is None:
+        student_batch_stride = student_logits.stride(0)
+    if teacher_logits.dtype != student_logits.dtype:
+        raise TypeError("teacher and student logits must share a dtype")
+    if mask is not None and (mask.dtype != torch.uint8 or not mask.is_contiguous()):
+        raise TypeError("mask must be a contiguous uint8 tensor")
+    kind_code = KINDS[kind] if isinstance(kind, str) else int(kind)
+    if out is None:
+        out = (torch.empty(2, dtype=torch.float32, device=dev),
+               torch.empty(B, K, dtype=torch.float32, device=dev) if row_loss else None,
+               torch.empty(B, K, V, dtype=student_logits.dtype, device=dev) if grad else None)
+    loss, rows, g = out
+    L = lib()
+    nbytes = L.osd_distill_workspace_bytes(B, K)
+    ws = workspace("distill", nbytes, dev)
+    st = L.osd_distill_loss_grad(_ptr(teacher_logits), int(teacher_batch_stride),
+                                 _ptr(student_logits), int(student_batch_stride),
+                                 _dtype_code(student_logits), B, K, V, _ptr(mask), kind_code,
+                                 float(beta), float(tau), _ptr(loss), _ptr(rows), _ptr(g),
+                                 _ptr(ws), ws.numel(), _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_distill_loss_grad", st)
+    return loss, rows, g

@@ -1,0 +1,387 @@
+// distill.hip -- distillation divergence and its gradient with respect to the
+// student logits on gfx950 (Section 4.1, Eq. 2-4 of arXiv:2310.07177).
+//
+// For each row n = (b, i) with mask 1, with p = softmax(t / tau) (teacher) and
+// q = softmax(s / tau) (student):
+//   FKL  D = sum p (log p - log q)                  g = (q - p) / tau
+//   RKL  D = sum q (log q - log p)                  g = q (log q - log p - D) / tau
+//   JSD  D = beta KL(p || m) + (1-beta) KL(q || m)   g = (1-beta) q (log q - log m - KL(q || m)) / tau
+//        with m = beta p + (1-beta) q
+// and 0 log 0 = 0.  Rows with mask 0 get D = 0 and a zero gradient row.
+//
+// One workgroup per row.  Both rows are read from HBM once, 16 bytes per
+// load, into registers; the row maxima and sums of exponentials are reduced
+// across the workgroup, the divergence terms are accumulated in fp32 per
+// thread and in fp64 across threads, and the gradient is written with 16-byte
+// stores.  The scalar loss is reduced without floating-point atomics: each
+// row stores its D, the last row of every 64-row slab to arrive sums its slab
+// in a fixed order, and the last slab to arrive sums the slabs in a fixed
+// order -- the result is bitwise reproducible.
+#include "osd_device.hpp"
+#include "osd_internal.hpp"
+
+namespace osd {
+namespace {
+
+struct DistillArgs {
+    const void* teacher;
+    int64_t tstride;
+    const void* student;
+    int64_t sstride;
+    int B, K, V;
+    const uint8_t* mask;
+    float beta;
+    float c2;       // log2(e) / tau
+    float inv_tau;  // 1 / tau
+    float* loss_out;
+    float* row_loss_out;
+    void* grad_out;
+    double* row_ws;    // [B*K]
+    double* slab_ws;   // [2*nslabs]: {sum, count} per slab
+    uint32_t* slab_cnt;
+    uint32_t* done_cnt;
+    int nslabs;
+};
+
+template <typename Fmt>
+__device__ inline chunk_t pack_grad(const float (&g)[Fmt::kPerChunk]) {
+    if constexpr (Fmt::kPerChunk == 8) {
+        return chunk_t{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]),
+                       pack_bf16x2(g[4], g[5]), pack_bf16x2(g[6], g[7])};
+    } else {
+        return chunk_t{__float_as_uint(g[0]), __float_as_uint(g[1]),
+                       __float_as_uint(g[2]), __float_as_uint(g[3])};
+    }
+}
+
+template <typename Fmt, int W, int CPT, bool VEC>
+__device__ inline void store_grad_chunk(void* row, int n, const chunk_t& c, int V) {
+    const int nchunks = (V + Fmt::kPerChunk - 1) / Fmt::kPerChunk;
+    const int ch = n * W + static_cast<int>(threadIdx.x);
+    if (ch >= nchunks) return;
+    if constexpr (VEC) {
+        __builtin_nontemporal_store(c, static_cast<chunk_t*>(row) + ch);
+    } else {
+        const int64_t first = int64_t(ch) * Fmt::kPerChunk;
+        if constexpr (Fmt::kPerChunk == 8) {
+            uint16_t* p = static_cast<uint16_t*>(row);
+            const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (first + e < V) p[first + e] = uint16_t((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+        } else {
+            uint32_t* p = static_cast<uint32_t*>(row);
+            const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (first + e < V) p[first + e] = w[e];
+        }
+    }
+}
+
+// Wave-wide fp64 sum with a fixed butterfly: every lane ends with the same,
+// run-to-run reproducible value.
+__device__ inline double wave_sum_fixed(double v) { return wave_sum(v); }
+
+// Executed by all lanes of wave 0: record D for row n and fold it into the
+// masked sum once every row of its slab (and then every slab) has arrived.
+__device__ void reduce_loss(const DistillArgs& a, int n, double D) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int rows = a.B * a.K;
+    const int slab = n / kSlabRows;
+    const int first = slab * kSlabRows;
+    const int in_slab = min(kSlabRows, rows - first);
+    uint32_t prev = 0;
+    if (lane == 0) {
+        store_relaxed(&a.row_ws[n], D);
+        prev = arrive(&a.slab_cnt[slab]);
+    }
+    prev = __shfl(prev, 0, kWave);
+    if (prev != uint32_t(in_slab - 1)) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    double v = 0.0, c = 0.0;
+    if (lane < in_slab) {
+        v = load_relaxed(&a.row_ws[first + lane]);
+        c = (a.mask == nullptr || a.mask[first + lane] != 0) ? 1.0 : 0.0;
+        store_relaxed(&a.row_ws[first + lane], 0.0);  // leave the workspace zeroed
+    }
+    const double slab_sum = wave_sum_fixed(v);
+    const double slab_cnt = wave_sum_fixed(c);
+    if (lane == 0) {
+        store_relaxed(&a.slab_ws[2 * slab], slab_sum);
+        store_relaxed(&a.slab_ws[2 * slab + 1], slab_cnt);
+        store_relaxed(&a.slab_cnt[slab], 0u);
+        prev = arrive(a.done_cnt);
+    }
+    prev = __shfl(prev, 0, kWave);
+    if (prev != uint32_t(a.nslabs - 1)) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    double ts = 0.0, tc = 0.0;
+    for (int s = lane; s < a.nslabs; s += kWave) {
+        ts += load_relaxed(&a.slab_ws[2 * s]);
+        tc += load_relaxed(&a.slab_ws[2 * s + 1]);
+        store_relaxed(&a.slab_ws[2 * s], 0.0);
+        store_relaxed(&a.slab_ws[2 * s + 1], 0.0);
+    }
+    ts = wave_sum_fixed(ts);
+    tc = wave_sum_fixed(tc);
+    if (lane == 0) {
+        a.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
+        a.loss_out[1] = float(ts);
+        store_relaxed(a.done_cnt, 0u);
+    }
+}
+
+template <typename Fmt, int W, int CPT, bool VEC, int KIND>
+__global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
+    constexpr int NW = W / kWave;
+    constexpr int EPC = Fmt::kPerChunk;
+    __shared__ float s_max[2][NW];
+    __shared__ double s_sum[2][NW];
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int K = a.K, V = a.V;
+    const int n = blockIdx.x;
+    const int b = n / K, i = n - b * K;
+    const bool on = a.mask == nullptr || a.mask[n] != 0;
+    void* grow = a.grad_out ? static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes : nullptr;
+    double D = 0.0;
+
+    if (!on) {
+        if (grow) {
+#pragma unroll
+            for (int c = 0; c < CPT; ++c)
+                store_grad_chunk<Fmt, W, CPT, VEC>(grow, c, chunk_t{0u, 0u, 0u, 0u}, V);
+        }
+    } else {
+        const char* trow = static_cast<const char*>(a.teacher) +
+                           (int64_t(b) * a.tstride + int64_t(i) * V) * Fmt::kBytes;
+        const char* srow = static_cast<const char*>(a.student) +
+                           (int64_t(b) * a.sstride + int64_t(i) * V) * Fmt::kBytes;
+        chunk_t tv[CPT], sv[CPT];
+        load_row<Fmt, W, CPT, VEC>(tv, trow, V);
+        load_row<Fmt, W, CPT, VEC>(sv, srow, V);
+        const float c2 = a.c2;
+
+        // Row maxima.
+        float mt = kNegInf, ms = kNegInf;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                mt = fmaxf(mt, Fmt::get(tv[c], e));
+                ms = fmaxf(ms, Fmt::get(sv[c], e));
+            }
+        mt = wave_max(mt);
+        ms = wave_max(ms);
+        if (lane == 0) {
+            s_max[0][wid] = mt;
+            s_max[1][wid] = ms;
+        }
+        __syncthreads();
+        mt = s_max[0][0];
+        ms = s_max[1][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            mt = fmaxf(mt, s_max[0][w]);
+            ms = fmaxf(ms, s_max[1][w]);
+        }
+
+        // Sums of exponentials, pairwise within a chunk.
+        opaque(tv);
+        opaque(sv);
+        float st = 0.0f, ss = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            float et[EPC], es[EPC];
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                et[e] = exp2_fast((Fmt::get(tv[c], e) - mt) * c2);
+                es[e] = exp2_fast((Fmt::get(sv[c], e) - ms) * c2);
+            }
+#pragma unroll
+            for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+                for (int e = 0; e < EPC; e += 2 * w) {
+                    et[e] = et[e] + et[e + w];
+                    es[e] = es[e] + es[e + w];
+                }
+            st = st + et[0];
+            ss = ss + es[0];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        {
+            const double dt = wave_sum(double(st));
+            const double ds = wave_sum(double(ss));
+            if (lane == 0) {
+                s_sum[0][wid] = dt;
+                s_sum[1][wid] = ds;
+            }
+        }
+        __syncthreads();
+        double St = 0.0, Ss = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            St += s_sum[0][w];
+            Ss += s_sum[1][w];
+        }
+        // log2 p_j = (t_j - m_t) c2 - log2 S_t, p_j = 2^((t_j - m_t) c2) / S_t.
+        const float l2t = float(log2(St)), l2s = float(log2(Ss));
+        const float inv_st = float(1.0 / St), inv_ss = float(1.0 / Ss);
+        const float beta = a.beta, omb = 1.0f - a.beta;
+        const float ln2 = float(kLn2);
+        const float inv_tau = a.inv_tau;
+
+        // Divergence terms.
+        float mt_c = mt, ms_c = ms;
+        asm volatile("" : "+v"(mt_c), "+v"(ms_c));
+        opaque(tv);
+        opaque(sv);
+        float acc0 = 0.0f, acc1 = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            float c0 = 0.0f, c1 = 0.0f;
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const float at = (Fmt::get(tv[c], e) - mt_c) * c2;
+                const float as = (Fmt::get(sv[c], e) - ms_c) * c2;
+                const float p = exp2_fast(at) * inv_st;
+                const float q = exp2_fast(as) * inv_ss;
+                const float lp = at - l2t, lq = as - l2s;
+                if constexpr (KIND == 0) {
+                    c0 = c0 + (p > 0.0f ? p * (lp - lq) : 0.0f);
+                } else if constexpr (KIND == 1) {
+                    c0 = c0 + (q > 0.0f ? q * (lq - lp) : 0.0f);
+                } else {
+                    const float lm = log2_fast(beta * p + omb * q);
+                    c0 = c0 + (p > 0.0f ? p * (lp - lm) : 0.0f);
+                    c1 = c1 + (q > 0.0f ? q * (lq - lm) : 0.0f);
+                }
+                if ((e & 1) == 1) __builtin_amdgcn_sched_barrier(0);  // 2 elements in flight
+            }
+            acc0 = acc0 + c0;
+            acc1 = acc1 + c1;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        {
+            const double d0 = wave_sum(double(acc0));
+            const double d1 = wave_sum(double(acc1));
+            __syncthreads();  // s_sum is reused
+            if (lane == 0) {
+                s_sum[0][wid] = d0;
+                s_sum[1][wid] = d1;
+            }
+        }
+        __syncthreads();
+        double A0 = 0.0, A1 = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            A0 += s_sum[0][w];
+            A1 += s_sum[1][w];
+        }
+        // Terms were accumulated in log2 units.
+        if constexpr (KIND == 2)
+            D = kLn2 * (double(a.beta) * A0 + (1.0 - double(a.beta)) * A1);
+        else
+            D = kLn2 * A0;
+
+        if (grow) {
+            // FKL: g = (q - p) / tau;  RKL: g = q (ln q - ln p - D) / tau;
+            // JSD: g = (1-beta) q (ln q - ln m - KL(q||m)) / tau.
+            const float shift = KIND == 1 ? float(D) : float(kLn2 * A1);
+            const float scale = (KIND == 2 ? omb : 1.0f) * inv_tau;
+            float mt_g = mt, ms_g = ms;
+            asm volatile("" : "+v"(mt_g), "+v"(ms_g));
+            opaque(tv);
+            opaque(sv);
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) {
+                float g[EPC];
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const float at = (Fmt::get(tv[c], e) - mt_g) * c2;
+                    const float as = (Fmt::get(sv[c], e) - ms_g) * c2;
+                    const float q = exp2_fast(as) * inv_ss;
+                    if constexpr (KIND == 0) {
+                        const float p = exp2_fast(at) * inv_st;
+                        g[e] = (q - p) * scale;
+                    } else {
+                        const float lq = as - l2s;
+                        float lr;
+                        if constexpr (KIND == 1) {
+                            lr = lq - (at - l2t);
+                        } else {
+                            const float p = exp2_fast(at) * inv_st;
+                            lr = lq - log2_fast(beta * p + omb * q);
+                        }
+                        g[e] = q > 0.0f ? q * (lr * ln2 - shift) * scale : 0.0f;
+                    }
+                    if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+                }
+                store_grad_chunk<Fmt, W, CPT, VEC>(grow, c, pack_grad<Fmt>(g), V);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+
+    if (a.row_loss_out && tid == 0) a.row_loss_out[n] = float(D);
+    if (wid == 0) reduce_loss(a, n, D);
+}
+
+template <typename Fmt, int W, int CPT, bool VEC>
+hipError_t launch_kind(const DistillLaunch& L, const DistillArgs& a) {
+    const dim3 grid(unsigned(L.B) * unsigned(L.K)), block(W);
+    switch (L.kind) {
+        case 0: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 0>), grid, block, 0, L.stream, a); break;
+        case 1: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 1>), grid, block, 0, L.stream, a); break;
+        default: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 2>), grid, block, 0, L.stream, a); break;
+    }
+    return hipGetLastError();
+}
+
+template <typename Fmt, int W, int CPT>
+hipError_t launch_tile(const DistillLaunch& L, const DistillArgs& a) {
+    return L.vec ? launch_kind<Fmt, W, CPT, true>(L, a) : launch_kind<Fmt, W, CPT, false>(L, a);
+}
+
+template <typename Fmt>
+hipError_t launch_fmt(const DistillLaunch& L, const DistillArgs& a) {
+    RowTile t;
+    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    switch (t.W * 100 + t.CPT) {
+        case 25601: return launch_tile<Fmt, 256, 1>(L, a);
+        case 25602: return launch_tile<Fmt, 256, 2>(L, a);
+        case 25604: return launch_tile<Fmt, 256, 4>(L, a);
+        case 51204: return launch_tile<Fmt, 512, 4>(L, a);
+        case 51208: return launch_tile<Fmt, 512, 8>(L, a);
+        case 102408: return launch_tile<Fmt, 1024, 8>(L, a);
+        case 102416: return launch_tile<Fmt, 1024, 16>(L, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_distill(const DistillLaunch& L) {
+    DistillArgs a;
+    a.teacher = L.teacher;
+    a.tstride = L.teacher_stride;
+    a.student = L.student;
+    a.sstride = L.student_stride;
+    a.B = L.B;
+    a.K = L.K;
+    a.V = L.V;
+    a.mask = L.mask;
+    a.beta = L.beta;
+    a.c2 = float(1.4426950408889634 / double(L.tau));
+    a.inv_tau = float(1.0 / double(L.tau));
+    a.loss_out = L.loss_out;
+    a.row_loss_out = L.row_loss_out;
+    a.grad_out = L.grad_out;
+    a.row_ws = L.row_loss_ws;
+    a.slab_ws = L.slab_ws;
+    a.slab_cnt = L.slab_counters;
+    a.done_cnt = L.done_counter;
+    a.nslabs = (L.B * L.K + kSlabRows - 1) / kSlabRows;
+    return L.dtype == 1 ? launch_fmt<BF16>(L, a) : launch_fmt<F32>(L, a);
+}
+
+}  // namespace osd

@@ -1,0 +1,177 @@
+// osd_api.hip -- the C ABI of libosd (declared in include/osd.h): argument
+// validation, workspace carving and kernel dispatch.  No allocation, no
+// synchronisation, no global mutable state.
+#include <math.h>
+
+#include "osd.h"
+#include "osd_internal.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int per_chunk(int dtype) { return dtype == OSD_BF16 ? 8 : (dtype == OSD_F32 ? 4 : 0); }
+int elem_bytes(int dtype) { return dtype == OSD_BF16 ? 2 : 4; }
+
+struct VerifyWs {
+    size_t records, counters, total;
+};
+VerifyWs verify_layout(int B, int K) {
+    VerifyWs w;
+    w.counters = 0;
+    w.records = round_up(size_t(B) * 4, kAlign);
+    w.total = w.records + round_up(size_t(B) * size_t(K + 1) * 4, kAlign);
+    return w;
+}
+
+struct DistillWs {
+    size_t done, slab_cnt, slabs, rows, total;
+    int nslabs;
+};
+// Counters first, at offsets that do not depend on B*K beyond their own
+// count, then the fp64 partial sums; the kernels leave every byte zero.
+DistillWs distill_layout(int B, int K) {
+    DistillWs w;
+    const size_t R = size_t(B) * size_t(K);
+    w.nslabs = int((R + osd::kSlabRows - 1) / osd::kSlabRows);
+    w.done = 0;
+    w.slab_cnt = 16;
+    w.slabs = round_up(w.slab_cnt + size_t(w.nslabs) * 4, kAlign);
+    w.rows = w.slabs + round_up(size_t(w.nslabs) * 16, kAlign);
+    w.total = w.rows + round_up(R * 8, kAlign);
+    return w;
+}
+
+bool sizes_ok(int B, int K, int V, int dtype) {
+    if (B <= 0 || K <= 0 || V <= 0 || K > OSD_MAX_K) return false;
+    if (per_chunk(dtype) == 0) return false;
+    if (V > osd::max_vocab_for(per_chunk(dtype))) return false;
+    // grid.x = B * (K + 1) must fit in 31 bits
+    if (int64_t(B) * int64_t(K + 1) > 0x7FFFFFFFll) return false;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int osd_max_vocab(int dtype) {
+    return per_chunk(dtype) ? osd::max_vocab_for(per_chunk(dtype)) : 0;
+}
+
+const char* osd_status_string(int status) {
+    switch (status) {
+        case OSD_OK: return "OSD_OK";
+        case OSD_ERR_INVALID_ARG: return "OSD_ERR_INVALID_ARG: an argument is out of range or a required pointer is NULL";
+        case OSD_ERR_UNSUPPORTED: return "OSD_ERR_UNSUPPORTED: the vocabulary size or dtype is not supported";
+        case OSD_ERR_DEVICE: return "OSD_ERR_DEVICE: the HIP runtime failed to launch a kernel";
+        case OSD_ERR_WORKSPACE: return "OSD_ERR_WORKSPACE: the workspace is NULL or smaller than required";
+        default: return "unknown osd status";
+    }
+}
+
+size_t osd_verify_workspace_bytes(int B, int K) {
+    if (B <= 0 || K <= 0 || K > OSD_MAX_K) return 0;
+    return verify_layout(B, K).total;
+}
+
+int osd_verify(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
+               int V, const int32_t* draft_tokens, const int32_t* draft_len,
+               const float* u_accept, const float* u_resample, float temperature,
+               int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+               void* workspace, size_t workspace_bytes, void* stream) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || K <= 0 || V <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
+    if (!sizes_ok(B, K, V, dtype)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    const bool greedy = temperature == 0.0f;
+    if (!target_logits || !draft_tokens || !accepted_len || !out_tokens) return OSD_ERR_INVALID_ARG;
+    if (!greedy && (!draft_logits || !u_accept || !u_resample)) return OSD_ERR_INVALID_ARG;
+    const VerifyWs ws = verify_layout(B, K);
+    if (!workspace || workspace_bytes < ws.total || (reinterpret_cast<uintptr_t>(workspace) & 15u))
+        return OSD_ERR_WORKSPACE;
+
+    osd::VerifyLaunch L;
+    L.target = target_logits;
+    L.draft = greedy ? nullptr : draft_logits;
+    L.dtype = dtype;
+    L.B = B;
+    L.K = K;
+    L.V = V;
+    L.tokens = draft_tokens;
+    L.draft_len = draft_len;
+    L.u_accept = u_accept;
+    L.u_resample = u_resample;
+    L.temperature = temperature;
+    L.accepted_len = accepted_len;
+    L.out_tokens = out_tokens;
+    L.reject_mask = reject_mask;
+    char* w = static_cast<char*>(workspace);
+    L.records = reinterpret_cast<uint32_t*>(w + ws.records);
+    L.counters = reinterpret_cast<uint32_t*>(w + ws.counters);
+    L.vec = (int64_t(V) * elem_bytes(dtype)) % 16 == 0 && aligned16(target_logits) &&
+            (greedy || aligned16(draft_logits));
+    L.stream = static_cast<hipStream_t>(stream);
+    return osd::launch_verify(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+size_t osd_distill_workspace_bytes(int B, int K) {
+    if (B <= 0 || K <= 0) return 0;
+    if (int64_t(B) * int64_t(K) > 0x7FFFFFFFll) return 0;
+    return distill_layout(B, K).total;
+}
+
+int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stride,
+                          const void* student_logits, int64_t student_batch_stride, int dtype,
+                          int B, int K, int V, const uint8_t* mask, int kind, float beta,
+                          float tau, float* loss_out, float* row_loss_out, void* grad_out,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || K <= 0 || V <= 0) return OSD_ERR_INVALID_ARG;
+    if (int64_t(B) * int64_t(K) > 0x7FFFFFFFll) return OSD_ERR_INVALID_ARG;
+    if (per_chunk(dtype) == 0 || V > osd::max_vocab_for(per_chunk(dtype))) return OSD_ERR_UNSUPPORTED;
+    if (kind != OSD_FKL && kind != OSD_RKL && kind != OSD_JSD) return OSD_ERR_INVALID_ARG;
+    if (!(tau > 0.0f) || isinf(tau)) return OSD_ERR_INVALID_ARG;
+    if (!(beta >= 0.0f && beta <= 1.0f)) return OSD_ERR_INVALID_ARG;
+    if (!teacher_logits || !student_logits || !loss_out) return OSD_ERR_INVALID_ARG;
+    // The K rows of one sequence must not overlap those of the next.
+    if (B > 1 && (teacher_batch_stride < int64_t(K) * V || student_batch_stride < int64_t(K) * V))
+        return OSD_ERR_INVALID_ARG;
+    const DistillWs ws = distill_layout(B, K);
+    if (!workspace || workspace_bytes < ws.total || (reinterpret_cast<uintptr_t>(workspace) & 15u))
+        return OSD_ERR_WORKSPACE;
+
+    osd::DistillLaunch L;
+    L.teacher = teacher_logits;
+    L.teacher_stride = teacher_batch_stride;
+    L.student = student_logits;
+    L.student_stride = student_batch_stride;
+    L.dtype = dtype;
+    L.B = B;
+    L.K = K;
+    L.V = V;
+    L.mask = mask;
+    L.kind = kind;
+    L.beta = beta;
+    L.tau = tau;
+    L.loss_out = loss_out;
+    L.row_loss_out = row_loss_out;
+    L.grad_out = grad_out;
+    char* w = static_cast<char*>(workspace);
+    L.row_loss_ws = reinterpret_cast<double*>(w + ws.rows);
+    L.slab_ws = reinterpret_cast<double*>(w + ws.slabs);
+    L.slab_counters = reinterpret_cast<uint32_t*>(w + ws.slab_cnt);
+    L.done_counter = reinterpret_cast<uint32_t*>(w + ws.done);
+    const int eb = elem_bytes(dtype);
+    L.vec = (int64_t(V) * eb) % 16 == 0 && (teacher_batch_stride * eb) % 16 == 0 &&
+            (student_batch_stride * eb) % 16 == 0 && aligned16(teacher_logits) &&
+            aligned16(student_logits) && (grad_out == nullptr || aligned16(grad_out));
+    L.stream = static_cast<hipStream_t>(stream);
+    return osd::launch_distill(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+}  // extern "C"

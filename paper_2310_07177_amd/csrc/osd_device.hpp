@@ -1,0 +1,216 @@
+// osd_device.hpp -- device-side building blocks shared by the verification and
+// distillation kernels (gfx950, wave64).
+//
+// Rows are read as 16-byte chunks (8 bf16 or 4 fp32 logits).  A workgroup of W
+// threads holds a row in registers as CPT chunks per thread: chunk n*W + tid
+// for round n, so each round is one fully coalesced sweep over W*16 bytes and
+// token ids grow with (round, thread, element).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace osd {
+
+constexpr int kWave = 64;
+
+// One 16-byte chunk of a row (a native vector so that loads stay dwordx4).
+typedef uint32_t chunk_t __attribute__((ext_vector_type(4)));
+constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr double kLn2 = 0.69314718055994530942;
+
+// ---------------------------------------------------------------------------
+// Logit formats
+// ---------------------------------------------------------------------------
+struct BF16 {
+    static constexpr int kPerChunk = 8;
+    static constexpr int kBytes = 2;
+    // One padding element: -inf has zero probability and never wins a max.
+    static constexpr uint16_t kPad = 0xFF80u;
+    __device__ static inline float get(const chunk_t& c, int e) {
+        const uint32_t w = (e >> 1) == 0 ? c.x : (e >> 1) == 1 ? c.y : (e >> 1) == 2 ? c.z : c.w;
+        return (e & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+    }
+    __device__ static inline float load_one(const void* row, int j) {
+        return __uint_as_float(uint32_t(static_cast<const uint16_t*>(row)[j]) << 16);
+    }
+    __device__ static inline chunk_t load_scalar(const void* row, int64_t first, int V) {
+        const uint16_t* p = static_cast<const uint16_t*>(row);
+        uint16_t v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (first + e < V) ? p[first + e] : kPad;
+        chunk_t c;
+        c.x = v[0] | (uint32_t(v[1]) << 16);
+        c.y = v[2] | (uint32_t(v[3]) << 16);
+        c.z = v[4] | (uint32_t(v[5]) << 16);
+        c.w = v[6] | (uint32_t(v[7]) << 16);
+        return c;
+    }
+};
+
+struct F32 {
+    static constexpr int kPerChunk = 4;
+    static constexpr int kBytes = 4;
+    __device__ static inline float get(const chunk_t& c, int e) {
+        const uint32_t w = e == 0 ? c.x : e == 1 ? c.y : e == 2 ? c.z : c.w;
+        return __uint_as_float(w);
+    }
+    __device__ static inline float load_one(const void* row, int j) {
+        return static_cast<const float*>(row)[j];
+    }
+    __device__ static inline chunk_t load_scalar(const void* row, int64_t first, int V) {
+        const float* p = static_cast<const float*>(row);
+        uint32_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = (first + e < V) ? __float_as_uint(p[first + e]) : 0xFF800000u;
+        return chunk_t{v[0], v[1], v[2], v[3]};
+    }
+};
+
+// Whole chunk of padding (past the end of the row).
+template <typename Fmt>
+__device__ inline chunk_t pad_chunk() {
+    if constexpr (Fmt::kPerChunk == 8)
+        return chunk_t{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
+    else
+        return chunk_t{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u};
+}
+
+// Load the CPT chunks of one row owned by this thread.  VEC: the row is
+// 16-byte aligned and V is a multiple of the chunk size.
+template <typename Fmt, int W, int CPT, bool VEC>
+__device__ inline void load_row(chunk_t (&c)[CPT], const void* row, int V) {
+    const int nchunks = (V + Fmt::kPerChunk - 1) / Fmt::kPerChunk;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const int ch = n * W + static_cast<int>(threadIdx.x);
+        if (ch < nchunks) {
+            if constexpr (VEC)
+                c[n] = __builtin_nontemporal_load(static_cast<const chunk_t*>(row) + ch);
+            else
+                c[n] = Fmt::load_scalar(row, int64_t(ch) * Fmt::kPerChunk, V);
+        } else {
+            c[n] = pad_chunk<Fmt>();
+        }
+    }
+}
+
+// Make register-resident chunks opaque to the optimiser at the start of a
+// sweep.  Unpacking a bf16 pair costs one instruction; without this the
+// compiler keeps every unpacked value of an earlier sweep alive to reuse it,
+// which doubles the register footprint of a row and spills.
+template <int CPT>
+__device__ inline void opaque(chunk_t (&c)[CPT]) {
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) asm volatile("" : "+v"(c[n]));
+}
+
+// ---------------------------------------------------------------------------
+// Wave64 reductions (lane order fixed, so results are deterministic)
+// ---------------------------------------------------------------------------
+__device__ inline float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ inline uint64_t wave_sum(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        v += static_cast<uint64_t>(__shfl_xor(static_cast<unsigned long long>(v), o, kWave));
+    return v;
+}
+
+__device__ inline uint64_t wave_inclusive_scan(uint64_t v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint64_t t = static_cast<uint64_t>(__shfl_up(static_cast<unsigned long long>(v), o, kWave));
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+// Max value, lowest index among equal maxima.
+__device__ inline void wave_argmax(float& v, int& idx) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(v, o, kWave);
+        const int oi = __shfl_xor(idx, o, kWave);
+        if (ov > v || (ov == v && oi < idx)) {
+            v = ov;
+            idx = oi;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fixed-point probability mass.  A non-negative fp32 value x < 2 maps to
+// floor(x * 2^62) exactly for x >= 2^-39 (the mantissa is shifted, not
+// rounded); integer sums of such values are associative, so every reduction
+// order partitions a CDF identically.
+// ---------------------------------------------------------------------------
+__device__ inline uint64_t mass_to_fixed(float x) {
+    const uint32_t b = __float_as_uint(x);
+    const int e = int((b >> 23) & 0xFF) - 127;
+    if (e < -126 || (b >> 31)) return 0;  // zero, subnormal or negative
+    const uint64_t m = uint64_t((b & 0x7FFFFFu) | 0x800000u);
+    const int sh = e + 39;  // x * 2^62 = m * 2^(e - 23 + 62)
+    if (sh >= 0) return m << sh;
+    if (sh <= -64) return 0;
+    return m >> (-sh);
+}
+
+// ---------------------------------------------------------------------------
+// Exponentials.  v_exp_f32 computes 2^x; scaled logits are formed as
+// (x - max) * log2(e)/T so that the term carrying the mass is exact-ish.
+// ---------------------------------------------------------------------------
+__device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ inline float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
+
+// fp32 -> bf16 bit pattern, round to nearest even (NaN stays NaN).
+__device__ inline uint32_t f32_to_bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ---------------------------------------------------------------------------
+// Cross-workgroup hand-off through device memory: relaxed agent-scope atomics
+// for the payload, an acquire-release add on the arrival counter.
+// ---------------------------------------------------------------------------
+__device__ inline void store_relaxed(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint32_t load_relaxed(const uint32_t* p) {
+    return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void store_relaxed(double* p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline double load_relaxed(const double* p) {
+    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint32_t arrive(uint32_t* counter) {
+    return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace osd

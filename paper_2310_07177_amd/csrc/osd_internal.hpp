@@ -1,0 +1,68 @@
+// osd_internal.hpp -- host-side launch interface between the C ABI layer and
+// the kernel translation units.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace osd {
+
+// Kernel tile shape chosen from V: W threads per workgroup, CPT 16-byte chunks
+// per thread per row.
+struct RowTile {
+    int W;
+    int CPT;
+};
+
+struct VerifyLaunch {
+    const void* target;
+    const void* draft;
+    int dtype;  // 0 fp32, 1 bf16
+    int B, K, V;
+    const int32_t* tokens;
+    const int32_t* draft_len;
+    const float* u_accept;
+    const float* u_resample;
+    float temperature;
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    uint32_t* records;   // [B*(K+1)] zero on entry and exit
+    uint32_t* counters;  // [B]       zero on entry and exit
+    bool vec;            // rows 16-byte aligned
+    hipStream_t stream;
+};
+
+struct DistillLaunch {
+    const void* teacher;
+    int64_t teacher_stride;
+    const void* student;
+    int64_t student_stride;
+    int dtype;
+    int B, K, V;
+    const uint8_t* mask;
+    int kind;
+    float beta, tau;
+    float* loss_out;
+    float* row_loss_out;
+    void* grad_out;
+    double* row_loss_ws;       // [B*K]
+    double* slab_ws;           // [nslabs]
+    uint32_t* slab_counters;   // [nslabs] zero on entry and exit
+    uint32_t* done_counter;    // [1]      zero on entry and exit
+    bool vec;
+    hipStream_t stream;
+};
+
+constexpr int kSlabRows = 64;
+
+// Largest V handled by the row-resident tiles for a chunk of `per_chunk`
+// elements.
+int max_vocab_for(int per_chunk);
+bool pick_tile(int V, int per_chunk, RowTile* t);
+
+hipError_t launch_verify(const VerifyLaunch& L);
+hipError_t launch_distill(const DistillLaunch& L);
+
+}  // namespace osd

@@ -1,0 +1,536 @@
+// verify.hip -- speculative-sampling verification on gfx950.
+//
+// Method (Appendix A.1 and Eq. 5 of arXiv:2310.07177; Algorithm 1, the step
+// that determines the accepted count and samples one more token): proposals
+// y_1..y_k are tested in order, y_i is accepted when u_i < p(y_i)/q(y_i), the
+// first rejection at position a ends the test, and one extra token is drawn
+// from norm(max(0, p - q)) at row a, or from p at the bonus row when all k
+// were accepted.  p and q are temperature softmaxes of the logits.
+//
+// Layout of the work: one workgroup per (sequence b, row i), rows 0..k_b;
+// workgroups are numbered position-major so that earlier positions dispatch
+// first.  A workgroup reads its target row (and draft row for i < k_b) from
+// HBM exactly once into registers, reduces the row maximum and the sum of
+// exponentials, decides acceptance, and -- when its own position rejects and
+// no earlier position of the sequence is known to have rejected -- draws the
+// correction token from the row it already holds.  The bonus workgroup draws
+// from p.  Each workgroup publishes a one-word record; the last of the k_b + 1
+// workgroups of a sequence to arrive selects the first rejection, writes the
+// outputs and clears the records and the arrival counter for the next call.
+#include "osd_device.hpp"
+#include "osd_internal.hpp"
+
+namespace osd {
+namespace {
+
+// Record word: state in bits 31..29, token in bits 28..0.
+enum : uint32_t {
+    kRecEmpty = 0,
+    kRecAccept = 1,
+    kRecReject = 2,         // rejected, correction token attached
+    kRecRejectSkipped = 3,  // rejected after an earlier rejection was seen
+    kRecBadRow = 4,         // no finite logit in a row that was read
+    kRecBadToken = 5,       // proposal outside [0, V)
+    kRecBonus = 6,          // bonus token attached
+    kRecBonusSkipped = 7,   // an earlier rejection was seen
+};
+
+__device__ inline uint32_t make_rec(uint32_t state, uint32_t tok) {
+    return (state << 29) | (tok & 0x1FFFFFFFu);
+}
+__device__ inline uint32_t rec_state(uint32_t r) { return r >> 29; }
+__device__ inline int rec_token(uint32_t r) { return int(r & 0x1FFFFFFFu); }
+
+struct VerifyArgs {
+    const void* target;
+    const void* draft;
+    int B, K, V;
+    const int32_t* tokens;
+    const int32_t* draft_len;
+    const float* u_accept;
+    const float* u_resample;
+    float c2;       // log2(e) / T
+    double inv_T;   // 1 / T in fp64 for the acceptance test
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    uint32_t* records;
+    uint32_t* counters;
+};
+
+__device__ void write_invalid(const VerifyArgs& a, int b) {
+    const int K = a.K;
+    for (int j = threadIdx.x; j <= K; j += blockDim.x) {
+        a.out_tokens[int64_t(b) * (K + 1) + j] = -1;
+        if (a.reject_mask && j < K) a.reject_mask[int64_t(b) * K + j] = 0;
+    }
+    if (threadIdx.x == 0) a.accepted_len[b] = -1;
+}
+
+// Executed by all 64 lanes of one wave with the same `record`: publish this
+// row's record, and if it is the last of the k_b + 1 rows of sequence b to
+// arrive, emit the outputs.  Lane j handles position j (K < 64).
+__device__ void publish(const VerifyArgs& a, int b, int i, int kb, uint32_t record) {
+    const int K = a.K;
+    const int lane = threadIdx.x & (kWave - 1);
+    uint32_t* recs = a.records + int64_t(b) * (K + 1);
+    uint32_t prev = 0;
+    if (lane == 0) {
+        store_relaxed(&recs[i], record);
+        prev = arrive(&a.counters[b]);
+    }
+    prev = __shfl(prev, 0, kWave);
+    if (prev != uint32_t(kb)) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+    // First rejection (Appendix A.1: the test stops there).  A proposal
+    // outside the vocabulary invalidates the sequence wherever it sits; a row
+    // without finite logits only if the test reaches it.
+    const uint32_t r = lane <= kb ? load_relaxed(&recs[lane]) : 0u;
+    const uint32_t s = rec_state(r);
+    const bool bad_token = __ballot(lane < kb && s == kRecBadToken) != 0;
+    const uint64_t stop = __ballot(lane < kb && s != kRecAccept);
+    int acc = kb;
+    if (stop) acc = __builtin_ctzll(stop);
+    const uint32_t ra = __shfl(r, acc, kWave);
+    bool bad = bad_token;
+    int extra = -1;
+    if (!bad) {
+        const uint32_t sa = rec_state(ra);
+        if (acc < kb ? sa == kRecReject : sa == kRecBonus)
+            extra = rec_token(ra);
+        else
+            bad = true;  // a row without finite logits, or an inconsistency
+    }
+    const int32_t* y = a.tokens + int64_t(b) * K;
+    if (lane <= K) {
+        int32_t o = -1;
+        if (!bad) o = lane < acc ? y[lane] : (lane == acc ? extra : -1);
+        a.out_tokens[int64_t(b) * (K + 1) + lane] = o;
+        if (a.reject_mask && lane < K)
+            a.reject_mask[int64_t(b) * K + lane] = (!bad && lane == acc && acc < kb) ? 1 : 0;
+    }
+    if (lane == 0) a.accepted_len[b] = bad ? -1 : acc;
+    if (lane <= kb) store_relaxed(&recs[lane], 0u);
+    if (lane == 0) store_relaxed(&a.counters[b], 0u);
+}
+
+// Has an earlier position of this sequence already been seen to reject?
+// Called by all lanes of a wave; the answer is uniform.
+__device__ bool earlier_rejection_seen(const VerifyArgs& a, int b, int i) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const uint32_t* recs = a.records + int64_t(b) * (a.K + 1);
+    uint32_t s = kRecEmpty;
+    if (lane < i) s = rec_state(load_relaxed(&recs[lane]));
+    return __ballot(s == kRecReject || s == kRecRejectSkipped) != 0;
+}
+
+struct DrawShared {
+    int cell_round, cell_wave;
+    unsigned long long target;  // offset of u*Z inside the winning cell
+};
+
+// Inverse-CDF draw over a register-resident row pair.  mass(t, d, e) returns
+// the non-negative fp32 mass of element e of the chunks t, d (0 for padding).
+// Returns the drawn token on exactly one thread and -1 on every other thread;
+// *z_zero is set (uniformly) when the total mass is zero.
+//
+// Token order is (round n, wave w, lane, element e).  Chunk masses are summed
+// left to right in fp32 and converted exactly to 2^-62 fixed point, so every
+// partial sum below is an exact integer and the CDF cells (n, w) partition
+// [0, Z) without gaps or overlaps whatever the reduction order.  The winning
+// wave stages its chunks through LDS (s_stage, 2*CPT*64 chunks) so that the
+// winning round is selected by address, never by register index.
+template <int W, int CPT, int EPC, typename MassFn>
+__device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CPT], MassFn mass,
+                                float u, unsigned long long* s_tot, DrawShared* s_draw,
+                                chunk_t* s_stage, bool* z_zero) {
+    constexpr int NW = W / kWave;
+    constexpr int CELLS = CPT * NW;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) s = s + mass(tv[n], dv[n], e);
+        const uint64_t t = wave_sum(mass_to_fixed(s));
+        if (lane == 0) s_tot[n * NW + wid] = t;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    if (wid == 0) {
+        uint64_t z = 0;
+        for (int c0 = lane; c0 < CELLS; c0 += kWave) z += s_tot[c0];
+        z = wave_sum(z);
+        if (lane == 0) s_draw->cell_round = -1;
+        if (z > 0) {
+            uint64_t c = static_cast<uint64_t>(double(u) * double(z));
+            if (c >= z) c = z - 1;
+            uint64_t carry = 0;
+            for (int base = 0; base < CELLS; base += kWave) {
+                const int idx = base + lane;
+                const uint64_t v = idx < CELLS ? uint64_t(s_tot[idx]) : 0;
+                const uint64_t incl = wave_inclusive_scan(v) + carry;
+                const uint64_t lo = incl - v;
+                if (v > 0 && lo <= c && c < incl) {
+                    s_draw->cell_round = idx / NW;
+                    s_draw->cell_wave = idx % NW;
+                    s_draw->target = c - lo;
+                }
+                carry = static_cast<uint64_t>(__shfl(static_cast<unsigned long long>(incl), kWave - 1, kWave));
+            }
+        }
+    }
+    __syncthreads();
+    const int nstar = s_draw->cell_round;
+    *z_zero = nstar < 0;
+    if (nstar < 0 || wid != s_draw->cell_wave) return -1;
+
+    // Winning wave: stage every round through LDS, pick round nstar by address.
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        s_stage[n * kWave + lane] = tv[n];
+        s_stage[(CPT + n) * kWave + lane] = dv[n];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const chunk_t tc = s_stage[nstar * kWave + lane];
+    const chunk_t dc = s_stage[(CPT + nstar) * kWave + lane];
+    float m[EPC];
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        m[e] = mass(tc, dc, e);
+        s = s + m[e];
+    }
+    const uint64_t v = mass_to_fixed(s);
+    const uint64_t incl = wave_inclusive_scan(v);
+    const uint64_t lo = incl - v;
+    const uint64_t target = s_draw->target;
+    if (!(v > 0 && lo <= target && target < incl)) return -1;
+    // Walk the chunk with the same left-to-right fp32 sum.
+    const uint64_t want = target - lo;
+    float run = 0.0f;
+    int pick = -1, last_pos = -1;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        run = run + m[e];
+        if (m[e] > 0.0f) last_pos = e;
+        if (pick < 0 && mass_to_fixed(run) > want) pick = e;
+    }
+    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+    return (nstar * W + tid) * EPC + pick;
+}
+
+template <typename Fmt, int W, int CPT, bool VEC, bool GREEDY>
+__global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
+    constexpr int NW = W / kWave;
+    constexpr int EPC = Fmt::kPerChunk;
+    __shared__ float s_max[2][NW];
+    __shared__ double s_sum[2][NW];
+    __shared__ int s_idx[NW];
+    __shared__ int s_flag;
+    __shared__ int s_tok;
+    __shared__ unsigned long long s_tot[CPT * NW];
+    __shared__ DrawShared s_draw;
+    __shared__ chunk_t s_stage[GREEDY ? 1 : 2 * CPT * kWave];
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int B = a.B, K = a.K, V = a.V;
+    const int i = blockIdx.x / B;
+    const int b = blockIdx.x - i * B;
+    const int kb = a.draft_len ? a.draft_len[b] : K;
+    if (kb < 1 || kb > K) {
+        if (i == 0) write_invalid(a, b);
+        return;
+    }
+    if (i > kb) return;  // padding row of a short proposal
+    const bool bonus = i == kb;
+    const int y = bonus ? 0 : a.tokens[int64_t(b) * K + i];
+    if (!bonus && (y < 0 || y >= V)) {
+        if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadToken, 0));
+        return;
+    }
+
+    const char* trow = static_cast<const char*>(a.target) +
+                       (int64_t(b) * (K + 1) + i) * int64_t(V) * Fmt::kBytes;
+    chunk_t tv[CPT];
+    load_row<Fmt, W, CPT, VEC>(tv, trow, V);
+
+    if constexpr (GREEDY) {
+        // Target argmax, lowest index on ties: within a thread indices grow
+        // with (n, e), so a strict ">" keeps the first maximum.
+        float best = kNegInf;
+        int bi = 0x7FFFFFFF;
+#pragma unroll
+        for (int n = 0; n < CPT; ++n)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const float x = Fmt::get(tv[n], e);
+                if (x > best) {
+                    best = x;
+                    bi = (n * W + tid) * EPC + e;
+                }
+            }
+        wave_argmax(best, bi);
+        if (lane == 0) {
+            s_max[0][wid] = best;
+            s_idx[wid] = bi;
+        }
+        __syncthreads();
+        if (wid == 0) {
+            float bv = s_max[0][0];
+            int g = s_idx[0];
+            for (int w = 1; w < NW; ++w)
+                if (s_max[0][w] > bv || (s_max[0][w] == bv && s_idx[w] < g)) {
+                    bv = s_max[0][w];
+                    g = s_idx[w];
+                }
+            uint32_t r;
+            if (!(bv > kNegInf) || bv == -kNegInf)
+                r = make_rec(kRecBadRow, 0);
+            else if (bonus)
+                r = make_rec(kRecBonus, uint32_t(g));
+            else
+                r = make_rec(y == g ? kRecAccept : kRecReject, uint32_t(g));
+            publish(a, b, i, kb, r);
+        }
+        return;
+    } else {
+        const float c2 = a.c2;
+        // The draft row is read only for proposal rows.
+        chunk_t dv[CPT];
+        const char* drow = static_cast<const char*>(a.draft) +
+                           (int64_t(b) * K + i) * int64_t(V) * Fmt::kBytes;
+        if (!bonus) load_row<Fmt, W, CPT, VEC>(dv, drow, V);
+
+        // The logits of the proposal itself, for the acceptance test.
+        float ty = 0.0f, dy = 0.0f;
+        if (!bonus) {
+            ty = Fmt::load_one(trow, y);
+            dy = Fmt::load_one(drow, y);
+        }
+
+        // Pass 1: row maxima.
+        float mt = kNegInf, md = kNegInf;
+#pragma unroll
+        for (int n = 0; n < CPT; ++n)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) mt = fmaxf(mt, Fmt::get(tv[n], e));
+        if (!bonus) {
+#pragma unroll
+            for (int n = 0; n < CPT; ++n)
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) md = fmaxf(md, Fmt::get(dv[n], e));
+        }
+        mt = wave_max(mt);
+        md = wave_max(md);
+        if (lane == 0) {
+            s_max[0][wid] = mt;
+            s_max[1][wid] = md;
+        }
+        if (tid == 0) s_tok = -1;
+        __syncthreads();
+        mt = s_max[0][0];
+        md = s_max[1][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            mt = fmaxf(mt, s_max[0][w]);
+            md = fmaxf(md, s_max[1][w]);
+        }
+        const bool bad = !(mt > kNegInf) || mt == -kNegInf ||
+                         (!bonus && (!(md > kNegInf) || md == -kNegInf));
+        if (bad) {
+            if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadRow, 0));
+            return;
+        }
+
+        // Pass 2: sums of exponentials, pairwise within a chunk.
+        opaque(tv);
+        if (!bonus) opaque(dv);
+        float st = 0.0f, sd = 0.0f;
+#pragma unroll
+        for (int n = 0; n < CPT; ++n) {
+            float e8[EPC];
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast((Fmt::get(tv[n], e) - mt) * c2);
+#pragma unroll
+            for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+                for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+            st = st + e8[0];
+            __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
+        }
+        if (!bonus) {
+#pragma unroll
+            for (int n = 0; n < CPT; ++n) {
+                float e8[EPC];
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast((Fmt::get(dv[n], e) - md) * c2);
+#pragma unroll
+                for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+                    for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+                sd = sd + e8[0];
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const double dst = wave_sum(double(st));
+        const double dsd = wave_sum(double(sd));
+        if (lane == 0) {
+            s_sum[0][wid] = dst;
+            s_sum[1][wid] = dsd;
+        }
+        __syncthreads();
+        double St = 0.0, Sd = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            St += s_sum[0][w];
+            Sd += s_sum[1][w];
+        }
+
+        // Wave 0 decides whether this workgroup draws a token.
+        if (wid == 0) {
+            int flag;
+            if (!bonus) {
+                // Acceptance test in fp64 on the gathered logits:
+                // log p(y) - log q(y) = ((t_y - m_t) - (d_y - m_d)) / T - (ln S_t - ln S_d).
+                const double L = ((double(ty) - double(mt)) - (double(dy) - double(md))) * a.inv_T -
+                                 (log(St) - log(Sd));
+                const double ratio = exp(L);
+                const double u = a.u_accept[int64_t(b) * K + i];
+                if (u < ratio) {
+                    flag = 0;
+                    publish(a, b, i, kb, make_rec(kRecAccept, 0));
+                } else if (earlier_rejection_seen(a, b, i)) {
+                    flag = 0;
+                    publish(a, b, i, kb, make_rec(kRecRejectSkipped, 0));
+                } else {
+                    flag = 1;
+                }
+            } else {
+                if (earlier_rejection_seen(a, b, i)) {
+                    flag = 0;
+                    publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
+                } else {
+                    flag = 1;
+                }
+            }
+            if (lane == 0) s_flag = flag;
+        }
+        __syncthreads();
+        if (s_flag == 0) return;
+
+        // Draw the extra token: from max(0, p - q) after a rejection, from p
+        // at the bonus row (and, should max(0, p - q) have no mass after
+        // rounding, from p as well).
+        const float inv_st = float(1.0 / St);
+        const float inv_sd = bonus ? 0.0f : float(1.0 / Sd);
+        const float u = a.u_resample[b];
+        bool use_p = bonus;
+        for (int attempt = 0; attempt < 2; ++attempt) {
+            // Opaque copies of the maxima, fresh in each attempt: without them
+            // the compiler keeps the exponentials of pass 2 (or of the first
+            // attempt) alive in order to reuse them, and spills.
+            float mt_d = mt, md_d = md;
+            asm volatile("" : "+v"(mt_d), "+v"(md_d));
+            opaque(tv);
+            if (!use_p) opaque(dv);
+            const bool p_only = use_p;
+            auto mass = [=](const chunk_t& tc, const chunk_t& dc, int e) -> float {
+                const float p = exp2_fast((Fmt::get(tc, e) - mt_d) * c2) * inv_st;
+                if (p_only) return p;
+                const float q = exp2_fast((Fmt::get(dc, e) - md_d) * c2) * inv_sd;
+                return fmaxf(p - q, 0.0f);
+            };
+            bool z_zero = false;
+            const int tok = draw_inverse_cdf<W, CPT, EPC>(tv, dv, mass, u, s_tot, &s_draw, s_stage, &z_zero);
+            if (tok >= 0) s_tok = tok;
+            if (!z_zero || use_p) break;
+            use_p = true;
+        }
+        __syncthreads();
+        if (wid == 0) {
+            const int tok = s_tok;
+            uint32_t r;
+            if (tok >= 0)
+                r = make_rec(bonus ? kRecBonus : kRecReject, uint32_t(tok));
+            else
+                r = make_rec(kRecBadRow, 0);  // no mass anywhere
+            publish(a, b, i, kb, r);
+        }
+    }
+}
+
+template <typename Fmt, int W, int CPT>
+hipError_t launch_tile(const VerifyLaunch& L, const VerifyArgs& a) {
+    const dim3 grid(unsigned(L.B) * unsigned(L.K + 1)), block(W);
+    const bool greedy = L.temperature == 0.0f;
+    if (L.vec) {
+        if (greedy)
+            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, true, true>), grid, block, 0, L.stream, a);
+        else
+            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, true, false>), grid, block, 0, L.stream, a);
+    } else {
+        if (greedy)
+            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, false, true>), grid, block, 0, L.stream, a);
+        else
+            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, false, false>), grid, block, 0, L.stream, a);
+    }
+    return hipGetLastError();
+}
+
+template <typename Fmt>
+hipError_t launch_fmt(const VerifyLaunch& L, const VerifyArgs& a) {
+    RowTile t;
+    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    switch (t.W * 100 + t.CPT) {
+        case 25601: return launch_tile<Fmt, 256, 1>(L, a);
+        case 25602: return launch_tile<Fmt, 256, 2>(L, a);
+        case 25604: return launch_tile<Fmt, 256, 4>(L, a);
+        case 51204: return launch_tile<Fmt, 512, 4>(L, a);
+        case 51208: return launch_tile<Fmt, 512, 8>(L, a);
+        case 102408: return launch_tile<Fmt, 1024, 8>(L, a);
+        case 102416: return launch_tile<Fmt, 1024, 16>(L, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+int max_vocab_for(int per_chunk) { return 1024 * 16 * per_chunk; }
+
+bool pick_tile(int V, int per_chunk, RowTile* t) {
+    static const RowTile tiles[] = {{256, 1}, {256, 2}, {256, 4}, {512, 4},
+                                    {512, 8}, {1024, 8}, {1024, 16}};
+    for (const RowTile& c : tiles)
+        if (int64_t(V) <= int64_t(c.W) * c.CPT * per_chunk) {
+            *t = c;
+            return true;
+        }
+    return false;
+}
+
+hipError_t launch_verify(const VerifyLaunch& L) {
+    VerifyArgs a;
+    a.target = L.target;
+    a.draft = L.draft;
+    a.B = L.B;
+    a.K = L.K;
+    a.V = L.V;
+    a.tokens = L.tokens;
+    a.draft_len = L.draft_len;
+    a.u_accept = L.u_accept;
+    a.u_resample = L.u_resample;
+    a.c2 = L.temperature > 0.0f ? float(1.4426950408889634 / double(L.temperature)) : 0.0f;
+    a.inv_T = L.temperature > 0.0f ? 1.0 / double(L.temperature) : 0.0;
+    a.accepted_len = L.accepted_len;
+    a.out_tokens = L.out_tokens;
+    a.reject_mask = L.reject_mask;
+    a.records = L.records;
+    a.counters = L.counters;
+    return L.dtype == 1 ? launch_fmt<BF16>(L, a) : launch_fmt<F32>(L, a);
+}
+
+}  // namespace osd

@@ -1,0 +1,105 @@
+"""The C ABI library loads, exports every function include/osd.h declares,
+and rejects host-checkable mistakes before touching the GPU (no kernel is
+launched by any call in this file)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2310_07177_amd as osd
+from paper_2310_07177_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "osd.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(osd_[a-z_]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = osd.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert getattr(L, name) is not None
+
+
+def test_status_strings_and_limits():
+    L = osd.lib()
+    for s in (0, -1, -2, -3, -4):
+        assert L.osd_status_string(s).startswith(b"OSD_")
+    assert L.osd_max_vocab(binding.OSD_BF16) >= 128256
+    assert L.osd_max_vocab(binding.OSD_F32) >= 32768
+    assert L.osd_max_vocab(7) == 0
+
+
+def test_workspace_sizes():
+    L = osd.lib()
+    assert L.osd_verify_workspace_bytes(64, 8) >= 4 * (64 * 9 + 64)
+    assert L.osd_verify_workspace_bytes(0, 8) == 0
+    assert L.osd_verify_workspace_bytes(4, 17) == 0
+    assert L.osd_distill_workspace_bytes(16384, 1) >= 8 * 16384
+    assert L.osd_distill_workspace_bytes(-1, 1) == 0
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+
+
+def verify(**kw):
+    a = dict(target=FAKE, draft=FAKE, dtype=1, B=2, K=3, V=64, tokens=FAKE, dlen=None,
+             ua=FAKE, ur=FAKE, T=1.0, acc=FAKE, toks=FAKE, rmask=None, ws=FAKE, wsb=1 << 20,
+             stream=None)
+    a.update(kw)
+    return osd.lib().osd_verify(a["target"], a["draft"], a["dtype"], a["B"], a["K"], a["V"],
+                                a["tokens"], a["dlen"], a["ua"], a["ur"], a["T"], a["acc"],
+                                a["toks"], a["rmask"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(target=None), -1), (dict(tokens=None), -1), (dict(acc=None), -1), (dict(toks=None), -1),
+    (dict(draft=None), -1), (dict(ua=None), -1), (dict(ur=None), -1),
+    (dict(B=0), -1), (dict(K=0), -1), (dict(V=0), -1), (dict(K=17), -1), (dict(dtype=5), -1),
+    (dict(V=1 << 20), -2), (dict(dtype=0, V=70000), -2),
+    (dict(T=-1.0), -1), (dict(T=float("nan")), -1), (dict(T=float("inf")), -1),
+    (dict(ws=None), -4), (dict(wsb=16), -4), (dict(ws=ctypes.c_void_p(0x1001)), -4),
+])
+def test_verify_rejects_bad_arguments(kw, status):
+    assert verify(**kw) == status
+
+
+def distill(**kw):
+    a = dict(t=FAKE, ts=3 * 64, s=FAKE, ss=2 * 64, dtype=1, B=2, K=2, V=64, mask=None, kind=0,
+             beta=0.5, tau=1.0, loss=FAKE, rows=None, grad=None, ws=FAKE, wsb=1 << 20, stream=None)
+    a.update(kw)
+    return osd.lib().osd_distill_loss_grad(a["t"], a["ts"], a["s"], a["ss"], a["dtype"], a["B"],
+                                           a["K"], a["V"], a["mask"], a["kind"], a["beta"],
+                                           a["tau"], a["loss"], a["rows"], a["grad"], a["ws"],
+                                           a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(t=None), -1), (dict(s=None), -1), (dict(loss=None), -1),
+    (dict(B=0), -1), (dict(K=-1), -1), (dict(V=0), -1), (dict(dtype=3), -1), (dict(kind=3), -1),
+    (dict(tau=0.0), -1), (dict(tau=-2.0), -1), (dict(tau=float("nan")), -1),
+    (dict(beta=-0.1), -1), (dict(beta=1.5), -1), (dict(beta=float("nan")), -1),
+    (dict(ts=10), -1), (dict(ss=10), -1),
+    (dict(V=1 << 20), -2),
+    (dict(ws=None), -4), (dict(wsb=8), -4),
+])
+def test_distill_rejects_bad_arguments(kw, status):
+    assert distill(**kw) == status
+
+
+def test_binding_fails_loudly_without_gpu_tensors():
+    import torch
+    t = torch.zeros(1, 2, 8)
+    with pytest.raises(ValueError):
+        osd.osd_verify(t, t[:, :1].contiguous(), torch.zeros(1, 1, dtype=torch.int32),
+                       torch.zeros(1, 1), torch.zeros(1), 1.0)

@@ -1,0 +1,322 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle.
+
+Inputs are the seeded synthetic workloads of paper_2310_07177_amd.synth.  The
+bar: accepted lengths, emitted tokens and reject masks bit-exact except for
+sequences where a decision the oracle evaluated sits within 1e-6 of its
+boundary (counted and printed); fp32 losses within 1e-5 relative; bf16
+gradients within 2e-3 absolute of the oracle's fp64 value rounded to bf16
+(elements at a bf16 rounding midpoint excluded and counted); fp32 gradients
+within 2e-6 absolute.
+"""
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_2310_07177_amd import synth
+from tests._helpers import (compare_grad_bf16, compare_grad_f32, compare_losses,
+                            compare_verify, to_device)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def osd():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    import paper_2310_07177_amd as m
+    m.lib()
+    return m
+
+
+def run_verify(osd, x):
+    import torch
+    T = x["T"]
+    out = osd.osd_verify(to_device(x["target"]), None if T == 0 else to_device(x["draft"]),
+                         to_device(x["tokens"].astype(np.int32)),
+                         None if T == 0 else to_device(x["u_accept"]),
+                         None if T == 0 else to_device(x["u_resample"]), T,
+                         draft_len=to_device(x.get("draft_len")))
+    torch.cuda.synchronize()
+    return [o.cpu().numpy() for o in out]
+
+
+def oracle_verify(x):
+    T = x["T"]
+    return ref.verify(x["target"], None if T == 0 else x["draft"], x["tokens"],
+                      None if T == 0 else x["u_accept"], None if T == 0 else x["u_resample"], T,
+                      draft_len=x.get("draft_len"))
+
+
+def check_verify(osd, x, label, max_excluded_frac=0.1):
+    acc, toks, rmask = run_verify(osd, x)
+    r = oracle_verify(x)
+    n, ex = compare_verify(r, acc, toks, rmask, label)
+    print(f"[{label}] compared {n} sequences, excluded {ex} (margin < 1e-6)", flush=True)
+    assert ex <= max(1, max_excluded_frac * len(acc))
+    return r, acc
+
+
+# --------------------------------------------------------------------------
+# Verification
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_verify_tiny_fp32(osd, seed):
+    check_verify(osd, synth.config_tiny(seed), f"tiny seed {seed}")
+
+
+@pytest.mark.parametrize("sigma", [0.25, 1.0, 2.0])
+def test_verify_llama_vocab(osd, sigma):
+    for seed in range(3):
+        check_verify(osd, synth.config_llama_vocab(sigma, seed), f"llama sigma={sigma} seed={seed}")
+
+
+def test_verify_t5_vocab_full_batch(osd):
+    for seed in range(2):
+        r, acc = check_verify(osd, synth.config_t5_vocab(seed), f"t5 B=64 K=8 seed={seed}")
+        print(f"  mean accepted {acc.mean():.3f}", flush=True)
+
+
+def test_verify_t5_vocab_greedy(osd):
+    for seed in range(2):
+        x = synth.config_t5_vocab(seed, greedy=True)
+        check_verify(osd, x, f"t5 greedy seed={seed}", max_excluded_frac=0.0)
+
+
+def test_verify_greedy_ties_lowest_index(osd):
+    g = np.random.default_rng(5)
+    B, K, V = 16, 4, 3000
+    t = g.integers(-2, 3, (B, K + 1, V)).astype(np.float32)  # massive ties
+    x = dict(target=synth.to_bf16(t), draft=None, tokens=np.argmax(t[:, :K], -1).astype(np.int32),
+             u_accept=None, u_resample=None, T=0.0)
+    x["tokens"][::3, 1] = 0
+    check_verify(osd, x, "greedy ties", max_excluded_frac=0.0)
+
+
+@pytest.mark.parametrize("V", [1, 7, 1001, 4099])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_verify_ragged_tail_vocab(osd, V, dtype):
+    """V not a multiple of the 16-byte chunk: the element-wise (unaligned)
+    path, and tiny vocabularies."""
+    x = synth.verify_inputs(6, 3, V, dtype, T=0.9, seed=V, target_std=2.0, draft_noise=1.0)
+    check_verify(osd, x, f"V={V} {dtype}")
+
+
+@pytest.mark.parametrize("V", [2048, 2049 * 8, 32000, 65536])
+def test_verify_tile_boundaries(osd, V):
+    x = synth.verify_inputs(4, 5, V, "bf16", T=1.0, seed=7, target_std=2.5, draft_noise=0.5)
+    check_verify(osd, x, f"tile V={V}")
+
+
+def test_verify_ragged_lengths_and_invalid_rows(osd):
+    g = np.random.default_rng(11)
+    x = synth.verify_inputs(12, 6, 5000, "bf16", T=1.0, seed=3, ragged=True, draft_noise=0.3)
+    x["draft_len"][0] = 0        # invalid k_b
+    x["draft_len"][1] = 7        # invalid k_b > K
+    x["tokens"][2, 0] = 5000     # out-of-range proposal
+    x["tokens"][3, x["draft_len"][3] - 1] = -3
+    # a row without finite logits at position 0 of sequence 4 (read: invalid)
+    x["target"][4, 0, :] = 0xFF80
+    # same, but after a certain rejection at position 0 of sequence 5 (never read)
+    x["draft_len"][5] = 3
+    x["target"][5, 0, :] = 0xFF80
+    x["target"][5, 0, 17] = synth.to_bf16(np.float32([0.0]))[0]
+    x["draft"][5, 0, :] = synth.to_bf16(np.float32([0.0]))[0]
+    x["tokens"][5, 0] = 3        # p(y) = 0: always rejected
+    x["target"][5, 1, :] = 0xFF80
+    r, acc = check_verify(osd, x, "ragged + invalid")
+    assert acc[:5].tolist() == [-1] * 5
+    assert acc[5] == 0 and r["out_tokens"][5, 0] == 17
+
+
+def test_verify_identical_rows_accept_all(osd):
+    x = synth.verify_inputs(32, 8, 32128, "bf16", T=0.7, seed=4)
+    x["draft"] = x["target"][:, :8].copy()
+    x["u_accept"][:] = np.float32(1 - 2 ** -24)
+    acc, toks, rmask = run_verify(osd, x)
+    assert (acc == 8).all() and (rmask == 0).all()
+    # u sits 2^-24 below the ratio 1, inside the margin band: only the
+    # all-accepted property above is exact; the bonus tokens are compared
+    # where their own CDF margin allows.
+    check_verify(osd, x, "identical rows", max_excluded_frac=1.0)
+
+
+def test_verify_neg_inf_entries(osd):
+    x = synth.verify_inputs(8, 4, 3000, "f32", T=1.0, seed=9, draft_noise=1.5)
+    g = np.random.default_rng(1)
+    holes = g.random(x["target"].shape) < 0.3
+    x["target"][holes] = -np.inf
+    dh = g.random(x["draft"].shape) < 0.3
+    x["draft"][dh] = -np.inf
+    # keep the proposals drawable from the draft
+    x["tokens"] = synth.gumbel_max_tokens(synth.rng(5), x["draft"], 1.0)
+    check_verify(osd, x, "-inf entries")
+
+
+def test_verify_large_vocab_ragged(osd):
+    x = synth.config_large_vocab(seed=0, B=8)
+    check_verify(osd, x, "V=128256 ragged B=8")
+
+
+def test_verify_deterministic(osd):
+    x = synth.config_t5_vocab(3)
+    a = run_verify(osd, x)
+    b = run_verify(osd, x)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_verify_repeated_calls_reuse_workspace(osd):
+    """The workspace is left zeroed: many consecutive calls on one stream stay
+    correct, including a switch of batch size."""
+    for seed, (B, K) in enumerate([(16, 4), (16, 4), (5, 8), (16, 4)]):
+        x = synth.verify_inputs(B, K, 8192, "bf16", T=1.0, seed=20 + seed, draft_noise=0.7)
+        check_verify(osd, x, f"repeat {seed} B={B} K={K}")
+
+
+# --------------------------------------------------------------------------
+# Distillation
+# --------------------------------------------------------------------------
+
+def run_distill(osd, teacher, student, kind, beta, tau, mask=None, B=None, K=None,
+                tstride=None, sstride=None):
+    import torch
+    loss, rows, grad = osd.osd_distill_loss_grad(
+        to_device(teacher), to_device(student), kind, beta, tau, mask=to_device(mask), B=B, K=K,
+        teacher_batch_stride=tstride, student_batch_stride=sstride)
+    torch.cuda.synchronize()
+    g = grad.cpu()
+    if g.dtype == torch.bfloat16:
+        g = g.view(torch.int16).numpy().view(np.uint16)
+    else:
+        g = g.numpy()
+    return loss.cpu().numpy(), rows.cpu().numpy(), g
+
+
+def check_distill(osd, teacher, student, kind, beta, tau, mask, label, B=None, K=None,
+                  tstride=None, sstride=None):
+    loss, rows, g = run_distill(osd, teacher, student, kind, beta, tau, mask, B, K, tstride, sstride)
+    r = ref.distill(teacher, student, kind, beta=beta, tau=tau, mask=mask, B=B, K=K,
+                    teacher_batch_stride=tstride, student_batch_stride=sstride)
+    compare_losses(rows, r["row_loss"], label=f"{label} row loss")
+    compare_losses(loss, [r["loss_mean"], r["loss_sum"]], label=f"{label} loss")
+    if g.dtype == np.uint16:
+        ex = compare_grad_bf16(g, r["grad"], label)
+    else:
+        compare_grad_f32(g, r["grad"], label)
+        ex = 0
+    print(f"[{label}] loss mean {loss[0]:.6g} sum {loss[1]:.6g}; {ex} midpoint elements excluded",
+          flush=True)
+    return loss, rows, g
+
+
+@pytest.mark.parametrize("kind", ["fkl", "rkl", "jsd"])
+def test_distill_tiny_fp32(osd, kind):
+    x = synth.config_tiny(0)
+    check_distill(osd, x["target"][:, :4].copy(), x["draft"], kind, 0.5, 1.0, x["mask"],
+                  f"tiny {kind}")
+
+
+@pytest.mark.parametrize("sigma", [0.25, 1.0, 2.0])
+def test_distill_llama_vocab_on_rejected_rows(osd, sigma):
+    x = synth.config_llama_vocab(sigma, 0)
+    r = oracle_verify(x)
+    mask = r["reject_mask"]
+    K = x["K"]
+    check_distill(osd, x["target"], x["draft"], "fkl", 0.5, 1.0, mask, f"llama fkl sigma={sigma}",
+                  B=x["B"], K=K, tstride=(K + 1) * x["V"], sstride=K * x["V"])
+
+
+@pytest.mark.parametrize("kind", ["rkl", "jsd"])
+def test_distill_t5_vocab_full_batch(osd, kind):
+    x = synth.config_t5_vocab(0)
+    B, K, V = x["B"], x["K"], x["V"]
+    check_distill(osd, x["target"], x["draft"], kind, 0.5, 0.7, x["mask"], f"t5 {kind}",
+                  B=B, K=K, tstride=(K + 1) * V, sstride=K * V)
+
+
+@pytest.mark.parametrize("kind,beta,tau", [("fkl", 0.5, 1.3), ("rkl", 0.5, 0.5),
+                                           ("jsd", 0.1, 1.0), ("jsd", 0.9, 0.8)])
+@pytest.mark.parametrize("V", [5, 1001, 32000])
+def test_distill_shapes_and_settings(osd, kind, beta, tau, V):
+    g = np.random.default_rng(V)
+    B, K = 3, 4
+    t = synth.to_bf16(g.normal(0, 2.5, (B, K, V)).astype(np.float32))
+    s = synth.to_bf16((synth.bf16_to_f32(t) + g.normal(0, 1, (B, K, V))).astype(np.float32))
+    mask = (g.random((B, K)) < 0.6).astype(np.uint8)
+    check_distill(osd, t, s, kind, beta, tau, mask, f"{kind} beta={beta} tau={tau} V={V}")
+
+
+def test_distill_identical_rows_zero(osd):
+    x = synth.config_t5_vocab(1, B=8)
+    K, V = x["K"], x["V"]
+    s = x["target"][:, :K].copy()
+    for kind in ("fkl", "rkl", "jsd"):
+        loss, rows, g = run_distill(osd, s, s, kind, 0.5, 0.7)
+        assert np.all(np.abs(rows) <= 1e-6), kind
+        assert np.all(np.abs(synth.bf16_to_f32(g)) <= 1e-6), kind
+
+
+def test_distill_empty_mask(osd):
+    x = synth.config_t5_vocab(1, B=4)
+    K = x["K"]
+    loss, rows, g = run_distill(osd, x["target"][:, :K].copy(), x["draft"], "jsd", 0.5, 0.7,
+                                mask=np.zeros((4, K), np.uint8))
+    assert loss.tolist() == [0.0, 0.0]
+    assert not rows.any() and not g.any()
+
+
+def test_distill_buffer_sampled_rows(osd):
+    """N = 16384 buffered positions x V = 32000 (JSD, beta 0.5, tau 1, 40 %
+    mask) at full size on the GPU; the oracle checks a sample of 96 rows one
+    by one, and the loss equals the fp64 sum of the per-row losses."""
+    x = synth.config_distill_buffer()
+    N, V = x["B"], x["V"]
+    loss, rows, g = run_distill(osd, x["teacher"], x["student"], "jsd", 0.5, 1.0, x["mask"])
+    idx = np.random.default_rng(0).choice(N, 96, replace=False)
+    idx = np.concatenate([idx, np.nonzero(x["mask"][:, 0])[0][:16], np.nonzero(x["mask"][:, 0] == 0)[0][:4]])
+    r = ref.distill(x["teacher"][idx], x["student"][idx], "jsd", beta=0.5, tau=1.0,
+                    mask=x["mask"][idx])
+    compare_losses(rows[idx], r["row_loss"], label="buffer rows")
+    compare_grad_bf16(g[idx], r["grad"], "buffer grad")
+    total = np.sum(rows.astype(np.float64))
+    count = float(x["mask"].sum())
+    compare_losses(loss, [total / count, total], rtol=1e-5, label="buffer loss vs row sum")
+
+
+def test_distill_deterministic(osd):
+    x = synth.config_t5_vocab(2)
+    B, K, V = x["B"], x["K"], x["V"]
+    a = run_distill(osd, x["target"], x["draft"], "jsd", 0.5, 0.7, x["mask"], B, K, (K + 1) * V, K * V)
+    b = run_distill(osd, x["target"], x["draft"], "jsd", 0.5, 0.7, x["mask"], B, K, (K + 1) * V, K * V)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_distill_large_vocab(osd):
+    x = synth.config_large_vocab(seed=1, B=4)
+    r = oracle_verify(x)
+    K, V = x["K"], x["V"]
+    check_distill(osd, x["target"], x["draft"], "fkl", 0.5, 0.8, r["reject_mask"], "V=128256 fkl",
+                  B=x["B"], K=K, tstride=(K + 1) * V, sstride=K * V)
+
+
+def test_workspaces_left_zero_across_shapes(osd):
+    """Every call leaves its workspace zeroed, so calls with different (B, K)
+    can share one workspace: alternate shapes and check losses and the
+    workspace bytes."""
+    import torch
+    from paper_2310_07177_amd import binding
+    g = np.random.default_rng(3)
+    for B, K in [(64, 8), (3, 4), (130, 1), (3, 4), (1, 2)]:
+        V = 2000
+        t = synth.to_bf16(g.normal(0, 2, (B, K, V)).astype(np.float32))
+        s = synth.to_bf16(g.normal(0, 2, (B, K, V)).astype(np.float32))
+        mask = (g.random((B, K)) < 0.5).astype(np.uint8)
+        check_distill(osd, t, s, "rkl", 0.5, 1.0, mask, f"ws B={B} K={K}")
+        x = synth.verify_inputs(B, K, V, "bf16", T=1.0, seed=B * 31 + K, draft_noise=0.8)
+        check_verify(osd, x, f"ws verify B={B} K={K}")
+        torch.cuda.synchronize()
+        for key, ws in binding._workspaces.items():
+            assert int(ws.count_nonzero()) == 0, key
