@@ -100,7 +100,7 @@ def cpu_baseline():
                     teacher_batch_stride=(K + 1) * V, student_batch_stride=K * V)
         reps += 1
         el = time.perf_counter() - t0
-        if el > 10.0 or reps >= 3:
+        if el > 10.0 or reps >= 60:
             break
     return {"value": reps * B * K / el, "unit": "positions/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} full batch(es) of B=64 k=8 V=32128 bf16 (verify T=0.7 + JSD "
@@ -190,24 +190,29 @@ def main():
         return e0.elapsed_time(e1) / iters  # ms
 
     if args.only:
+        # Profiling aid: run only the named loops (comma-separated), each
+        # warmed up and timed on its own; "copy" is a plain 256 MiB device
+        # copy used to calibrate the HBM byte counters.
         loops = {"verify": lambda r: call(fv, verify_args[r % R]),
                  "greedy": lambda r: call(fv, greedy_args[r % R]),
                  "jsd": lambda r: call(fd, jsd_args[r % R]),
                  "rkl": lambda r: call(fd, rkl_args[r % R])}
-        if args.only == "copy":
-            # a plain copy of known size, to calibrate the HBM byte counters
-            src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-            dst = torch.empty_like(src)
-            for _ in range(10):
-                dst.copy_(src)
-            torch.cuda.synchronize()
-            print(json.dumps({"only": "copy", "bytes_read": src.numel(), "bytes_written": dst.numel()}))
-            return
-        fn = loops[args.only]
-        for r in range(args.warmup):
-            fn(r)
-        ms = time_loop(fn, args.kernel_iters)
-        print(json.dumps({"only": args.only, "us_per_launch": ms * 1e3}), flush=True)
+        for name in args.only.split(","):
+            if name == "copy":
+                src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+                dst = torch.empty_like(src)
+                for _ in range(10):
+                    dst.copy_(src)
+                torch.cuda.synchronize()
+                print(json.dumps({"only": "copy", "bytes_read": src.numel(),
+                                  "bytes_written": dst.numel(), "launches": 10}), flush=True)
+                continue
+            fn = loops[name]
+            for r in range(args.warmup):
+                fn(r)
+            ms = time_loop(fn, args.kernel_iters)
+            print(json.dumps({"only": name, "us_per_launch": ms * 1e3,
+                              "launches": args.warmup + args.kernel_iters}), flush=True)
         return
 
     for r in range(args.warmup):

@@ -84,52 +84,99 @@ __device__ inline void store_grad_chunk(void* row, int n, const chunk_t& c, int 
 __device__ inline double wave_sum_fixed(double v) { return wave_sum(v); }
 
 // Executed by all lanes of wave 0: record D for row n and fold it into the
-// masked sum once every row of its slab (and then every slab) has arrived.
+// masked sum once every row has arrived.  Up to kOneLevelRows rows, the last
+// row to arrive sums them all (each lane a fixed strided subset, then a fixed
+// butterfly); beyond that, rows are summed per 64-row slab first and the last
+// slab to arrive sums the slabs.  Every order is fixed, so the result is
+// reproducible bit for bit.
+__device__ void finish_loss(const DistillArgs& a, double sum, double count) {
+    const int lane = threadIdx.x & (kWave - 1);
+    if (lane == 0) {
+        a.loss_out[0] = count > 0.0 ? float(sum / count) : 0.0f;
+        a.loss_out[1] = float(sum);
+    }
+}
+
 __device__ void reduce_loss(const DistillArgs& a, int n, double D) {
     const int lane = threadIdx.x & (kWave - 1);
     const int rows = a.B * a.K;
+    uint32_t prev = 0;
+    if (rows <= kOneLevelRows) {
+        if (lane == 0) {
+            publish_f64(&a.row_ws[n], D);
+            prev = arrive(a.done_cnt);
+        }
+        prev = __shfl(prev, 0, kWave);
+        if (prev != uint32_t(rows - 1)) return;
+        double v[kOneLevelRows / kWave];
+#pragma unroll
+        for (int k = 0; k < kOneLevelRows / kWave; ++k) {
+            const int r = k * kWave + lane;
+            v[k] = r < rows ? take_f64(&a.row_ws[r]) : 0.0;  // read and clear
+        }
+        double s = 0.0, c = 0.0;
+#pragma unroll
+        for (int k = 0; k < kOneLevelRows / kWave; ++k) {
+            const int r = k * kWave + lane;
+            s += v[k];
+            c += (r < rows && (a.mask == nullptr || a.mask[r] != 0)) ? 1.0 : 0.0;
+        }
+        s = wave_sum_fixed(s);
+        c = wave_sum_fixed(c);
+        finish_loss(a, s, c);
+        if (lane == 0) take_u32(a.done_cnt);
+        return;
+    }
     const int slab = n / kSlabRows;
     const int first = slab * kSlabRows;
     const int in_slab = min(kSlabRows, rows - first);
-    uint32_t prev = 0;
     if (lane == 0) {
-        store_relaxed(&a.row_ws[n], D);
+        publish_f64(&a.row_ws[n], D);
         prev = arrive(&a.slab_cnt[slab]);
     }
     prev = __shfl(prev, 0, kWave);
     if (prev != uint32_t(in_slab - 1)) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     double v = 0.0, c = 0.0;
     if (lane < in_slab) {
-        v = load_relaxed(&a.row_ws[first + lane]);
+        v = take_f64(&a.row_ws[first + lane]);  // read and clear
         c = (a.mask == nullptr || a.mask[first + lane] != 0) ? 1.0 : 0.0;
-        store_relaxed(&a.row_ws[first + lane], 0.0);  // leave the workspace zeroed
     }
     const double slab_sum = wave_sum_fixed(v);
     const double slab_cnt = wave_sum_fixed(c);
     if (lane == 0) {
-        store_relaxed(&a.slab_ws[2 * slab], slab_sum);
-        store_relaxed(&a.slab_ws[2 * slab + 1], slab_cnt);
-        store_relaxed(&a.slab_cnt[slab], 0u);
+        publish_f64(&a.slab_ws[2 * slab], slab_sum);
+        publish_f64(&a.slab_ws[2 * slab + 1], slab_cnt);
+        take_u32(&a.slab_cnt[slab]);
         prev = arrive(a.done_cnt);
     }
     prev = __shfl(prev, 0, kWave);
     if (prev != uint32_t(a.nslabs - 1)) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     double ts = 0.0, tc = 0.0;
     for (int s = lane; s < a.nslabs; s += kWave) {
-        ts += load_relaxed(&a.slab_ws[2 * s]);
-        tc += load_relaxed(&a.slab_ws[2 * s + 1]);
-        store_relaxed(&a.slab_ws[2 * s], 0.0);
-        store_relaxed(&a.slab_ws[2 * s + 1], 0.0);
+        ts += take_f64(&a.slab_ws[2 * s]);
+        tc += take_f64(&a.slab_ws[2 * s + 1]);
     }
     ts = wave_sum_fixed(ts);
     tc = wave_sum_fixed(tc);
-    if (lane == 0) {
-        a.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
-        a.loss_out[1] = float(ts);
-        store_relaxed(a.done_cnt, 0u);
-    }
+    finish_loss(a, ts, tc);
+    if (lane == 0) take_u32(a.done_cnt);
+}
+
+// Largest finite fp32 magnitude used to stand in for log2(0) = -inf, so that
+// p * log2(p) stays 0 * finite = 0 for logits of -inf.
+constexpr float kLogFloor = -1.0e30f;
+// Smallest mixture probability fed to log2 (a normal fp32 number, so that
+// v_log_f32 stays finite when both p and q underflow).
+constexpr float kMixFloor = 1.0e-37f;
+
+template <typename Fmt, int CPT>
+__device__ inline float row_max(const chunk_t (&c)[CPT]) {
+    float m = kNegInf;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n)
+#pragma unroll
+        for (int e = 0; e < Fmt::kPerChunk; ++e) m = fmaxf(m, Fmt::get(c[n], e));
+    return m;
 }
 
 template <typename Fmt, int W, int CPT, bool VEC, int KIND>
@@ -164,16 +211,8 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
         const float c2 = a.c2;
 
         // Row maxima.
-        float mt = kNegInf, ms = kNegInf;
-#pragma unroll
-        for (int c = 0; c < CPT; ++c)
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                mt = fmaxf(mt, Fmt::get(tv[c], e));
-                ms = fmaxf(ms, Fmt::get(sv[c], e));
-            }
-        mt = wave_max(mt);
-        ms = wave_max(ms);
+        float mt = wave_max(row_max<Fmt, CPT>(tv));
+        float ms = wave_max(row_max<Fmt, CPT>(sv));
         if (lane == 0) {
             s_max[0][wid] = mt;
             s_max[1][wid] = ms;
@@ -186,33 +225,58 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
             mt = fmaxf(mt, s_max[0][w]);
             ms = fmaxf(ms, s_max[1][w]);
         }
+        // Exponents are x c2 - m c2 (one fma); the shift cancels on normalising.
+        const float mtc = mt * c2, msc = ms * c2;
 
-        // Sums of exponentials, pairwise within a chunk.
+        // Sums of exponentials.  FKL and RKL are first-order sensitive to the
+        // normaliser (an error s in S shifts every log-ratio by s), so they
+        // accumulate every term in fp64; JSD is not (the mixture absorbs a
+        // common scale error), so it sums pairwise in fp32 within a chunk.
         opaque(tv);
         opaque(sv);
-        float st = 0.0f, ss = 0.0f;
+        double dst = 0.0, dss = 0.0;
+        if constexpr (KIND == 2) {
+            float st = 0.0f, ss = 0.0f;
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) {
-            float et[EPC], es[EPC];
+            for (int c = 0; c < CPT; ++c) {
+                float et[EPC], es[EPC];
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                et[e] = exp2_fast((Fmt::get(tv[c], e) - mt) * c2);
-                es[e] = exp2_fast((Fmt::get(sv[c], e) - ms) * c2);
-            }
-#pragma unroll
-            for (int w = 1; w < EPC; w <<= 1)
-#pragma unroll
-                for (int e = 0; e < EPC; e += 2 * w) {
-                    et[e] = et[e] + et[e + w];
-                    es[e] = es[e] + es[e + w];
+                for (int e = 0; e < EPC; ++e) {
+                    et[e] = exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e), c2, -mtc));
+                    es[e] = exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e), c2, -msc));
                 }
-            st = st + et[0];
-            ss = ss + es[0];
-            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+                    for (int e = 0; e < EPC; e += 2 * w) {
+                        et[e] = et[e] + et[e + w];
+                        es[e] = es[e] + es[e + w];
+                    }
+                st = st + et[0];
+                ss = ss + es[0];
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            dst = st;
+            dss = ss;
+        } else {
+            double t0 = 0.0, t1 = 0.0, s0 = 0.0, s1 = 0.0;
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) {
+#pragma unroll
+                for (int e = 0; e < EPC; e += 2) {
+                    t0 += double(exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e), c2, -mtc)));
+                    t1 += double(exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e + 1), c2, -mtc)));
+                    s0 += double(exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e), c2, -msc)));
+                    s1 += double(exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e + 1), c2, -msc)));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            dst = t0 + t1;
+            dss = s0 + s1;
         }
         {
-            const double dt = wave_sum(double(st));
-            const double ds = wave_sum(double(ss));
+            const double dt = wave_sum(dst);
+            const double ds = wave_sum(dss);
             if (lane == 0) {
                 s_sum[0][wid] = dt;
                 s_sum[1][wid] = ds;
@@ -224,16 +288,20 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
             St += s_sum[0][w];
             Ss += s_sum[1][w];
         }
-        // log2 p_j = (t_j - m_t) c2 - log2 S_t, p_j = 2^((t_j - m_t) c2) / S_t.
-        const float l2t = float(log2(St)), l2s = float(log2(Ss));
-        const float inv_st = float(1.0 / St), inv_ss = float(1.0 / Ss);
+        // log2 p_j = t_j c2 - (m_t c2 + log2 S_t) and p_j = 2^(log2 p_j): one
+        // fma and one exponential per element; likewise for q.
+        const double ktd = double(mtc) + log2(St), ksd = double(msc) + log2(Ss);
+        const float kt = float(ktd), ks = float(ksd);
+        // log2(p_j / q_j) = (t_j - s_j) c2 - (k_t - k_s): the difference of the
+        // two constants is taken in fp64, so the loss of FKL and RKL carries no
+        // rounding of the (much larger) constants themselves.
+        const float dk = float(ktd - ksd);
         const float beta = a.beta, omb = 1.0f - a.beta;
         const float ln2 = float(kLn2);
-        const float inv_tau = a.inv_tau;
 
-        // Divergence terms.
-        float mt_c = mt, ms_c = ms;
-        asm volatile("" : "+v"(mt_c), "+v"(ms_c));
+        // Divergence terms, in log2 units.
+        float kt_c = kt, ks_c = ks, dk_c = dk;
+        asm volatile("" : "+v"(kt_c), "+v"(ks_c), "+v"(dk_c));
         opaque(tv);
         opaque(sv);
         float acc0 = 0.0f, acc1 = 0.0f;
@@ -242,21 +310,27 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
             float c0 = 0.0f, c1 = 0.0f;
 #pragma unroll
             for (int e = 0; e < EPC; ++e) {
-                const float at = (Fmt::get(tv[c], e) - mt_c) * c2;
-                const float as = (Fmt::get(sv[c], e) - ms_c) * c2;
-                const float p = exp2_fast(at) * inv_st;
-                const float q = exp2_fast(as) * inv_ss;
-                const float lp = at - l2t, lq = as - l2s;
-                if constexpr (KIND == 0) {
-                    c0 = c0 + (p > 0.0f ? p * (lp - lq) : 0.0f);
-                } else if constexpr (KIND == 1) {
-                    c0 = c0 + (q > 0.0f ? q * (lq - lp) : 0.0f);
+                const float t = Fmt::get(tv[c], e), sx = Fmt::get(sv[c], e);
+                if constexpr (KIND == 0 || KIND == 1) {
+                    // log2(p/q), clamped so that a zero probability times an
+                    // infinite log-ratio stays 0.
+                    const float lr = fmaxf(fminf(__builtin_fmaf(t - sx, c2, -dk_c), -kLogFloor), kLogFloor);
+                    if constexpr (KIND == 0) {
+                        const float p = exp2_fast(__builtin_fmaf(t, c2, -kt_c));
+                        c0 = __builtin_fmaf(p, lr, c0);
+                    } else {
+                        const float q = exp2_fast(__builtin_fmaf(sx, c2, -ks_c));
+                        c0 = __builtin_fmaf(-q, lr, c0);
+                    }
                 } else {
-                    const float lm = log2_fast(beta * p + omb * q);
-                    c0 = c0 + (p > 0.0f ? p * (lp - lm) : 0.0f);
-                    c1 = c1 + (q > 0.0f ? q * (lq - lm) : 0.0f);
+                    const float lp = fmaxf(__builtin_fmaf(t, c2, -kt_c), kLogFloor);
+                    const float lq = fmaxf(__builtin_fmaf(sx, c2, -ks_c), kLogFloor);
+                    const float p = exp2_fast(lp), q = exp2_fast(lq);
+                    const float lm = log2_fast(fmaxf(__builtin_fmaf(beta, p, omb * q), kMixFloor));
+                    c0 = __builtin_fmaf(p, lp - lm, c0);
+                    c1 = __builtin_fmaf(q, lq - lm, c1);
                 }
-                if ((e & 1) == 1) __builtin_amdgcn_sched_barrier(0);  // 2 elements in flight
+                if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);  // 4 elements in flight
             }
             acc0 = acc0 + c0;
             acc1 = acc1 + c1;
@@ -287,9 +361,9 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
             // FKL: g = (q - p) / tau;  RKL: g = q (ln q - ln p - D) / tau;
             // JSD: g = (1-beta) q (ln q - ln m - KL(q||m)) / tau.
             const float shift = KIND == 1 ? float(D) : float(kLn2 * A1);
-            const float scale = (KIND == 2 ? omb : 1.0f) * inv_tau;
-            float mt_g = mt, ms_g = ms;
-            asm volatile("" : "+v"(mt_g), "+v"(ms_g));
+            const float scale = (KIND == 2 ? omb : 1.0f) * a.inv_tau;
+            float kt_g = kt, ks_g = ks;
+            asm volatile("" : "+v"(kt_g), "+v"(ks_g));
             opaque(tv);
             opaque(sv);
 #pragma unroll
@@ -297,22 +371,20 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
                 float g[EPC];
 #pragma unroll
                 for (int e = 0; e < EPC; ++e) {
-                    const float at = (Fmt::get(tv[c], e) - mt_g) * c2;
-                    const float as = (Fmt::get(sv[c], e) - ms_g) * c2;
-                    const float q = exp2_fast(as) * inv_ss;
+                    const float lp = fmaxf(__builtin_fmaf(Fmt::get(tv[c], e), c2, -kt_g), kLogFloor);
+                    const float lq = fmaxf(__builtin_fmaf(Fmt::get(sv[c], e), c2, -ks_g), kLogFloor);
+                    const float q = exp2_fast(lq);
                     if constexpr (KIND == 0) {
-                        const float p = exp2_fast(at) * inv_st;
-                        g[e] = (q - p) * scale;
+                        g[e] = (q - exp2_fast(lp)) * scale;
                     } else {
-                        const float lq = as - l2s;
                         float lr;
                         if constexpr (KIND == 1) {
-                            lr = lq - (at - l2t);
+                            lr = lq - lp;
                         } else {
-                            const float p = exp2_fast(at) * inv_st;
-                            lr = lq - log2_fast(beta * p + omb * q);
+                            const float p = exp2_fast(lp);
+                            lr = lq - log2_fast(fmaxf(__builtin_fmaf(beta, p, omb * q), kMixFloor));
                         }
-                        g[e] = q > 0.0f ? q * (lr * ln2 - shift) * scale : 0.0f;
+                        g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
                     }
                     if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
                 }

@@ -159,17 +159,18 @@ __device__ inline void wave_argmax(float& v, int& idx) {
 }
 
 // ---------------------------------------------------------------------------
-// Fixed-point probability mass.  A non-negative fp32 value x < 2 maps to
-// floor(x * 2^62) exactly for x >= 2^-39 (the mantissa is shifted, not
-// rounded); integer sums of such values are associative, so every reduction
-// order partitions a CDF identically.
+// Fixed-point probability mass.  A non-negative fp32 value x < 2^(63-SH) maps
+// to floor(x * 2^SH); the conversion is exact for x >= 2^(23-SH) (the
+// mantissa is shifted, not rounded).  Integer sums of such values are
+// associative, so every reduction order partitions a CDF identically.
 // ---------------------------------------------------------------------------
+template <int SH>
 __device__ inline uint64_t mass_to_fixed(float x) {
     const uint32_t b = __float_as_uint(x);
     const int e = int((b >> 23) & 0xFF) - 127;
     if (e < -126 || (b >> 31)) return 0;  // zero, subnormal or negative
     const uint64_t m = uint64_t((b & 0x7FFFFFu) | 0x800000u);
-    const int sh = e + 39;  // x * 2^62 = m * 2^(e - 23 + 62)
+    const int sh = e + SH - 23;  // x * 2^SH = m * 2^(e - 23 + SH)
     if (sh >= 0) return m << sh;
     if (sh <= -64) return 0;
     return m >> (-sh);
@@ -182,35 +183,54 @@ __device__ inline uint64_t mass_to_fixed(float x) {
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ inline float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
 
-// fp32 -> bf16 bit pattern, round to nearest even (NaN stays NaN).
-__device__ inline uint32_t f32_to_bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
-
+// Two fp32 values to a packed pair of bf16, round to nearest even, with the
+// native v_cvt_pk_bf16_f32 of gfx950.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 // ---------------------------------------------------------------------------
-// Cross-workgroup hand-off through device memory: relaxed agent-scope atomics
-// for the payload, an acquire-release add on the arrival counter.
+// Cross-workgroup hand-off through device memory, without cache flushes.
+//
+// Every word that crosses workgroups is written and read with agent-scope
+// atomic read-modify-write operations, which the hardware performs at the
+// device-wide coherence point (not in an XCD's private L2).  A publisher
+// waits for its payload RMW to complete (s_waitcnt) before it bumps the
+// arrival counter; the last arriver reads (and clears) the payloads with RMWs
+// issued after its counter RMW returned.  Release/acquire fences would instead
+// write back and invalidate the whole L2 of the XCD on every arrival.
 // ---------------------------------------------------------------------------
-__device__ inline void store_relaxed(uint32_t* p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// The publishing RMWs return their old value (consumed by an empty asm) so
+// that the hardware reports their completion to the waiting s_waitcnt.
+__device__ inline void publish_u32(uint32_t* p, uint32_t v) {
+    uint32_t old = __hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("" ::"v"(old));
+}
+__device__ inline uint32_t take_u32(uint32_t* p) {  // read and clear
+    return __hip_atomic_exchange(p, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void publish_f64(double* p, double v) {
+    double old = __hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("" ::"v"(old));
+}
+__device__ inline double take_f64(double* p) {
+    return __hip_atomic_exchange(p, 0.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ inline uint32_t load_relaxed(const uint32_t* p) {
     return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline void store_relaxed(double* p, double v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline double load_relaxed(const double* p) {
-    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+// Arrive at a counter; returns the number of earlier arrivals.  The caller's
+// payload RMWs have completed before the add is issued.
 __device__ inline uint32_t arrive(uint32_t* counter) {
-    return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    wait_memory();
+    const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    wait_memory();
+    return prev;
 }
 
 }  // namespace osd

@@ -56,6 +56,8 @@ struct DistillLaunch {
 };
 
 constexpr int kSlabRows = 64;
+// Row counts up to this are reduced in one level (see distill.hip).
+constexpr int kOneLevelRows = 1024;
 
 // Largest V handled by the row-resident tiles for a chunk of `per_chunk`
 // elements.

@@ -7,39 +7,55 @@
 // from norm(max(0, p - q)) at row a, or from p at the bonus row when all k
 // were accepted.  p and q are temperature softmaxes of the logits.
 //
-// Layout of the work: one workgroup per (sequence b, row i), rows 0..k_b;
-// workgroups are numbered position-major so that earlier positions dispatch
-// first.  A workgroup reads its target row (and draft row for i < k_b) from
-// HBM exactly once into registers, reduces the row maximum and the sum of
-// exponentials, decides acceptance, and -- when its own position rejects and
-// no earlier position of the sequence is known to have rejected -- draws the
-// correction token from the row it already holds.  The bonus workgroup draws
-// from p.  Each workgroup publishes a one-word record; the last of the k_b + 1
-// workgroups of a sequence to arrive selects the first rejection, writes the
-// outputs and clears the records and the arrival counter for the next call.
+// Work layout.  One workgroup per (sequence b, proposal row i), numbered
+// position-major, then one workgroup per bonus row.  A proposal workgroup
+// reads its target and draft rows from HBM exactly once into registers,
+// reduces the row maxima and sums of exponentials, and takes the acceptance
+// test.  A rejecting workgroup announces the rejection at once, then learns
+// (by polling the records of the earlier positions of its sequence, with a
+// bounded number of polls) whether it is the first rejection; only the first
+// draws the correction token, from the rows it already holds.  If the polls
+// run out it draws anyway, which is always correct.  A bonus workgroup first
+// checks whether an earlier position has already rejected and, if so, skips
+// its row entirely.  Every workgroup publishes a one-word record; the last of
+// the k_b + 1 workgroups of a sequence to arrive selects the first rejection,
+// writes the outputs, and clears the records and the counter.
 #include "osd_device.hpp"
 #include "osd_internal.hpp"
 
 namespace osd {
 namespace {
 
-// Record word: state in bits 31..29, token in bits 28..0.
+// Record word: state in bits 31..28, token in bits 27..0.
 enum : uint32_t {
     kRecEmpty = 0,
     kRecAccept = 1,
-    kRecReject = 2,         // rejected, correction token attached
-    kRecRejectSkipped = 3,  // rejected after an earlier rejection was seen
-    kRecBadRow = 4,         // no finite logit in a row that was read
-    kRecBadToken = 5,       // proposal outside [0, V)
-    kRecBonus = 6,          // bonus token attached
-    kRecBonusSkipped = 7,   // an earlier rejection was seen
+    kRecReject = 2,          // rejected, correction token attached
+    kRecRejectSkipped = 3,   // rejected after an earlier rejection was seen
+    kRecBadRow = 4,          // no finite logit in a row that was read
+    kRecBadToken = 5,        // proposal outside [0, V)
+    kRecBonus = 6,           // bonus token attached
+    kRecBonusSkipped = 7,    // an earlier rejection was seen
+    kRecRejectPending = 8,   // rejected, correction not yet decided
 };
 
 __device__ inline uint32_t make_rec(uint32_t state, uint32_t tok) {
-    return (state << 29) | (tok & 0x1FFFFFFFu);
+    return (state << 28) | (tok & 0x0FFFFFFFu);
 }
-__device__ inline uint32_t rec_state(uint32_t r) { return r >> 29; }
-__device__ inline int rec_token(uint32_t r) { return int(r & 0x1FFFFFFFu); }
+__device__ inline uint32_t rec_state(uint32_t r) { return r >> 28; }
+__device__ inline int rec_token(uint32_t r) { return int(r & 0x0FFFFFFFu); }
+__device__ inline bool rejects(uint32_t s) {
+    return s == kRecReject || s == kRecRejectSkipped || s == kRecRejectPending || s == kRecBadToken;
+}
+
+// Residual masses are handled in units of S_t (the target row's sum of
+// exponentials), where every element is at most about 1: chunk sums stay
+// below 16 and row totals below 2^17, so a 2^-44 fixed point never overflows.
+constexpr int kFixedShift = 44;
+// Polls of the earlier positions' records before a rejecting workgroup draws
+// speculatively.  Each poll is one device-coherent round trip plus a short
+// sleep; the bound keeps every wait finite whatever the dispatch order.
+constexpr int kMaxPolls = 24;
 
 struct VerifyArgs {
     const void* target;
@@ -49,8 +65,8 @@ struct VerifyArgs {
     const int32_t* draft_len;
     const float* u_accept;
     const float* u_resample;
-    float c2;       // log2(e) / T
-    double inv_T;   // 1 / T in fp64 for the acceptance test
+    float c2;        // log2(e) / T, the scale of every exponent
+    double c2d;      // the same value in fp64
     int32_t* accepted_len;
     int32_t* out_tokens;
     uint8_t* reject_mask;
@@ -68,25 +84,25 @@ __device__ void write_invalid(const VerifyArgs& a, int b) {
 }
 
 // Executed by all 64 lanes of one wave with the same `record`: publish this
-// row's record, and if it is the last of the k_b + 1 rows of sequence b to
-// arrive, emit the outputs.  Lane j handles position j (K < 64).
+// row's final record, and if it is the last of the k_b + 1 rows of sequence b
+// to arrive, emit the outputs.  Lane j handles position j (K < 64).
 __device__ void publish(const VerifyArgs& a, int b, int i, int kb, uint32_t record) {
     const int K = a.K;
     const int lane = threadIdx.x & (kWave - 1);
     uint32_t* recs = a.records + int64_t(b) * (K + 1);
     uint32_t prev = 0;
     if (lane == 0) {
-        store_relaxed(&recs[i], record);
+        publish_u32(&recs[i], record);
         prev = arrive(&a.counters[b]);
     }
     prev = __shfl(prev, 0, kWave);
     if (prev != uint32_t(kb)) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     // First rejection (Appendix A.1: the test stops there).  A proposal
     // outside the vocabulary invalidates the sequence wherever it sits; a row
-    // without finite logits only if the test reaches it.
-    const uint32_t r = lane <= kb ? load_relaxed(&recs[lane]) : 0u;
+    // without finite logits only if the test reaches it.  Records are read
+    // and cleared in one step.
+    const uint32_t r = lane <= kb ? take_u32(&recs[lane]) : 0u;
     const uint32_t s = rec_state(r);
     const bool bad_token = __ballot(lane < kb && s == kRecBadToken) != 0;
     const uint64_t stop = __ballot(lane < kb && s != kRecAccept);
@@ -100,7 +116,7 @@ __device__ void publish(const VerifyArgs& a, int b, int i, int kb, uint32_t reco
         if (acc < kb ? sa == kRecReject : sa == kRecBonus)
             extra = rec_token(ra);
         else
-            bad = true;  // a row without finite logits, or an inconsistency
+            bad = true;  // a row without finite logits
     }
     const int32_t* y = a.tokens + int64_t(b) * K;
     if (lane <= K) {
@@ -110,19 +126,25 @@ __device__ void publish(const VerifyArgs& a, int b, int i, int kb, uint32_t reco
         if (a.reject_mask && lane < K)
             a.reject_mask[int64_t(b) * K + lane] = (!bad && lane == acc && acc < kb) ? 1 : 0;
     }
-    if (lane == 0) a.accepted_len[b] = bad ? -1 : acc;
-    if (lane <= kb) store_relaxed(&recs[lane], 0u);
-    if (lane == 0) store_relaxed(&a.counters[b], 0u);
+    if (lane == 0) {
+        a.accepted_len[b] = bad ? -1 : acc;
+        take_u32(&a.counters[b]);
+    }
 }
 
-// Has an earlier position of this sequence already been seen to reject?
-// Called by all lanes of a wave; the answer is uniform.
-__device__ bool earlier_rejection_seen(const VerifyArgs& a, int b, int i) {
+// Called by all lanes of a wave.  Looks at the records of positions 0..i-1:
+// returns 2 if one of them rejected (or proposed an invalid token), 1 if all
+// accepted, 0 if still undecided after `polls` looks.
+__device__ int poll_earlier(const VerifyArgs& a, int b, int i, int polls) {
     const int lane = threadIdx.x & (kWave - 1);
     const uint32_t* recs = a.records + int64_t(b) * (a.K + 1);
-    uint32_t s = kRecEmpty;
-    if (lane < i) s = rec_state(load_relaxed(&recs[lane]));
-    return __ballot(s == kRecReject || s == kRecRejectSkipped) != 0;
+    for (int p = 0;; ++p) {
+        const uint32_t s = lane < i ? rec_state(load_relaxed(&recs[lane])) : uint32_t(kRecAccept);
+        if (__ballot(rejects(s)) != 0) return 2;
+        if (__ballot(s != kRecAccept) == 0) return 1;
+        if (p + 1 >= polls) return 0;
+        __builtin_amdgcn_s_sleep(8);
+    }
 }
 
 struct DrawShared {
@@ -136,10 +158,10 @@ struct DrawShared {
 // *z_zero is set (uniformly) when the total mass is zero.
 //
 // Token order is (round n, wave w, lane, element e).  Chunk masses are summed
-// left to right in fp32 and converted exactly to 2^-62 fixed point, so every
-// partial sum below is an exact integer and the CDF cells (n, w) partition
-// [0, Z) without gaps or overlaps whatever the reduction order.  The winning
-// wave stages its chunks through LDS (s_stage, 2*CPT*64 chunks) so that the
+// left to right in fp32 and converted exactly to fixed point, so every partial
+// sum below is an exact integer and the CDF cells (n, w) partition [0, Z)
+// without gaps or overlaps whatever the reduction order.  The winning wave
+// stages its chunks through LDS (s_stage, 2*CPT*64 chunks) so that the
 // winning round is selected by address, never by register index.
 template <int W, int CPT, int EPC, typename MassFn>
 __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CPT], MassFn mass,
@@ -154,7 +176,7 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
         float s = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) s = s + mass(tv[n], dv[n], e);
-        const uint64_t t = wave_sum(mass_to_fixed(s));
+        const uint64_t t = wave_sum(mass_to_fixed<kFixedShift>(s));
         if (lane == 0) s_tot[n * NW + wid] = t;
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -205,7 +227,7 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
         m[e] = mass(tc, dc, e);
         s = s + m[e];
     }
-    const uint64_t v = mass_to_fixed(s);
+    const uint64_t v = mass_to_fixed<kFixedShift>(s);
     const uint64_t incl = wave_inclusive_scan(v);
     const uint64_t lo = incl - v;
     const uint64_t target = s_draw->target;
@@ -218,10 +240,41 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
     for (int e = 0; e < EPC; ++e) {
         run = run + m[e];
         if (m[e] > 0.0f) last_pos = e;
-        if (pick < 0 && mass_to_fixed(run) > want) pick = e;
+        if (pick < 0 && mass_to_fixed<kFixedShift>(run) > want) pick = e;
     }
     if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
     return (nstar * W + tid) * EPC + pick;
+}
+
+// Row maximum of register-resident chunks.
+template <typename Fmt, int CPT>
+__device__ inline float row_max(const chunk_t (&c)[CPT]) {
+    float m = kNegInf;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n)
+#pragma unroll
+        for (int e = 0; e < Fmt::kPerChunk; ++e) m = fmaxf(m, Fmt::get(c[n], e));
+    return m;
+}
+
+// Sum of 2^(x c2 - mc) over register-resident chunks, pairwise within a chunk.
+template <typename Fmt, int CPT>
+__device__ inline float row_sum_exp(const chunk_t (&c)[CPT], float c2, float mc) {
+    constexpr int EPC = Fmt::kPerChunk;
+    float s = 0.0f;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        float e8[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(c[n], e), c2, -mc));
+#pragma unroll
+        for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+            for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+        s = s + e8[0];
+        __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
+    }
+    return s;
 }
 
 template <typename Fmt, int W, int CPT, bool VEC, bool GREEDY>
@@ -239,19 +292,40 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
 
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const int B = a.B, K = a.K, V = a.V;
-    const int i = blockIdx.x / B;
-    const int b = blockIdx.x - i * B;
+    const bool bonus = int(blockIdx.x) >= B * K;
+    int b, i;
+    if (!bonus) {
+        i = blockIdx.x / B;
+        b = blockIdx.x - i * B;
+    } else {
+        b = blockIdx.x - B * K;
+        i = -1;
+    }
     const int kb = a.draft_len ? a.draft_len[b] : K;
     if (kb < 1 || kb > K) {
-        if (i == 0) write_invalid(a, b);
+        if (bonus) write_invalid(a, b);
         return;
     }
-    if (i > kb) return;  // padding row of a short proposal
-    const bool bonus = i == kb;
+    if (bonus) {
+        i = kb;
+    } else if (i >= kb) {
+        return;  // padding row of a short proposal
+    }
     const int y = bonus ? 0 : a.tokens[int64_t(b) * K + i];
     if (!bonus && (y < 0 || y >= V)) {
         if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadToken, 0));
         return;
+    }
+    if (bonus) {
+        // The bonus row matters only if every proposal is accepted: skip it
+        // when a rejection is already visible.
+        if (wid == 0) {
+            const int st = poll_earlier(a, b, i, 1);
+            if (lane == 0) s_flag = st;
+            if (st == 2) publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
+        }
+        __syncthreads();
+        if (s_flag == 2) return;
     }
 
     const char* trow = static_cast<const char*>(a.target) +
@@ -305,7 +379,6 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
         const char* drow = static_cast<const char*>(a.draft) +
                            (int64_t(b) * K + i) * int64_t(V) * Fmt::kBytes;
         if (!bonus) load_row<Fmt, W, CPT, VEC>(dv, drow, V);
-
         // The logits of the proposal itself, for the acceptance test.
         float ty = 0.0f, dy = 0.0f;
         if (!bonus) {
@@ -314,19 +387,8 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
         }
 
         // Pass 1: row maxima.
-        float mt = kNegInf, md = kNegInf;
-#pragma unroll
-        for (int n = 0; n < CPT; ++n)
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) mt = fmaxf(mt, Fmt::get(tv[n], e));
-        if (!bonus) {
-#pragma unroll
-            for (int n = 0; n < CPT; ++n)
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) md = fmaxf(md, Fmt::get(dv[n], e));
-        }
-        mt = wave_max(mt);
-        md = wave_max(md);
+        float mt = wave_max(row_max<Fmt, CPT>(tv));
+        float md = bonus ? kNegInf : wave_max(row_max<Fmt, CPT>(dv));
         if (lane == 0) {
             s_max[0][wid] = mt;
             s_max[1][wid] = md;
@@ -346,42 +408,25 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
             if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadRow, 0));
             return;
         }
+        // Exponents are x c2 - m c2 (one fma): the shift is common to every
+        // term of a row, so it cancels in every normalised quantity.
+        const float mtc = mt * c2, mdc = md * c2;
 
-        // Pass 2: sums of exponentials, pairwise within a chunk.
+        // Pass 2: S = sum 2^(x c2 - m c2) for each row.
         opaque(tv);
-        if (!bonus) opaque(dv);
-        float st = 0.0f, sd = 0.0f;
-#pragma unroll
-        for (int n = 0; n < CPT; ++n) {
-            float e8[EPC];
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast((Fmt::get(tv[n], e) - mt) * c2);
-#pragma unroll
-            for (int w = 1; w < EPC; w <<= 1)
-#pragma unroll
-                for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
-            st = st + e8[0];
-            __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
-        }
+        const float st = row_sum_exp<Fmt, CPT>(tv, c2, mtc);
+        float sd = 0.0f;
         if (!bonus) {
-#pragma unroll
-            for (int n = 0; n < CPT; ++n) {
-                float e8[EPC];
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast((Fmt::get(dv[n], e) - md) * c2);
-#pragma unroll
-                for (int w = 1; w < EPC; w <<= 1)
-#pragma unroll
-                    for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
-                sd = sd + e8[0];
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            opaque(dv);
+            sd = row_sum_exp<Fmt, CPT>(dv, c2, mdc);
         }
-        const double dst = wave_sum(double(st));
-        const double dsd = wave_sum(double(sd));
-        if (lane == 0) {
-            s_sum[0][wid] = dst;
-            s_sum[1][wid] = dsd;
+        {
+            const double dst = wave_sum(double(st));
+            const double dsd = wave_sum(double(sd));
+            if (lane == 0) {
+                s_sum[0][wid] = dst;
+                s_sum[1][wid] = dsd;
+            }
         }
         __syncthreads();
         double St = 0.0, Sd = 0.0;
@@ -392,30 +437,30 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
 
         // Wave 0 decides whether this workgroup draws a token.
         if (wid == 0) {
-            int flag;
+            int flag = 1;
             if (!bonus) {
-                // Acceptance test in fp64 on the gathered logits:
-                // log p(y) - log q(y) = ((t_y - m_t) - (d_y - m_d)) / T - (ln S_t - ln S_d).
-                const double L = ((double(ty) - double(mt)) - (double(dy) - double(md))) * a.inv_T -
-                                 (log(St) - log(Sd));
-                const double ratio = exp(L);
+                // Acceptance test in fp64, in the log2 units of the sums:
+                // log2 p(y) - log2 q(y) = (t_y c2 - m_t c2 - log2 S_t) - (d_y c2 - m_d c2 - log2 S_d).
+                const double L2 = (double(ty) * a.c2d - double(mtc) - log2(St)) -
+                                  (double(dy) * a.c2d - double(mdc) - log2(Sd));
+                const double ratio = exp2(L2);
                 const double u = a.u_accept[int64_t(b) * K + i];
                 if (u < ratio) {
                     flag = 0;
                     publish(a, b, i, kb, make_rec(kRecAccept, 0));
-                } else if (earlier_rejection_seen(a, b, i)) {
-                    flag = 0;
-                    publish(a, b, i, kb, make_rec(kRecRejectSkipped, 0));
                 } else {
-                    flag = 1;
+                    // Announce the rejection, then find out whether it is the
+                    // first one of the sequence.
+                    if (lane == 0)
+                        publish_u32(a.records + int64_t(b) * (K + 1) + i, make_rec(kRecRejectPending, 0));
+                    if (i > 0 && poll_earlier(a, b, i, kMaxPolls) == 2) {
+                        flag = 0;
+                        publish(a, b, i, kb, make_rec(kRecRejectSkipped, 0));
+                    }
                 }
-            } else {
-                if (earlier_rejection_seen(a, b, i)) {
-                    flag = 0;
-                    publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
-                } else {
-                    flag = 1;
-                }
+            } else if (poll_earlier(a, b, i, kMaxPolls) == 2) {
+                flag = 0;
+                publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
             }
             if (lane == 0) s_flag = flag;
         }
@@ -424,25 +469,25 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
 
         // Draw the extra token: from max(0, p - q) after a rejection, from p
         // at the bonus row (and, should max(0, p - q) have no mass after
-        // rounding, from p as well).
-        const float inv_st = float(1.0 / St);
-        const float inv_sd = bonus ? 0.0f : float(1.0 / Sd);
+        // rounding, from p as well).  Masses are in units of S_t:
+        //   p_j S_t = 2^(t_j c2 - m_t c2),  q_j S_t = 2^(d_j c2 - m_d c2) (S_t / S_d).
+        const float rho = bonus ? 0.0f : float(St / Sd);
         const float u = a.u_resample[b];
         bool use_p = bonus;
         for (int attempt = 0; attempt < 2; ++attempt) {
-            // Opaque copies of the maxima, fresh in each attempt: without them
+            // Opaque copies of the shifts, fresh in each attempt: without them
             // the compiler keeps the exponentials of pass 2 (or of the first
             // attempt) alive in order to reuse them, and spills.
-            float mt_d = mt, md_d = md;
-            asm volatile("" : "+v"(mt_d), "+v"(md_d));
+            float mtc_d = mtc, mdc_d = mdc;
+            asm volatile("" : "+v"(mtc_d), "+v"(mdc_d));
             opaque(tv);
             if (!use_p) opaque(dv);
             const bool p_only = use_p;
             auto mass = [=](const chunk_t& tc, const chunk_t& dc, int e) -> float {
-                const float p = exp2_fast((Fmt::get(tc, e) - mt_d) * c2) * inv_st;
-                if (p_only) return p;
-                const float q = exp2_fast((Fmt::get(dc, e) - md_d) * c2) * inv_sd;
-                return fmaxf(p - q, 0.0f);
+                const float pt = exp2_fast(__builtin_fmaf(Fmt::get(tc, e), c2, -mtc_d));
+                if (p_only) return pt;
+                const float qt = exp2_fast(__builtin_fmaf(Fmt::get(dc, e), c2, -mdc_d));
+                return fmaxf(__builtin_fmaf(-qt, rho, pt), 0.0f);
             };
             bool z_zero = false;
             const int tok = draw_inverse_cdf<W, CPT, EPC>(tv, dv, mass, u, s_tot, &s_draw, s_stage, &z_zero);
@@ -524,7 +569,7 @@ hipError_t launch_verify(const VerifyLaunch& L) {
     a.u_accept = L.u_accept;
     a.u_resample = L.u_resample;
     a.c2 = L.temperature > 0.0f ? float(1.4426950408889634 / double(L.temperature)) : 0.0f;
-    a.inv_T = L.temperature > 0.0f ? 1.0 / double(L.temperature) : 0.0;
+    a.c2d = double(a.c2);
     a.accepted_len = L.accepted_len;
     a.out_tokens = L.out_tokens;
     a.reject_mask = L.reject_mask;

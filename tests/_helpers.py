@@ -68,6 +68,14 @@ def compare_grad_bf16(gpu_bits, ref_f64, label=""):
     bad = (err > BF16_GRAD_ATOL) & ~mid
     assert not bad.any(), (f"{label}: {int(bad.sum())} gradient elements off by > 2e-3, "
                            f"max {float(err[~mid].max())}")
+    # Where |g| >= 1e-2 the fp32 arithmetic is accurate to well under 2^-14
+    # relative (no cancellation to speak of), so away from that band around a
+    # rounding midpoint the kernel's round-to-nearest-even must land on the
+    # very same bf16 value: this catches a wrong rounding mode.
+    wide = oref.bf16_midpoint_flags(ref_f64, rel=2.0 ** -14)
+    flips = (g != w) & ~wide & np.isfinite(ref_f64) & (np.abs(ref_f64) >= 1e-2)
+    assert not flips.any(), (f"{label}: {int(flips.sum())} gradient elements not the RNE bf16 "
+                             f"of the exact value (first at {np.argwhere(flips)[0].tolist()})")
     return int(mid.sum())
 
 

@@ -320,3 +320,22 @@ def test_workspaces_left_zero_across_shapes(osd):
         torch.cuda.synchronize()
         for key, ws in binding._workspaces.items():
             assert int(ws.count_nonzero()) == 0, key
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", ["fkl", "rkl", "jsd"])
+def test_distill_neg_inf_entries(osd, kind, dtype):
+    """-inf logits (probability 0) at the same vocabulary positions of teacher
+    and student: 0 log 0 = 0, finite losses, zero gradient there."""
+    g = np.random.default_rng(17)
+    B, K, V = 2, 3, 4096
+    t = g.normal(0, 2, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    holes = g.random((B, K, V)) < 0.2
+    t[holes] = -np.inf
+    s[holes] = -np.inf
+    mask = np.ones((B, K), np.uint8)
+    tt, ss = (synth.to_bf16(t), synth.to_bf16(s)) if dtype == "bf16" else (t, s)
+    _, _, grad = check_distill(osd, tt, ss, kind, 0.5, 0.9, mask, f"-inf {kind} {dtype}")
+    gg = synth.bf16_to_f32(grad) if dtype == "bf16" else grad
+    assert np.all(gg[holes] == 0)
