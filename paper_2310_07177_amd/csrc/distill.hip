@@ -169,18 +169,8 @@ constexpr float kLogFloor = -1.0e30f;
 // v_log_f32 stays finite when both p and q underflow).
 constexpr float kMixFloor = 1.0e-37f;
 
-template <typename Fmt, int CPT>
-__device__ inline float row_max(const chunk_t (&c)[CPT]) {
-    float m = kNegInf;
-#pragma unroll
-    for (int n = 0; n < CPT; ++n)
-#pragma unroll
-        for (int e = 0; e < Fmt::kPerChunk; ++e) m = fmaxf(m, Fmt::get(c[n], e));
-    return m;
-}
-
 template <typename Fmt, int W, int CPT, bool VEC, int KIND>
-__global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
+__global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(DistillArgs a) {
     constexpr int NW = W / kWave;
     constexpr int EPC = Fmt::kPerChunk;
     __shared__ float s_max[2][NW];
@@ -210,87 +200,49 @@ __global__ __launch_bounds__(W, 4) void distill_kernel(DistillArgs a) {
         load_row<Fmt, W, CPT, VEC>(sv, srow, V);
         const float c2 = a.c2;
 
-        // Row maxima.
-        float mt = wave_max(row_max<Fmt, CPT>(tv));
-        float ms = wave_max(row_max<Fmt, CPT>(sv));
-        if (lane == 0) {
-            s_max[0][wid] = mt;
-            s_max[1][wid] = ms;
-        }
-        __syncthreads();
-        mt = s_max[0][0];
-        ms = s_max[1][0];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) {
-            mt = fmaxf(mt, s_max[0][w]);
-            ms = fmaxf(ms, s_max[1][w]);
-        }
-        // Exponents are x c2 - m c2 (one fma); the shift cancels on normalising.
-        const float mtc = mt * c2, msc = ms * c2;
-
-        // Sums of exponentials.  FKL and RKL are first-order sensitive to the
-        // normaliser (an error s in S shifts every log-ratio by s), so they
-        // accumulate every term in fp64; JSD is not (the mixture absorbs a
-        // common scale error), so it sums pairwise in fp32 within a chunk.
-        opaque(tv);
-        opaque(sv);
-        double dst = 0.0, dss = 0.0;
-        if constexpr (KIND == 2) {
-            float st = 0.0f, ss = 0.0f;
-#pragma unroll
-            for (int c = 0; c < CPT; ++c) {
-                float et[EPC], es[EPC];
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    et[e] = exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e), c2, -mtc));
-                    es[e] = exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e), c2, -msc));
-                }
-#pragma unroll
-                for (int w = 1; w < EPC; w <<= 1)
-#pragma unroll
-                    for (int e = 0; e < EPC; e += 2 * w) {
-                        et[e] = et[e] + et[e + w];
-                        es[e] = es[e] + es[e + w];
-                    }
-                st = st + et[0];
-                ss = ss + es[0];
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            dst = st;
-            dss = ss;
-        } else {
-            double t0 = 0.0, t1 = 0.0, s0 = 0.0, s1 = 0.0;
-#pragma unroll
-            for (int c = 0; c < CPT; ++c) {
-#pragma unroll
-                for (int e = 0; e < EPC; e += 2) {
-                    t0 += double(exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e), c2, -mtc)));
-                    t1 += double(exp2_fast(__builtin_fmaf(Fmt::get(tv[c], e + 1), c2, -mtc)));
-                    s0 += double(exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e), c2, -msc)));
-                    s1 += double(exp2_fast(__builtin_fmaf(Fmt::get(sv[c], e + 1), c2, -msc)));
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            dst = t0 + t1;
-            dss = s0 + s1;
-        }
+        // Row statistics (K, S), folded in chunk by chunk as the loads land.
+        // FKL and RKL are first-order sensitive to the normaliser (an error s
+        // in S shifts every log-ratio by s), so they accumulate every term in
+        // fp64; JSD is not (the mixture absorbs a common scale error), so it
+        // sums pairwise in fp32 within a chunk.
+        float Kt = kNegInf, Ks = kNegInf;
         {
-            const double dt = wave_sum(dst);
-            const double ds = wave_sum(dss);
+            double dt = 0.0, ds = 0.0;
+            if constexpr (KIND == 2) {
+                float ft = 0.0f, fs = 0.0f;
+                row_stats<Fmt, CPT>(tv, c2, Kt, ft);
+                row_stats<Fmt, CPT>(sv, c2, Ks, fs);
+                dt = ft;
+                ds = fs;
+            } else {
+                row_stats<Fmt, CPT>(tv, c2, Kt, dt);
+                row_stats<Fmt, CPT>(sv, c2, Ks, ds);
+            }
+            wave_merge_stats(Kt, dt);
+            wave_merge_stats(Ks, ds);
             if (lane == 0) {
+                s_max[0][wid] = Kt;
+                s_max[1][wid] = Ks;
                 s_sum[0][wid] = dt;
                 s_sum[1][wid] = ds;
             }
         }
         __syncthreads();
+        Kt = s_max[0][0];
+        Ks = s_max[1][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            Kt = fmaxf(Kt, s_max[0][w]);
+            Ks = fmaxf(Ks, s_max[1][w]);
+        }
         double St = 0.0, Ss = 0.0;
         for (int w = 0; w < NW; ++w) {
-            St += s_sum[0][w];
-            Ss += s_sum[1][w];
+            St += rescale(s_sum[0][w], s_max[0][w], Kt);
+            Ss += rescale(s_sum[1][w], s_max[1][w], Ks);
         }
-        // log2 p_j = t_j c2 - (m_t c2 + log2 S_t) and p_j = 2^(log2 p_j): one
+        // log2 p_j = t_j c2 - (K_t + log2 S_t) and p_j = 2^(log2 p_j): one
         // fma and one exponential per element; likewise for q.
-        const double ktd = double(mtc) + log2(St), ksd = double(msc) + log2(Ss);
+        const double ktd = double(Kt) + log2(St), ksd = double(Ks) + log2(Ss);
         const float kt = float(ktd), ks = float(ksd);
         // log2(p_j / q_j) = (t_j - s_j) c2 - (k_t - k_s): the difference of the
         // two constants is taken in fp64, so the loss of FKL and RKL carries no

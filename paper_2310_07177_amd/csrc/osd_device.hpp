@@ -21,6 +21,13 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLn2 = 0.69314718055994530942;
 
 // ---------------------------------------------------------------------------
+// Exponentials.  v_exp_f32 computes 2^x; scaled logits are formed as
+// (x - max) * log2(e)/T so that the term carrying the mass is exact-ish.
+// ---------------------------------------------------------------------------
+__device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ inline float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
+
+// ---------------------------------------------------------------------------
 // Logit formats
 // ---------------------------------------------------------------------------
 struct BF16 {
@@ -159,6 +166,86 @@ __device__ inline void wave_argmax(float& v, int& idx) {
 }
 
 // ---------------------------------------------------------------------------
+// Streaming softmax statistics of a register-resident row.
+//
+// Each thread keeps S = sum_j 2^(x_j c2 - K) over its elements, where c2 =
+// log2(e)/T and the shift K is a whole number at least ceil(max_j x_j c2).
+// Chunks are folded in as their loads land (no barrier between the maximum
+// and the sum); raising K rescales S by an exact power of two (ldexp), so
+// the statistics carry no rounding from the shift.  Lanes and waves merge
+// the same way.  A row without finite logits ends with K = -inf, S = 0.
+// ---------------------------------------------------------------------------
+template <typename Fmt>
+__device__ inline float chunk_max(const chunk_t& c) {
+    float m = Fmt::get(c, 0);
+#pragma unroll
+    for (int e = 1; e < Fmt::kPerChunk; ++e) m = fmaxf(m, Fmt::get(c, e));
+    return m;
+}
+
+// 2^(from - to) * S for whole numbers from <= to (exact; -inf/NaN -> 0).
+__device__ inline float rescale(float S, float from, float to) {
+    return __builtin_ldexpf(S, int(fmaxf(from - to, -256.0f)));
+}
+__device__ inline double rescale(double S, float from, float to) {
+    return __builtin_ldexp(S, int(fmaxf(from - to, -2048.0f)));
+}
+
+// fp32 accumulation, pairwise within a chunk.
+template <typename Fmt, int CPT>
+__device__ inline void row_stats(const chunk_t (&c)[CPT], float c2, float& K, float& S) {
+    constexpr int EPC = Fmt::kPerChunk;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(c[n]) * c2));
+        S = rescale(S, K, kn);
+        K = kn;
+        // While K is still -inf every element seen is -inf: a finite stand-in
+        // keeps 2^(x c2 - K) at 2^-inf = 0 instead of -inf + inf = NaN.
+        const float kx = fmaxf(K, -3.0e38f);
+        float e8[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(c[n], e), c2, -kx));
+#pragma unroll
+        for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+            for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+        S = S + e8[0];
+        __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
+    }
+}
+
+// fp64 accumulation of every term (for quantities first-order sensitive to
+// the normaliser).
+template <typename Fmt, int CPT>
+__device__ inline void row_stats(const chunk_t (&c)[CPT], float c2, float& K, double& S) {
+    constexpr int EPC = Fmt::kPerChunk;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(c[n]) * c2));
+        S = rescale(S, K, kn);
+        K = kn;
+        const float kx = fmaxf(K, -3.0e38f);  // see the fp32 version
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int e = 0; e < EPC; e += 2) {
+            s0 += double(exp2_fast(__builtin_fmaf(Fmt::get(c[n], e), c2, -kx)));
+            s1 += double(exp2_fast(__builtin_fmaf(Fmt::get(c[n], e + 1), c2, -kx)));
+        }
+        S += s0 + s1;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Merge (K, S) across the wave; every lane returns the wave's pair.
+template <typename Acc>
+__device__ inline void wave_merge_stats(float& K, Acc& S) {
+    const float kw = wave_max(K);
+    S = wave_sum(rescale(S, K, kw));
+    K = kw;
+}
+
+// ---------------------------------------------------------------------------
 // Fixed-point probability mass.  A non-negative fp32 value x < 2^(63-SH) maps
 // to floor(x * 2^SH); the conversion is exact for x >= 2^(23-SH) (the
 // mantissa is shifted, not rounded).  Integer sums of such values are
@@ -175,13 +262,6 @@ __device__ inline uint64_t mass_to_fixed(float x) {
     if (sh <= -64) return 0;
     return m >> (-sh);
 }
-
-// ---------------------------------------------------------------------------
-// Exponentials.  v_exp_f32 computes 2^x; scaled logits are formed as
-// (x - max) * log2(e)/T so that the term carrying the mass is exact-ish.
-// ---------------------------------------------------------------------------
-__device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ inline float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
 
 // Two fp32 values to a packed pair of bf16, round to nearest even, with the
 // native v_cvt_pk_bf16_f32 of gfx950.

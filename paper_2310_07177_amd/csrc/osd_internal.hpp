@@ -15,6 +15,12 @@ struct RowTile {
     int CPT;
 };
 
+// Occupancy target of a row-resident tile (waves per SIMD the compiler must
+// leave room for): 4, i.e. up to 128 VGPRs -- two 512-thread workgroups or
+// one 1024-thread workgroup per CU.  (Eight waves per SIMD would cap a wave at
+// 64 VGPRs, and the spills that forces cost more than the occupancy gains.)
+constexpr int min_waves_per_simd(int W, int CPT) { return (void)W, (void)CPT, 4; }
+
 struct VerifyLaunch {
     const void* target;
     const void* draft;

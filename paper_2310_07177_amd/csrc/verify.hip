@@ -246,39 +246,8 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
     return (nstar * W + tid) * EPC + pick;
 }
 
-// Row maximum of register-resident chunks.
-template <typename Fmt, int CPT>
-__device__ inline float row_max(const chunk_t (&c)[CPT]) {
-    float m = kNegInf;
-#pragma unroll
-    for (int n = 0; n < CPT; ++n)
-#pragma unroll
-        for (int e = 0; e < Fmt::kPerChunk; ++e) m = fmaxf(m, Fmt::get(c[n], e));
-    return m;
-}
-
-// Sum of 2^(x c2 - mc) over register-resident chunks, pairwise within a chunk.
-template <typename Fmt, int CPT>
-__device__ inline float row_sum_exp(const chunk_t (&c)[CPT], float c2, float mc) {
-    constexpr int EPC = Fmt::kPerChunk;
-    float s = 0.0f;
-#pragma unroll
-    for (int n = 0; n < CPT; ++n) {
-        float e8[EPC];
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(c[n], e), c2, -mc));
-#pragma unroll
-        for (int w = 1; w < EPC; w <<= 1)
-#pragma unroll
-            for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
-        s = s + e8[0];
-        __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
-    }
-    return s;
-}
-
 template <typename Fmt, int W, int CPT, bool VEC, bool GREEDY>
-__global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
+__global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(VerifyArgs a) {
     constexpr int NW = W / kWave;
     constexpr int EPC = Fmt::kPerChunk;
     __shared__ float s_max[2][NW];
@@ -386,64 +355,60 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
             dy = Fmt::load_one(drow, y);
         }
 
-        // Pass 1: row maxima.
-        float mt = wave_max(row_max<Fmt, CPT>(tv));
-        float md = bonus ? kNegInf : wave_max(row_max<Fmt, CPT>(dv));
-        if (lane == 0) {
-            s_max[0][wid] = mt;
-            s_max[1][wid] = md;
+        // Row statistics (K, S), folded in chunk by chunk as the loads land.
+        float Kt = kNegInf, Kd = kNegInf;
+        {
+            float st = 0.0f, sd = 0.0f;
+            row_stats<Fmt, CPT>(tv, c2, Kt, st);
+            if (!bonus) row_stats<Fmt, CPT>(dv, c2, Kd, sd);
+            double dt = st, dd = sd;
+            wave_merge_stats(Kt, dt);
+            wave_merge_stats(Kd, dd);
+            if (lane == 0) {
+                s_max[0][wid] = Kt;
+                s_max[1][wid] = Kd;
+                s_sum[0][wid] = dt;
+                s_sum[1][wid] = dd;
+            }
         }
         if (tid == 0) s_tok = -1;
         __syncthreads();
-        mt = s_max[0][0];
-        md = s_max[1][0];
+        Kt = s_max[0][0];
+        Kd = s_max[1][0];
 #pragma unroll
         for (int w = 1; w < NW; ++w) {
-            mt = fmaxf(mt, s_max[0][w]);
-            md = fmaxf(md, s_max[1][w]);
+            Kt = fmaxf(Kt, s_max[0][w]);
+            Kd = fmaxf(Kd, s_max[1][w]);
         }
-        const bool bad = !(mt > kNegInf) || mt == -kNegInf ||
-                         (!bonus && (!(md > kNegInf) || md == -kNegInf));
+        double St = 0.0, Sd = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            St += rescale(s_sum[0][w], s_max[0][w], Kt);
+            Sd += rescale(s_sum[1][w], s_max[1][w], Kd);
+        }
+        const bool bad = !(Kt > kNegInf && Kt < -kNegInf) ||
+                         (!bonus && !(Kd > kNegInf && Kd < -kNegInf));
         if (bad) {
             if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadRow, 0));
             return;
-        }
-        // Exponents are x c2 - m c2 (one fma): the shift is common to every
-        // term of a row, so it cancels in every normalised quantity.
-        const float mtc = mt * c2, mdc = md * c2;
-
-        // Pass 2: S = sum 2^(x c2 - m c2) for each row.
-        opaque(tv);
-        const float st = row_sum_exp<Fmt, CPT>(tv, c2, mtc);
-        float sd = 0.0f;
-        if (!bonus) {
-            opaque(dv);
-            sd = row_sum_exp<Fmt, CPT>(dv, c2, mdc);
-        }
-        {
-            const double dst = wave_sum(double(st));
-            const double dsd = wave_sum(double(sd));
-            if (lane == 0) {
-                s_sum[0][wid] = dst;
-                s_sum[1][wid] = dsd;
-            }
-        }
-        __syncthreads();
-        double St = 0.0, Sd = 0.0;
-        for (int w = 0; w < NW; ++w) {
-            St += s_sum[0][w];
-            Sd += s_sum[1][w];
         }
 
         // Wave 0 decides whether this workgroup draws a token.
         if (wid == 0) {
             int flag = 1;
             if (!bonus) {
-                // Acceptance test in fp64, in the log2 units of the sums:
-                // log2 p(y) - log2 q(y) = (t_y c2 - m_t c2 - log2 S_t) - (d_y c2 - m_d c2 - log2 S_d).
-                const double L2 = (double(ty) * a.c2d - double(mtc) - log2(St)) -
-                                  (double(dy) * a.c2d - double(mdc) - log2(Sd));
-                const double ratio = exp2(L2);
+                // Acceptance test: p(y)/q(y) = 2^e * S_d / S_t with
+                // e = (t_y c2 - K_t) - (d_y c2 - K_d) in fp64; 2^e is split
+                // into an exact power of two and 2^frac (v_exp_f32, 1 ulp).
+                const double e = (double(ty) * a.c2d - double(Kt)) - (double(dy) * a.c2d - double(Kd));
+                double ratio;
+                if (!(e > -2000.0)) {
+                    ratio = 0.0;  // p(y) = 0 (or both probabilities 0)
+                } else if (e > 2000.0) {
+                    ratio = __builtin_huge_val();
+                } else {
+                    const double n = floor(e);
+                    ratio = __builtin_ldexp(double(exp2_fast(float(e - n))), int(n)) * (Sd / St);
+                }
                 const double u = a.u_accept[int64_t(b) * K + i];
                 if (u < ratio) {
                     flag = 0;
@@ -470,15 +435,15 @@ __global__ __launch_bounds__(W, 4) void verify_kernel(VerifyArgs a) {
         // Draw the extra token: from max(0, p - q) after a rejection, from p
         // at the bonus row (and, should max(0, p - q) have no mass after
         // rounding, from p as well).  Masses are in units of S_t:
-        //   p_j S_t = 2^(t_j c2 - m_t c2),  q_j S_t = 2^(d_j c2 - m_d c2) (S_t / S_d).
+        //   p_j S_t = 2^(t_j c2 - K_t),  q_j S_t = 2^(d_j c2 - K_d) (S_t / S_d).
         const float rho = bonus ? 0.0f : float(St / Sd);
         const float u = a.u_resample[b];
         bool use_p = bonus;
         for (int attempt = 0; attempt < 2; ++attempt) {
             // Opaque copies of the shifts, fresh in each attempt: without them
-            // the compiler keeps the exponentials of pass 2 (or of the first
-            // attempt) alive in order to reuse them, and spills.
-            float mtc_d = mtc, mdc_d = mdc;
+            // the compiler may keep exponentials alive across passes (to reuse
+            // them) and spill.
+            float mtc_d = Kt, mdc_d = Kd;
             asm volatile("" : "+v"(mtc_d), "+v"(mdc_d));
             opaque(tv);
             if (!use_p) opaque(dv);
