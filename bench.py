@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--kernel-iters", type=int, default=400)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--only", default=None,
-                   help="profiling aid: run just one kernel loop (verify|greedy|jsd|rkl|copy)")
+                   help="profiling aid: run only the named loops, comma-separated (verify,greedy,jsd,rkl,copy)")
     return p.parse_args()
 
 
@@ -254,7 +254,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f32",
         "data": "synthetic (seeded; target ~ N(0,2.5^2), draft = 0.7 target + N(0,1.5^2))",
         "config": {"workload": "T5-vocab verify + JSD distill step", "B": B, "k": K, "V": V,
                    "logits": "bf16", "T": T_VERIFY, "tau": TAU, "beta": BETA, "mask": "all ones",
