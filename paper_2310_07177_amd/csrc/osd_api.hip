@@ -17,14 +17,20 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int per_chunk(int dtype) { return dtype == OSD_BF16 ? 8 : (dtype == OSD_F32 ? 4 : 0); }
 int elem_bytes(int dtype) { return dtype == OSD_BF16 ? 2 : 4; }
 
+// Counters and records of the row-resident kernel, then the segment
+// statistics and proposal logits of the segmented kernels.  Every call leaves
+// all of it zero.
 struct VerifyWs {
-    size_t records, counters, total;
+    size_t records, counters, stats, yv, total;
 };
 VerifyWs verify_layout(int B, int K) {
     VerifyWs w;
+    const size_t rows = size_t(B) * size_t(K + 1);
     w.counters = 0;
     w.records = round_up(size_t(B) * 4, kAlign);
-    w.total = w.records + round_up(size_t(B) * size_t(K + 1) * 4, kAlign);
+    w.stats = w.records + round_up(rows * 4, kAlign);
+    w.yv = w.stats + round_up(rows * osd::kMaxSeg * sizeof(osd::SegStats), kAlign);
+    w.total = w.yv + round_up(rows * 8, kAlign);
     return w;
 }
 
@@ -44,6 +50,23 @@ DistillWs distill_layout(int B, int K) {
     w.rows = w.slabs + round_up(size_t(w.nslabs) * 16, kAlign);
     w.total = w.rows + round_up(R * 8, kAlign);
     return w;
+}
+
+// Compute units of the device that runs `stream` (queried once per device).
+int device_cus(hipStream_t stream) {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (stream == nullptr || hipStreamGetDevice(stream, &dev) != hipSuccess) {
+        if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    }
+    if (dev < 0 || dev >= 64) dev = 0;
+    int n = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+    if (n <= 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        __atomic_store_n(&cache[dev], n, __ATOMIC_RELAXED);
+    }
+    return n;
 }
 
 bool sizes_ok(int B, int K, int V, int dtype) {
@@ -113,10 +136,15 @@ int osd_verify(const void* target_logits, const void* draft_logits, int dtype, i
     char* w = static_cast<char*>(workspace);
     L.records = reinterpret_cast<uint32_t*>(w + ws.records);
     L.counters = reinterpret_cast<uint32_t*>(w + ws.counters);
+    L.seg_stats = reinterpret_cast<osd::SegStats*>(w + ws.stats);
+    L.seg_y = reinterpret_cast<float*>(w + ws.yv);
     L.vec = (int64_t(V) * elem_bytes(dtype)) % 16 == 0 && aligned16(target_logits) &&
             (greedy || aligned16(draft_logits));
     L.stream = static_cast<hipStream_t>(stream);
-    return osd::launch_verify(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+    int cpt = 0, nseg = 0;
+    const bool segmented = L.vec && osd::pick_seg_cpt(V, per_chunk(dtype), &cpt, &nseg);
+    const hipError_t e = segmented ? osd::launch_verify_seg(L) : osd::launch_verify(L);
+    return e == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 
 size_t osd_distill_workspace_bytes(int B, int K) {
@@ -171,7 +199,11 @@ int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stri
             (student_batch_stride * eb) % 16 == 0 && aligned16(teacher_logits) &&
             aligned16(student_logits) && (grad_out == nullptr || aligned16(grad_out));
     L.stream = static_cast<hipStream_t>(stream);
-    return osd::launch_distill(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+    L.cus = device_cus(L.stream);
+    osd::RowTile t;
+    const bool streaming = L.vec && osd::pick_stream_tile(V, per_chunk(dtype), &t);
+    const hipError_t e = streaming ? osd::launch_distill_stream(L) : osd::launch_distill(L);
+    return e == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 
 }  // extern "C"

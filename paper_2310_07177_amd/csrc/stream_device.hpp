@@ -1,0 +1,243 @@
+// stream_device.hpp -- building blocks of the persistent streaming kernels
+// (gfx950, wave64).
+//
+// A persistent workgroup walks a list of rows.  Each thread owns the 16-byte
+// chunks n*W + tid (n = 0..CPT-1) of every row, so each round n is one
+// coalesced sweep over W*16 bytes.  Rows are read through buffer descriptors:
+// a descriptor of 0 bytes turns every load into a no-op that returns zeros
+// without touching memory, so the instruction stream is the same whether or
+// not the next row exists.  That keeps the hardware load counter in a fixed
+// order, which lets the compiler wait for exactly the chunk it needs while
+// the prefetch of the next row stays in flight.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "osd_device.hpp"
+
+namespace osd {
+
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Fourth descriptor word for raw (untyped) buffer access on gfx9-class parts:
+// 32-bit data format, no swizzle, no index stride.
+constexpr int kRsrcWord3 = 0x00020000;
+// Cache policy of streaming loads and stores: non-temporal (the data is used
+// once per call).
+constexpr int kStreamAux = 2;
+
+__device__ inline rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kRsrcWord3);
+}
+
+// Chunk n of this thread (byte offset (n*W + tid)*16).  Out-of-range chunks
+// read as zeros.
+template <int W>
+__device__ inline chunk_t load_chunk(rsrc_t r, int n) {
+    const int off = (n * W + static_cast<int>(threadIdx.x)) * 16;
+    return __builtin_bit_cast(chunk_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kStreamAux));
+}
+
+template <int W>
+__device__ inline void store_chunk(rsrc_t r, int n, const chunk_t& c) {
+    const int off = (n * W + static_cast<int>(threadIdx.x)) * 16;
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) int, c),
+                                           r, off, 0, kStreamAux);
+}
+
+// Uniform (scalar-cache) loads of small per-row arguments.  The address must
+// be the same in every lane; the value lands in a scalar register and its
+// wait does not depend on the vector loads in flight.
+template <typename T>
+__device__ inline T scalar_load(const T* p) {
+    return *(const __attribute__((address_space(4))) T*)(p);
+}
+
+// Byte i of a uint8 array, through the aligned dword that holds it.
+__device__ inline uint32_t scalar_load_u8(const uint8_t* base, int64_t i) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(base) + uintptr_t(i);
+    const uint32_t w = scalar_load(reinterpret_cast<const uint32_t*>(a & ~uintptr_t(3)));
+    return (w >> (8 * (a & 3))) & 0xFFu;
+}
+
+// Element j of a logit row as fp32, through the aligned dword that holds it
+// (the row itself is 16-byte aligned on the streaming path).
+template <typename Fmt>
+__device__ inline float scalar_load_logit(const void* row, int j) {
+    if constexpr (Fmt::kBytes == 2) {
+        const uint32_t w = scalar_load(static_cast<const uint32_t*>(row) + (j >> 1));
+        return (j & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+    } else {
+        return scalar_load(static_cast<const float*>(row) + j);
+    }
+}
+
+// The per-thread shift of a row: the whole number ceil(max * c2) over the
+// thread's first chunk, or 0 when that chunk has no finite logit.  Every
+// later exponent is taken relative to it; a row whose later elements exceed
+// it by more than the fp32 exponent range is caught by the caller (the sum
+// overflows) and rescaled exactly.
+template <typename Fmt>
+__device__ inline float first_chunk_shift(const chunk_t& c, float c2) {
+    const float k = ceilf(chunk_max<Fmt>(c) * c2);
+    return (k > -3.0e38f && k < 3.0e38f) ? k : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Wave64 reductions and scans on DPP (data-parallel primitives: operand lane
+// permutations inside the vector ALU).  Lane shuffles compile to LDS permute
+// round trips; these do not.  Steps: row_shr 1, 2, 4, 8 form inclusive
+// prefixes inside each row of 16 lanes, then row_bcast 15 and 31 carry the row
+// totals into the later rows.  Lanes whose source is outside the row (or a
+// disabled row) take the identity.  The order of operations is fixed, so
+// results are reproducible.  The total ends in lane 63; readlane broadcasts it.
+// ---------------------------------------------------------------------------
+enum : int { kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
+             kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143 };
+
+template <int CTRL, int ROWS>
+__device__ inline uint32_t dpp(uint32_t identity, uint32_t v) {
+    return uint32_t(__builtin_amdgcn_update_dpp(int(identity), int(v), CTRL, ROWS, 0xF, false));
+}
+__device__ inline uint32_t readlane_u32(uint32_t v, int lane) {
+    return uint32_t(__builtin_amdgcn_readlane(int(v), lane));
+}
+__device__ inline float readlane_f32(float v, int lane) {
+    return __uint_as_float(readlane_u32(__float_as_uint(v), lane));
+}
+__device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
+    return uint64_t(readlane_u32(uint32_t(v), lane)) | (uint64_t(readlane_u32(uint32_t(v >> 32), lane)) << 32);
+}
+__device__ inline double readlane_f64(double v, int lane) {
+    return __builtin_bit_cast(double, readlane_u64(__builtin_bit_cast(uint64_t, v), lane));
+}
+
+template <int CTRL, int ROWS>
+__device__ inline float dpp_max_step(float v) {
+    const uint32_t ninf = 0xFF800000u;
+    return fmaxf(v, __uint_as_float(dpp<CTRL, ROWS>(ninf, __float_as_uint(v))));
+}
+template <int CTRL, int ROWS>
+__device__ inline double dpp_add_step(double v) {
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const uint64_t o = uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(b))) | (uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(b >> 32))) << 32);
+    return v + __builtin_bit_cast(double, o);
+}
+template <int CTRL, int ROWS>
+__device__ inline uint64_t dpp_add_step(uint64_t v) {
+    const uint64_t o = uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(v))) | (uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(v >> 32))) << 32);
+    return v + o;
+}
+
+// Inclusive scans over the wave (lane 63 holds the total).
+__device__ inline float wave_scan_max(float v) {
+    v = dpp_max_step<kDppRowShr1, 0xF>(v);
+    v = dpp_max_step<kDppRowShr2, 0xF>(v);
+    v = dpp_max_step<kDppRowShr4, 0xF>(v);
+    v = dpp_max_step<kDppRowShr8, 0xF>(v);
+    v = dpp_max_step<kDppRowBcast15, 0xA>(v);
+    v = dpp_max_step<kDppRowBcast31, 0xC>(v);
+    return v;
+}
+template <typename T>
+__device__ inline T wave_scan_add(T v) {
+    v = dpp_add_step<kDppRowShr1, 0xF>(v);
+    v = dpp_add_step<kDppRowShr2, 0xF>(v);
+    v = dpp_add_step<kDppRowShr4, 0xF>(v);
+    v = dpp_add_step<kDppRowShr8, 0xF>(v);
+    v = dpp_add_step<kDppRowBcast15, 0xA>(v);
+    v = dpp_add_step<kDppRowBcast31, 0xC>(v);
+    return v;
+}
+
+// Wave totals, uniform.
+__device__ inline float wave_max_u(float v) { return readlane_f32(wave_scan_max(v), kWave - 1); }
+__device__ inline double wave_sum_u(double v) { return readlane_f64(wave_scan_add(v), kWave - 1); }
+
+// Merge (K, S) pairs over the wave: K = max K, S = sum S 2^(K_lane - K).
+// Every lane gets the wave's pair.
+__device__ inline void wave_merge_stats_u(float& K, double& S) {
+    const float kw = wave_max_u(K);
+    S = wave_sum_u(rescale(S, K, kw));
+    K = kw;
+}
+
+// Workgroup merge of the (K, S) pairs of two rows.  Each wave merges its
+// lanes; lane 0 of every wave posts the wave's pairs to LDS; after one
+// barrier every wave merges the NW posted pairs the same way (so all agree,
+// bit for bit).  s_k: [2*NW] floats, s_s: [2*NW] doubles, not written again
+// before the caller's next barrier.
+template <int NW>
+__device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1, float* s_k, double* s_s) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    wave_merge_stats_u(K0, S0);
+    wave_merge_stats_u(K1, S1);
+    if (lane == 0) {
+        s_k[wid] = K0;
+        s_k[NW + wid] = K1;
+        s_s[wid] = S0;
+        s_s[NW + wid] = S1;
+    }
+    __syncthreads();
+    float k0 = kNegInf, k1 = kNegInf;
+    double t0 = 0.0, t1 = 0.0;
+    if (lane < NW) {
+        k0 = s_k[lane];
+        k1 = s_k[NW + lane];
+        t0 = s_s[lane];
+        t1 = s_s[NW + lane];
+    }
+    wave_merge_stats_u(k0, t0);
+    wave_merge_stats_u(k1, t1);
+    K0 = k0;
+    S0 = t0;
+    K1 = k1;
+    S1 = t1;
+}
+
+// Workgroup sums of two doubles, the same way (one barrier).
+template <int NW>
+__device__ inline void block_sum2(double& A0, double& A1, double* s_a) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    A0 = wave_sum_u(A0);
+    A1 = wave_sum_u(A1);
+    if (lane == 0) {
+        s_a[wid] = A0;
+        s_a[NW + wid] = A1;
+    }
+    __syncthreads();
+    double t0 = lane < NW ? s_a[lane] : 0.0;
+    double t1 = lane < NW ? s_a[NW + lane] : 0.0;
+    A0 = wave_sum_u(t0);
+    A1 = wave_sum_u(t1);
+}
+
+// Argmax step: the larger value, the lower index among equal values.
+template <int CTRL, int ROWS>
+__device__ inline void dpp_argmax_step(float& v, int& idx) {
+    const float ov = __uint_as_float(dpp<CTRL, ROWS>(0xFF800000u, __float_as_uint(v)));
+    const int oi = int(dpp<CTRL, ROWS>(0x7FFFFFFFu, uint32_t(idx)));
+    if (ov > v || (ov == v && oi < idx)) {
+        v = ov;
+        idx = oi;
+    }
+}
+// Max value, lowest index among equal maxima; uniform result.
+__device__ inline void wave_argmax_u(float& v, int& idx) {
+    dpp_argmax_step<kDppRowShr1, 0xF>(v, idx);
+    dpp_argmax_step<kDppRowShr2, 0xF>(v, idx);
+    dpp_argmax_step<kDppRowShr4, 0xF>(v, idx);
+    dpp_argmax_step<kDppRowShr8, 0xF>(v, idx);
+    dpp_argmax_step<kDppRowBcast15, 0xA>(v, idx);
+    dpp_argmax_step<kDppRowBcast31, 0xC>(v, idx);
+    v = readlane_f32(v, kWave - 1);
+    idx = int(readlane_u32(uint32_t(idx), kWave - 1));
+}
+
+// Exact fp32 -> fixed point with SH fractional bits (x >= 0, x < 2^(63-SH)).
+template <int SH>
+__device__ inline uint64_t to_fixed(float x) { return mass_to_fixed<SH>(x); }
+
+
+}  // namespace osd

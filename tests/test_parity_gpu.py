@@ -103,10 +103,19 @@ def test_verify_ragged_tail_vocab(osd, V, dtype):
     check_verify(osd, x, f"V={V} {dtype}")
 
 
-@pytest.mark.parametrize("V", [2048, 2049 * 8, 32000, 65536])
+@pytest.mark.parametrize("V", [2048, 2049 * 8, 8192, 8200, 32000, 32768, 32776, 65536, 131072])
 def test_verify_tile_boundaries(osd, V):
+    """bf16 rows around the statistics segments (8192 logits each) and the
+    draw workgroup's 8192-logit rounds, up to the largest vocabulary."""
     x = synth.verify_inputs(4, 5, V, "bf16", T=1.0, seed=7, target_std=2.5, draft_noise=0.5)
     check_verify(osd, x, f"tile V={V}")
+
+
+@pytest.mark.parametrize("V", [4096, 4100, 16388, 65536])
+def test_verify_tile_boundaries_f32(osd, V):
+    """fp32 rows around the 4096-logit segments, up to the largest vocabulary."""
+    x = synth.verify_inputs(3, 4, V, "f32", T=0.8, seed=11, target_std=2.5, draft_noise=0.7)
+    check_verify(osd, x, f"tile f32 V={V}")
 
 
 def test_verify_ragged_lengths_and_invalid_rows(osd):
