@@ -24,9 +24,10 @@
 // FKL and RKL is formed from the exact difference t - s, so it carries no
 // rounding of the (much larger) normalisers.
 //
-// Each row leaves its D in fp64 in the workspace; a one-workgroup second
-// kernel (distill_reduce) sums them in a fixed order, so the loss is bitwise
-// reproducible.
+// Each workgroup adds the D of its rows in fp64 in row order and posts the
+// partial at the device-wide coherence point; the last workgroup to finish
+// adds the partials in workgroup order, so the loss is reproducible for a
+// given grid.
 #include "osd_device.hpp"
 #include "osd_internal.hpp"
 #include "stream_device.hpp"
@@ -46,7 +47,9 @@ struct StreamDistillArgs {
     float inv_tau;  // 1 / tau
     float* row_loss_out;
     void* grad_out;
-    double* row_ws;  // [B*K]
+    double* row_ws;     // [grid] per-workgroup loss partials, zero between calls
+    uint32_t* done;     // workgroups finished, zero between calls
+    float* loss_out;    // {masked mean, masked sum}
     int nrows;
     int nchunks;
     uint32_t row_bytes;
@@ -130,6 +133,61 @@ struct LdsCache {
     __device__ void store(int r, int g, const f32x4_t& v) const { base[(r * (EPC / 4) + g) * W + threadIdx.x] = v; }
 };
 
+// Masked sum and mean of the row divergences.  Each workgroup adds its rows
+// in row order (D = 0 for masked-out rows) and posts the partial at the
+// device-wide coherence point; the last workgroup to finish adds the
+// partials in workgroup order, counts the mask, writes the loss and zeroes
+// what it read.  The result depends only on the grid size.
+// What the tail needs, staged in LDS at kernel start so that none of it stays
+// in registers across the row loop.
+struct LossTail {
+    double* row_ws;
+    uint32_t* done;
+    float* loss_out;
+    const uint8_t* mask;
+    int nrows;
+};
+
+template <int W>
+__device__ inline void finish_loss(const LossTail& a, const double* s_part) {
+    __shared__ int s_last;
+    __shared__ double s_sum[W / kWave], s_cnt[W / kWave];
+    // Thread indices recomputed from an opaque copy: values derived from them
+    // before the row loop are then not kept alive across it.
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & (kWave - 1), wid = tid / kWave;
+    const int G = gridDim.x;
+    __syncthreads();
+    if (tid == 0) {
+        __hip_atomic_exchange(&a.row_ws[blockIdx.x], s_part[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = int(arrive(a.done)) == G - 1;  // after the post completed
+    }
+    __syncthreads();
+    if (!s_last) return;
+    // Thread t adds partials t, t+W, ... (one each when G <= W).
+    double sm = 0.0, cn = 0.0;
+    for (int g = tid; g < G; g += W) sm += take_f64(&a.row_ws[g]);
+    for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
+    sm = wave_sum(sm);
+    cn = wave_sum(cn);
+    if (lane == 0) {
+        s_sum[wid] = sm;
+        s_cnt[wid] = cn;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double ts = 0.0, tc = 0.0;
+        for (int w = 0; w < W / kWave; ++w) {
+            ts += s_sum[w];
+            tc += s_cnt[w];
+        }
+        a.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
+        a.loss_out[1] = float(ts);
+        take_u32(a.done);
+    }
+}
+
 template <typename Fmt, int W, int CPT, int KIND>
 __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs a) {
     constexpr int NW = W / kWave, EPC = Fmt::kPerChunk, NG = EPC / 4;
@@ -137,6 +195,8 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
     __shared__ double s_s[2 * NW];
     __shared__ double s_a[2 * NW];
     __shared__ uint8_t s_on[W];
+    __shared__ double s_part[1];  // sum of this workgroup's row divergences
+    __shared__ LossTail s_tail;
     __shared__ f32x4_t s_c0[CPT * NG * W];
     const LdsCache<W, EPC> lc{s_c0};
 
@@ -155,6 +215,14 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
     // reads global memory except the rows themselves (a scalar load there
     // would share its wait counter with LDS traffic).
     const int nk = (a.nrows - int(blockIdx.x) + G - 1) / G;
+    if (tid == 0) {
+        s_part[0] = 0.0;  // read and written by thread 0 only
+        s_tail.row_ws = a.row_ws;
+        s_tail.done = a.done;
+        s_tail.loss_out = a.loss_out;
+        s_tail.mask = a.mask;
+        s_tail.nrows = a.nrows;
+    }
     uint32_t mine = 1u;
     if (a.mask && tid < nk) mine = a.mask[int(blockIdx.x) + tid * G];
     // The pipeline starts one step early: step -1 computes nothing; it issues
@@ -351,47 +419,11 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
         }
         if (tid == 0 && n >= 0) {
             if (a.row_loss_out) a.row_loss_out[n] = float(D);
-            a.row_ws[n] = D;
+            s_part[0] += D;  // this workgroup's rows, in row order
         }
         cur = nxt;
     }
-}
-
-// Masked sum and mean of the per-row divergences, in a fixed order: thread t
-// sums rows t, t+1024, ... in fp64, then a fixed butterfly per wave and the
-// waves in index order.
-struct ReduceArgs {
-    double* row_ws;
-    const uint8_t* mask;
-    int nrows;
-    float* loss_out;
-};
-
-__global__ __launch_bounds__(1024) void distill_reduce_kernel(ReduceArgs r) {
-    __shared__ double s_sum[16], s_cnt[16];
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-    double s = 0.0, c = 0.0;
-    for (int n = tid; n < r.nrows; n += 1024) {
-        s += r.row_ws[n];
-        r.row_ws[n] = 0.0;  // the workspace is zero between calls
-        c += (r.mask == nullptr || r.mask[n] != 0) ? 1.0 : 0.0;
-    }
-    s = wave_sum(s);
-    c = wave_sum(c);
-    if (lane == 0) {
-        s_sum[wid] = s;
-        s_cnt[wid] = c;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        double ts = 0.0, tc = 0.0;
-        for (int w = 0; w < 16; ++w) {
-            ts += s_sum[w];
-            tc += s_cnt[w];
-        }
-        r.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
-        r.loss_out[1] = float(ts);
-    }
+    finish_loss<W>(s_tail, s_part);
 }
 
 template <typename Fmt, int W, int CPT, int KIND>
@@ -471,19 +503,13 @@ hipError_t launch_distill_stream(const DistillLaunch& L) {
     a.row_loss_out = L.row_loss_out;
     a.grad_out = L.grad_out;
     a.row_ws = L.row_loss_ws;
+    a.done = L.done_counter;
+    a.loss_out = L.loss_out;
     a.nrows = L.B * L.K;
     const int eb = L.dtype == 1 ? 2 : 4;
     a.nchunks = int((int64_t(L.V) * eb) / 16);
     a.row_bytes = uint32_t(int64_t(L.V) * eb);
-    hipError_t err = L.dtype == 1 ? launch_fmt<BF16>(L, a) : launch_fmt<F32>(L, a);
-    if (err != hipSuccess) return err;
-    ReduceArgs r;
-    r.row_ws = L.row_loss_ws;
-    r.mask = L.mask;
-    r.nrows = a.nrows;
-    r.loss_out = L.loss_out;
-    hipLaunchKernelGGL(distill_reduce_kernel, dim3(1), dim3(1024), 0, L.stream, r);
-    return hipGetLastError();
+    return L.dtype == 1 ? launch_fmt<BF16>(L, a) : launch_fmt<F32>(L, a);
 }
 
 }  // namespace osd

@@ -17,11 +17,10 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int per_chunk(int dtype) { return dtype == OSD_BF16 ? 8 : (dtype == OSD_F32 ? 4 : 0); }
 int elem_bytes(int dtype) { return dtype == OSD_BF16 ? 2 : 4; }
 
-// Counters and records of the row-resident kernel, then the segment
-// statistics and proposal logits of the segmented kernels.  Every call leaves
-// all of it zero.
+// Counters and records of the row-resident kernel, then the argmax partials
+// of the segmented greedy kernels.  Every call leaves all of it zero.
 struct VerifyWs {
-    size_t records, counters, stats, yv, total;
+    size_t records, counters, stats, total;
 };
 VerifyWs verify_layout(int B, int K) {
     VerifyWs w;
@@ -29,8 +28,7 @@ VerifyWs verify_layout(int B, int K) {
     w.counters = 0;
     w.records = round_up(size_t(B) * 4, kAlign);
     w.stats = w.records + round_up(rows * 4, kAlign);
-    w.yv = w.stats + round_up(rows * osd::kMaxSeg * sizeof(osd::SegStats), kAlign);
-    w.total = w.yv + round_up(rows * 8, kAlign);
+    w.total = w.stats + round_up(rows * osd::kMaxSeg * sizeof(osd::SegStats), kAlign);
     return w;
 }
 
@@ -137,13 +135,14 @@ int osd_verify(const void* target_logits, const void* draft_logits, int dtype, i
     L.records = reinterpret_cast<uint32_t*>(w + ws.records);
     L.counters = reinterpret_cast<uint32_t*>(w + ws.counters);
     L.seg_stats = reinterpret_cast<osd::SegStats*>(w + ws.stats);
-    L.seg_y = reinterpret_cast<float*>(w + ws.yv);
     L.vec = (int64_t(V) * elem_bytes(dtype)) % 16 == 0 && aligned16(target_logits) &&
             (greedy || aligned16(draft_logits));
     L.stream = static_cast<hipStream_t>(stream);
-    int cpt = 0, nseg = 0;
-    const bool segmented = L.vec && osd::pick_seg_cpt(V, per_chunk(dtype), &cpt, &nseg);
-    const hipError_t e = segmented ? osd::launch_verify_seg(L) : osd::launch_verify(L);
+    // Greedy: segmented kernels (balanced over every CU).  Sampling: the
+    // row-resident kernel, which draws from rows it already holds.
+    int nseg = 0;
+    const bool segmented = greedy && L.vec && osd::greedy_segments(V, per_chunk(dtype), &nseg);
+    const hipError_t e = segmented ? osd::launch_verify_greedy(L) : osd::launch_verify(L);
     return e == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 

@@ -21,14 +21,13 @@ struct RowTile {
 // 64 VGPRs, and the spills that forces cost more than the occupancy gains.)
 constexpr int min_waves_per_simd(int W, int CPT) { return (void)W, (void)CPT, 4; }
 
-// Softmax statistics of one vocabulary segment of a row pair (segmented
-// verification): S = sum 2^(x log2(e)/T - K) over the segment, K a whole
-// number.  Greedy verification keeps (max, index) in (kt, kd).
+// Argmax partial of one vocabulary segment of a target row (segmented greedy
+// verification): (max, lowest index) in (kt, kd's bits).
 struct SegStats {
     double st, sd;
     float kt, kd;
 };
-// Segments per row in the segmented verification kernels (at most).
+// Segments per row in the segmented greedy kernels (at most).
 constexpr int kMaxSeg = 16;
 
 struct VerifyLaunch {
@@ -46,8 +45,7 @@ struct VerifyLaunch {
     uint8_t* reject_mask;
     uint32_t* records;   // [B*(K+1)] zero on entry and exit
     uint32_t* counters;  // [B]       zero on entry and exit
-    SegStats* seg_stats;           // [B*(K+1)*kMaxSeg] (segmented kernels)
-    float* seg_y;                  // [B*(K+1)*2]
+    SegStats* seg_stats;  // [B*(K+1)*kMaxSeg] greedy argmax partials, zero on entry and exit
     bool vec;            // rows 16-byte aligned
     hipStream_t stream;
 };
@@ -86,10 +84,10 @@ bool pick_tile(int V, int per_chunk, RowTile* t);
 hipError_t launch_verify(const VerifyLaunch& L);
 hipError_t launch_distill(const DistillLaunch& L);
 
-// Segmented verification: rows whose byte length and base are 16-byte
-// multiples.  Chunks per thread and segments per row for V.
-bool pick_seg_cpt(int V, int per_chunk, int* cpt, int* nseg);
-hipError_t launch_verify_seg(const VerifyLaunch& L);
+// Segmented greedy verification: rows whose byte length and base are
+// 16-byte multiples.  Segments per row for V (false: V too large).
+bool greedy_segments(int V, int per_chunk, int* nseg);
+hipError_t launch_verify_greedy(const VerifyLaunch& L);
 
 // Streaming (persistent-workgroup) distillation: rows whose byte length and
 // base are 16-byte multiples and whose V fits one of the streaming tiles.
