@@ -8,8 +8,11 @@ bf16 logits, target ~ N(0, 2.5^2), draft = 0.7 target + N(0, 1.5^2).
 
 Inputs are synthetic and seeded; R copies of the batch rotate through the
 timed loop so that consecutive launches never find their inputs in the 256 MB
-Infinity Cache.  Each kernel is also timed alone (HIP events on the stream the
-kernels are launched on) to report its achieved HBM bandwidth against the
+Infinity Cache.  The timed steps are captured once into a HIP graph and
+replayed, so that host launch overhead does not pace the GPU (the library
+allocates nothing and clears its own workspace, so its calls capture as they
+are).  Each entry point is also timed alone the same way (HIP events on the
+stream the kernels run on) to report its achieved HBM bandwidth against the
 8 TB/s peak.  The CPU baseline is the fp64 oracle on the host.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -148,13 +151,17 @@ def main():
         s["rows"] = torch.empty(B, K, dtype=torch.float32, device=dev)
         s["grad"] = torch.empty(B, K, V, dtype=torch.bfloat16, device=dev)
         sets.append(s)
-    stream = torch.cuda.current_stream(dev)
+    # Everything runs on one side stream: the graphs are captured and
+    # replayed on it, and the library's calls take its handle.
+    stream = torch.cuda.Stream(dev)
+    stream.wait_stream(torch.cuda.current_stream(dev))
     hs = ctypes.c_void_p(stream.cuda_stream)
     vws = torch.zeros(L.osd_verify_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
     dws = torch.zeros(L.osd_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
     P = lambda t: ctypes.c_void_p(t.data_ptr())
 
-    # Pre-marshalled argument tuples: the timed loops are pure C calls.
+    # Pre-marshalled argument tuples: the captured loops are pure C calls.
     verify_args = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, B, K, V, P(s["tokens"]), None,
                     P(s["ua"]), P(s["ur"]), ctypes.c_float(T_VERIFY), P(s["acc"]), P(s["toks"]),
                     P(s["rmask"]), P(vws), vws.numel(), hs) for s in sets]
@@ -179,15 +186,32 @@ def main():
         call(fv, verify_args[r % R])
         call(fd, jsd_args[r % R])
 
+    def capture(fn, iters):
+        """A HIP graph of fn(0..iters-1) on the side stream."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for r in range(iters):
+                fn(r)
+        return g
+
+    def time_graph(g, iters):
+        """Replay g once untimed, then once between events; ms per iteration."""
+        with torch.cuda.stream(stream):
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
     def time_loop(fn, iters):
+        with torch.cuda.stream(stream):
+            for r in range(10):
+                fn(r)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for r in range(iters):
-            fn(r)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters  # ms
+        return time_graph(capture(fn, iters), iters)
 
     if args.only:
         # Profiling aid: run only the named loops (comma-separated), each
@@ -208,18 +232,21 @@ def main():
                                   "bytes_written": dst.numel(), "launches": 10}), flush=True)
                 continue
             fn = loops[name]
-            for r in range(args.warmup):
-                fn(r)
+            with torch.cuda.stream(stream):
+                for r in range(args.warmup):
+                    fn(r)
             ms = time_loop(fn, args.kernel_iters)
             print(json.dumps({"only": name, "us_per_launch": ms * 1e3,
                               "launches": args.warmup + args.kernel_iters}), flush=True)
         return
 
-    for r in range(args.warmup):
-        step(r)
+    with torch.cuda.stream(stream):
+        for r in range(args.warmup):
+            step(r)
     torch.cuda.synchronize()
     print(f"# warmup done: {args.warmup} steps, R={R} rotating input sets", file=sys.stderr, flush=True)
-    ms_step = time_loop(step, args.steps)
+    # Exactly K steps, captured once and replayed between events.
+    ms_step = time_graph(capture(step, args.steps), args.steps)
     print(f"# timed {args.steps} steps: {ms_step * 1e3:.2f} us/step", file=sys.stderr, flush=True)
 
     kernels = {}
@@ -229,9 +256,7 @@ def main():
             ("verify_greedy", fv, greedy_args, verify_bytes(B, K, V, greedy=True)),
             ("distill_jsd", fd, jsd_args, distill_bytes(B, K, V, masked)),
             ("distill_rkl", fd, rkl_args, distill_bytes(B, K, V, masked))):
-        for r in range(10):
-            call(f, argl[r % R])
-        ms = time_loop(lambda r: call(f, argl[r % R]), args.kernel_iters)
+        ms = time_loop(lambda r, f=f, argl=argl: call(f, argl[r % R]), args.kernel_iters)
         gbs = nbytes / (ms * 1e-3) / 1e9
         kernels[name] = {"us_per_launch": round(ms * 1e3, 3), "algorithmic_bytes": nbytes,
                          "achieved_GBps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
