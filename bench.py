@@ -44,7 +44,8 @@ def parse():
     p.add_argument("--kernel-iters", type=int, default=400)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--only", default=None,
-                   help="profiling aid: run only the named loops, comma-separated (verify,greedy,jsd,rkl,copy)")
+                   help="profiling aid: run only the named loops, comma-separated "
+                        "(verify,greedy,jsd,rkl,fused,copy)")
     return p.parse_args()
 
 
@@ -62,6 +63,14 @@ def distill_bytes(B, K, V, masked_rows, elem=2):
     rows read once where the mask is 1, the whole gradient written once, the
     mask read, the per-row and total losses written."""
     return masked_rows * 2 * V * elem + B * K * V * elem + B * K + 4 * B * K + 8
+
+
+def fused_bytes(B, K, V, masked_rows, elem=2):
+    """Algorithmic bytes of one osd_verify_distill call: the verification's
+    row reads (each row pair once; the distillation reuses them), its small
+    inputs and outputs, the whole gradient written once, the mask read, the
+    per-row and total losses written."""
+    return verify_bytes(B, K, V, elem) + B * K * V * elem + B * K + 4 * B * K + 8
 
 
 def kernel_source_hash():
@@ -175,7 +184,13 @@ def main():
                  P(s["rows"]), P(s["grad"]), P(dws), dws.numel(), hs) for s in sets]
 
     jsd_args, rkl_args = distill_args(binding.OSD_JSD), distill_args(binding.OSD_RKL)
-    fv, fd = L.osd_verify, L.osd_distill_loss_grad
+    fws = torch.zeros(L.osd_verify_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    fused_args = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, B, K, V, P(s["tokens"]), None,
+                   P(s["ua"]), P(s["ur"]), ctypes.c_float(T_VERIFY), P(s["acc"]), P(s["toks"]),
+                   P(s["rmask"]), P(s["mask"]), binding.OSD_JSD, ctypes.c_float(BETA), P(s["loss"]),
+                   P(s["rows"]), P(s["grad"]), P(fws), fws.numel(), hs) for s in sets]
+    fv, fd, ff = L.osd_verify, L.osd_distill_loss_grad, L.osd_verify_distill
 
     def call(f, a):
         st = f(*a)
@@ -218,6 +233,7 @@ def main():
         # warmed up and timed on its own; "copy" is a plain 256 MiB device
         # copy used to calibrate the HBM byte counters.
         loops = {"verify": lambda r: call(fv, verify_args[r % R]),
+                 "fused": lambda r: call(ff, fused_args[r % R]),
                  "greedy": lambda r: call(fv, greedy_args[r % R]),
                  "jsd": lambda r: call(fd, jsd_args[r % R]),
                  "rkl": lambda r: call(fd, rkl_args[r % R])}

@@ -142,6 +142,45 @@ int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stri
                           float* loss_out, float* row_loss_out, void* grad_out,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* Workspace needed by osd_verify_distill for B sequences of up to K proposals. */
+size_t osd_verify_distill_workspace_bytes(int B, int K);
+
+/*
+ * osd_verify_distill -- one speculative step's verification and
+ * distillation in a single pass over the row pairs (Algorithm 1 verifies the
+ * proposals and records, at the error index, what distillation later trains
+ * on; Section 4.1 and Eq. 2-4 give the divergence).  The results are those
+ * of
+ *   osd_verify(target, draft, ..., temperature, ...) and
+ *   osd_distill_loss_grad(target, (K+1)*V, draft, K*V, dtype, B, K, V,
+ *                         distill_mask, kind, beta, temperature, ...):
+ * teacher = target rows 0..K-1, student = draft rows, tau = temperature.
+ * Both read the same row pairs; done together they are read once and their
+ * softmax normalisers are computed once.
+ *
+ * Arguments as in osd_verify and osd_distill_loss_grad, with:
+ * temperature   T > 0: verification temperature and distillation tau
+ * distill_mask  [B, K] uint8 0/1, or NULL for all rows: which rows are
+ *               distilled (independent of the verification outcome)
+ * workspace     osd_verify_distill_workspace_bytes(B, K) zero-initialised
+ *               bytes
+ *
+ * Verification decisions have the same guarantee as osd_verify's (their
+ * masses are formed from the distillation's cached exponents, so a draw that
+ * sits within ~1e-7 of a CDF edge may differ from osd_verify's); losses and
+ * gradients match osd_distill_loss_grad's within fp32 rounding (the fp64 loss
+ * sum is taken in a different fixed order).
+ */
+int osd_verify_distill(const void* target_logits, const void* draft_logits, int dtype,
+                       int B, int K, int V,
+                       const int32_t* draft_tokens, const int32_t* draft_len,
+                       const float* u_accept, const float* u_resample,
+                       float temperature,
+                       int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+                       const uint8_t* distill_mask, int kind, float beta,
+                       float* loss_out, float* row_loss_out, void* grad_out,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

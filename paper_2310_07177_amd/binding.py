@@ -21,7 +21,8 @@ OSD_MAX_K = 16
 KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
 EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify",
-           "osd_distill_workspace_bytes", "osd_distill_loss_grad")
+           "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
+           "osd_verify_distill")
 
 _lib = None
 _lock = threading.Lock()
@@ -58,6 +59,11 @@ def lib():
             L.osd_distill_loss_grad.restype = i32
             L.osd_distill_loss_grad.argtypes = [vp, i64, vp, i64, i32, i32, i32, i32, vp, i32,
                                                 f32, f32, vp, vp, vp, vp, sz, vp]
+            L.osd_verify_distill_workspace_bytes.restype = sz
+            L.osd_verify_distill_workspace_bytes.argtypes = [i32, i32]
+            L.osd_verify_distill.restype = i32
+            L.osd_verify_distill.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp,
+                                             vp, i32, f32, vp, vp, vp, vp, sz, vp]
             _lib = L
     return _lib
 
@@ -187,3 +193,44 @@ def osd_distill_loss_grad(teacher_logits, student_logits, kind, beta=0.5, tau=1.
     if st != OSD_OK:
         raise OsdError("osd_distill_loss_grad", st)
     return loss, rows, g
+
+
+def osd_verify_distill(target_logits, draft_logits, draft_tokens, u_accept, u_resample, temperature,
+                       kind, beta=0.5, distill_mask=None, draft_len=None, grad=True, row_loss=True):
+    """Verification and distillation of one step in one pass through the C
+    ABI: the results of osd_verify(...) and of osd_distill_loss_grad on the
+    first K target rows and the draft rows at tau = temperature.
+
+    Returns (accepted_len [B], out_tokens [B, K+1], reject_mask [B, K],
+    loss [2], row_loss [B, K] or None, grad [B, K, V] or None)."""
+    torch = _torch()
+    B, K1, V = target_logits.shape
+    K = K1 - 1
+    _check_cuda(target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len, distill_mask)
+    dev = target_logits.device
+    for t in (target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len, distill_mask):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if draft_tokens.dtype != torch.int32 or (draft_len is not None and draft_len.dtype != torch.int32):
+        raise TypeError("draft_tokens and draft_len must be int32")
+    if target_logits.dtype != draft_logits.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    if distill_mask is not None and distill_mask.dtype != torch.uint8:
+        raise TypeError("distill_mask must be uint8")
+    kind_code = KINDS[kind] if isinstance(kind, str) else int(kind)
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    toks = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+    rmask = torch.empty(B, K, dtype=torch.uint8, device=dev)
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    rows = torch.empty(B, K, dtype=torch.float32, device=dev) if row_loss else None
+    g = torch.empty(B, K, V, dtype=draft_logits.dtype, device=dev) if grad else None
+    L = lib()
+    ws = workspace("verify_distill", L.osd_verify_distill_workspace_bytes(B, K), dev)
+    st = L.osd_verify_distill(_ptr(target_logits), _ptr(draft_logits), _dtype_code(target_logits), B, K, V,
+                              _ptr(draft_tokens), _ptr(draft_len), _ptr(u_accept), _ptr(u_resample),
+                              float(temperature), _ptr(acc), _ptr(toks), _ptr(rmask), _ptr(distill_mask),
+                              kind_code, float(beta), _ptr(loss), _ptr(rows), _ptr(g), _ptr(ws), ws.numel(),
+                              _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_verify_distill", st)
+    return acc, toks, rmask, loss, rows, g

@@ -50,6 +50,21 @@ DistillWs distill_layout(int B, int K) {
     return w;
 }
 
+// The fused entry point: the verify workspace, then the distill workspace
+// (both used as they are by the two-call path), then per-workgroup loss
+// partials of the fused kernel (at most one per item).
+struct FusedWs {
+    size_t verify, distill, part, total;
+};
+FusedWs fused_layout(int B, int K) {
+    FusedWs w;
+    w.verify = 0;
+    w.distill = round_up(verify_layout(B, K).total, kAlign);
+    w.part = w.distill + round_up(distill_layout(B, K).total, kAlign);
+    w.total = w.part + round_up(size_t(B) * size_t(K + 1) * 8, kAlign);
+    return w;
+}
+
 // Compute units of the device that runs `stream` (queried once per device).
 int device_cus(hipStream_t stream) {
     static int cache[64] = {0};
@@ -203,6 +218,76 @@ int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stri
     const bool streaming = L.vec && osd::pick_stream_tile(V, per_chunk(dtype), &t);
     const hipError_t e = streaming ? osd::launch_distill_stream(L) : osd::launch_distill(L);
     return e == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+size_t osd_verify_distill_workspace_bytes(int B, int K) {
+    if (B <= 0 || K <= 0 || K > OSD_MAX_K) return 0;
+    if (int64_t(B) * int64_t(K + 1) > 0x7FFFFFFFll) return 0;
+    return fused_layout(B, K).total;
+}
+
+int osd_verify_distill(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
+                       int V, const int32_t* draft_tokens, const int32_t* draft_len,
+                       const float* u_accept, const float* u_resample, float temperature,
+                       int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+                       const uint8_t* distill_mask, int kind, float beta, float* loss_out,
+                       float* row_loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || K <= 0 || V <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
+    if (!sizes_ok(B, K, V, dtype)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature > 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    if (kind != OSD_FKL && kind != OSD_RKL && kind != OSD_JSD) return OSD_ERR_INVALID_ARG;
+    if (!(beta >= 0.0f && beta <= 1.0f)) return OSD_ERR_INVALID_ARG;
+    if (!target_logits || !draft_logits || !draft_tokens || !u_accept || !u_resample || !accepted_len ||
+        !out_tokens || !loss_out)
+        return OSD_ERR_INVALID_ARG;
+    const FusedWs ws = fused_layout(B, K);
+    if (!workspace || workspace_bytes < ws.total || (reinterpret_cast<uintptr_t>(workspace) & 15u))
+        return OSD_ERR_WORKSPACE;
+    char* w = static_cast<char*>(workspace);
+    const int eb = elem_bytes(dtype);
+    osd::RowTile t;
+    const bool fused = (int64_t(V) * eb) % 16 == 0 && aligned16(target_logits) && aligned16(draft_logits) &&
+                       (grad_out == nullptr || aligned16(grad_out)) && osd::pick_stream_tile(V, per_chunk(dtype), &t);
+    if (!fused) {  // the two calls, each on its own part of the workspace
+        const VerifyWs vw = verify_layout(B, K);
+        const DistillWs dw = distill_layout(B, K);
+        int st = osd_verify(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept,
+                            u_resample, temperature, accepted_len, out_tokens, reject_mask, w + ws.verify,
+                            vw.total, stream);
+        if (st != OSD_OK) return st;
+        return osd_distill_loss_grad(target_logits, int64_t(K + 1) * V, draft_logits, int64_t(K) * V, dtype, B,
+                                     K, V, distill_mask, kind, beta, temperature, loss_out, row_loss_out,
+                                     grad_out, w + ws.distill, dw.total, stream);
+    }
+    osd::FusedLaunch L;
+    L.target = target_logits;
+    L.draft = draft_logits;
+    L.dtype = dtype;
+    L.B = B;
+    L.K = K;
+    L.V = V;
+    L.tokens = draft_tokens;
+    L.draft_len = draft_len;
+    L.u_accept = u_accept;
+    L.u_resample = u_resample;
+    L.temperature = temperature;
+    L.mask = distill_mask;
+    L.kind = kind;
+    L.beta = beta;
+    L.accepted_len = accepted_len;
+    L.out_tokens = out_tokens;
+    L.reject_mask = reject_mask;
+    L.loss_out = loss_out;
+    L.row_loss_out = row_loss_out;
+    L.grad_out = grad_out;
+    L.records = reinterpret_cast<uint32_t*>(w + ws.verify + verify_layout(B, K).records);
+    L.done = reinterpret_cast<uint32_t*>(w + ws.distill + distill_layout(B, K).done);
+    L.part_ws = reinterpret_cast<double*>(w + ws.part);
+    L.stream = static_cast<hipStream_t>(stream);
+    L.cus = device_cus(L.stream);
+    return osd::launch_verify_distill(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 
 }  // extern "C"

@@ -89,6 +89,36 @@ hipError_t launch_distill(const DistillLaunch& L);
 bool greedy_segments(int V, int per_chunk, int* nseg);
 hipError_t launch_verify_greedy(const VerifyLaunch& L);
 
+// Fused verification + distillation of one step (streaming layout), the
+// distillation at the verification temperature: teacher = target rows
+// 0..K-1, student = draft rows.
+struct FusedLaunch {
+    const void* target;
+    const void* draft;
+    int dtype;
+    int B, K, V;
+    const int32_t* tokens;
+    const int32_t* draft_len;
+    const float* u_accept;
+    const float* u_resample;
+    float temperature;
+    const uint8_t* mask;  // distillation mask [B, K] or null
+    int kind;
+    float beta;
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    float* loss_out;
+    float* row_loss_out;
+    void* grad_out;
+    uint32_t* records;  // [B*(K+1)]     zero on entry and exit
+    double* part_ws;    // [B*(K+1)]     zero on entry and exit
+    uint32_t* done;     // [1]           zero on entry and exit
+    int cus;
+    hipStream_t stream;
+};
+hipError_t launch_verify_distill(const FusedLaunch& L);
+
 // Streaming (persistent-workgroup) distillation: rows whose byte length and
 // base are 16-byte multiples and whose V fits one of the streaming tiles.
 bool pick_stream_tile(int V, int per_chunk, RowTile* t);

@@ -96,6 +96,15 @@ __device__ inline float first_chunk_shift(const chunk_t& c, float c2) {
 enum : int { kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
              kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143 };
 
+// The thread index through an opaque copy: lane and wave numbers derived from
+// it are recomputed where they are used instead of being kept alive (or
+// spilled) across a long loop.
+__device__ inline int opaque_tid() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
 template <int CTRL, int ROWS>
 __device__ inline uint32_t dpp(uint32_t identity, uint32_t v) {
     return uint32_t(__builtin_amdgcn_update_dpp(int(identity), int(v), CTRL, ROWS, 0xF, false));
@@ -170,7 +179,7 @@ __device__ inline void wave_merge_stats_u(float& K, double& S) {
 // before the caller's next barrier.
 template <int NW>
 __device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1, float* s_k, double* s_s) {
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    const int t = opaque_tid(), lane = t & (kWave - 1), wid = t / kWave;
     wave_merge_stats_u(K0, S0);
     wave_merge_stats_u(K1, S1);
     if (lane == 0) {
@@ -199,7 +208,7 @@ __device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1
 // Workgroup sums of two doubles, the same way (one barrier).
 template <int NW>
 __device__ inline void block_sum2(double& A0, double& A1, double* s_a) {
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    const int t = opaque_tid(), lane = t & (kWave - 1), wid = t / kWave;
     A0 = wave_sum_u(A0);
     A1 = wave_sum_u(A1);
     if (lane == 0) {

@@ -1,0 +1,844 @@
+// verify_distill.hip -- verification and distillation of one speculative
+// step in a single pass over the row pairs (gfx950).
+//
+// Method.  Verification: Appendix A.1 and Eq. 5 of arXiv:2310.07177 (the
+// verification step of Algorithm 1) -- proposals y_1..y_k are tested in
+// order, y_i is accepted when u_i < p(y_i)/q(y_i), the first rejection at
+// position a ends the test, and one more token is drawn from
+// norm(max(0, p - q)) at row a, or from p at the bonus row k_b when all were
+// accepted.  Distillation: Section 4.1, Eq. 2-4 -- the divergence D (FKL,
+// RKL or JSD with weight beta) between the target distribution p and the
+// draft distribution q of each masked row, and its gradient with respect to
+// the draft logits.  Both use the same temperature T, so the softmax
+// normalisers of a row pair are computed once and serve both.
+//
+// Work layout: the streaming layout of distill_stream.hip.  About one
+// workgroup per CU walks the items g, g+G, ...: the B*K row pairs
+// (target row i, draft row i) numbered position-major (item i*B + b), then
+// the B bonus rows (target row k_b).  While one item is computed, the next
+// one's chunks are in flight.  Per row pair:
+//   1. statistics pass (max and sum of exponentials of both rows; fills the
+//      per-element cache; the thread holding y_i posts t_i[y_i], d_i[y_i]);
+//   2. workgroup merge of the normalisers;
+//   3. acceptance test; if the proposal is rejected and no earlier rejection
+//      of the sequence is known to this workgroup, the correction draw from
+//      the cache (exact fixed-point inverse CDF);
+//   4. loss and gradient passes from the cache, for rows with mask 1.
+// Bonus rows run 1-3 on the target row alone, and are not read at all when
+// an earlier rejection of their sequence is known.  Each item posts a
+// one-word record; the last workgroup to finish reduces the loss and turns
+// the records of every sequence into the outputs.
+#include "osd.h"
+#include "osd_device.hpp"
+#include "osd_internal.hpp"
+#include "stream_device.hpp"
+#include "distill_common.hpp"
+
+namespace osd {
+namespace {
+
+// Record word: state in bits 31..28, token in bits 27..0.
+enum : uint32_t {
+    kRecAccept = 1,
+    kRecReject = 2,          // rejected, correction token attached
+    kRecRejectSkipped = 3,   // rejected after a known earlier rejection
+    kRecBadRow = 4,          // no finite logit in a row that was read
+    kRecBadToken = 5,        // proposal outside [0, V)
+    kRecBonus = 6,           // bonus token attached
+    kRecBonusSkipped = 7,    // an earlier rejection was known
+};
+__device__ inline uint32_t make_rec(uint32_t state, uint32_t tok) { return (state << 28) | (tok & 0x0FFFFFFFu); }
+
+// Masses are probabilities (at most 1 per element); chunk sums become exact
+// 2^-40 fixed point, so every partial sum of the CDF is an exact integer.
+constexpr int kFixedShift = 40;
+// Items per workgroup (their arguments are staged in LDS) and the outcomes a
+// workgroup remembers.
+constexpr int kMaxItems = 256;
+
+struct FusedArgs {
+    const void* target;  // [B, K+1, V]
+    const void* draft;   // [B, K, V]
+    int B, K, V;
+    const int32_t* tokens;     // [B, K]
+    const int32_t* draft_len;  // [B] or null
+    const float* u_accept;     // [B, K]
+    const float* u_resample;   // [B]
+    const uint8_t* mask;       // [B, K] distillation mask or null (all rows)
+    float c2;                  // log2(e) / T
+    double c2d;
+    float inv_tau;             // 1 / T
+    float beta;
+    uint32_t* records;         // [B, K+1], zero between calls
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    float* row_loss_out;       // [B, K] or null
+    void* grad_out;            // [B, K, V] or null
+    double* part_ws;           // [G] loss partials, zero between calls
+    uint32_t* done;            // workgroups finished, zero between calls
+    float* loss_out;
+    int nitems;                // B*K + B
+    int nchunks;
+    uint32_t row_bytes;
+    int seq_step;              // items k and k - seq_step of a workgroup share a sequence
+};
+
+// Per-item arguments, loaded once per workgroup (thread j: its j-th item)
+// and staged in LDS, so nothing in the item loop reads global memory except
+// the rows (a scalar load there would share its wait counter with LDS).
+struct Meta {
+    int kb, y;
+    float u, u_res;
+    int on;  // distillation mask flag
+};
+
+__device__ inline Meta load_meta(const FusedArgs& a, int it) {
+    Meta m;
+    const int BK = a.B * a.K;
+    const bool bonus = it >= BK;
+    const int i = bonus ? 0 : it / a.B;
+    const int b = bonus ? it - BK : it - i * a.B;
+    m.kb = a.draft_len ? a.draft_len[b] : a.K;
+    const int64_t ti = int64_t(b) * a.K + i;
+    m.y = bonus ? 0 : a.tokens[ti];
+    m.u = bonus ? 0.0f : a.u_accept[ti];
+    m.u_res = a.u_resample[b];
+    m.on = bonus ? 0 : (a.mask ? int(a.mask[ti]) : 1);
+    return m;
+}
+
+__device__ inline Meta meta_at(const Meta* s_meta, int k) {
+    const Meta v = s_meta[k];
+    Meta m;
+    m.kb = __builtin_amdgcn_readfirstlane(v.kb);
+    m.y = __builtin_amdgcn_readfirstlane(v.y);
+    m.u = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v.u)));
+    m.u_res = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v.u_res)));
+    m.on = __builtin_amdgcn_readfirstlane(v.on);
+    return m;
+}
+
+enum : int { kItemNone = 0, kItemBadToken = 1, kItemLive = 2 };
+
+struct Item {
+    int b, i;
+    bool bonus;
+    int vkind;    // verification: none, bad token or live
+    bool dist;    // distillation row with mask 1
+    int y;
+    float u, u_res;
+    const char* trow;
+    const char* drow;
+    int grow;     // gradient and row-loss index b*K + i, or -1 (bonus row)
+};
+
+template <typename Fmt>
+__device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
+    Item t;
+    t.vkind = kItemNone;
+    t.dist = false;
+    t.trow = nullptr;
+    t.drow = nullptr;
+    t.grow = -1;
+    t.y = m.y;
+    t.u = m.u;
+    t.u_res = m.u_res;
+    const int BK = a.B * a.K;
+    t.bonus = it >= BK;
+    const int i = t.bonus ? 0 : it / a.B;
+    t.b = t.bonus ? it - BK : it - i * a.B;
+    t.i = t.bonus ? m.kb : i;
+    if (it < 0 || it >= a.nitems) return t;
+    const bool kb_ok = m.kb >= 1 && m.kb <= a.K;
+    if (!t.bonus) {
+        t.grow = t.b * a.K + i;
+        t.dist = m.on != 0;
+        if (kb_ok && i < m.kb) t.vkind = (m.y < 0 || m.y >= a.V) ? kItemBadToken : kItemLive;
+    } else if (kb_ok) {
+        t.vkind = kItemLive;
+    }
+    if (t.vkind == kItemLive || t.dist) {
+        t.trow = static_cast<const char*>(a.target) + (int64_t(t.b) * (a.K + 1) + t.i) * int64_t(a.V) * Fmt::kBytes;
+        if (!t.bonus)
+            t.drow = static_cast<const char*>(a.draft) + (int64_t(t.b) * a.K + t.i) * int64_t(a.V) * Fmt::kBytes;
+    }
+    return t;
+}
+
+// s_rej[k] = 1 if item k of this workgroup or an earlier item of the same
+// sequence ended the test (or could not be tested).  The previous item of
+// the same sequence is k - seq_step.
+__device__ inline bool known_rejection(const uint8_t* s_rej, int k, int seq_step) {
+    const int kk = k - seq_step;
+    return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
+}
+
+// Inverse-CDF draw over the cached row pair.  mass(r, e, residual) gives the
+// fp32 mass of element e of round r (residual: max(0, p - q); else p) and
+// mass_at(rr, e, residual) the same for a round rr known only at run time.
+// Token order is chunk order c = r*W + tid, then element; the cells are
+// (round r, wave w, lane).  Pass A sums each thread's chunks exactly in fixed
+// point and posts each (round, wave) total; one wave scans them
+// (CPT*NW <= 64 cells).  The wave whose cell holds u*Z recomputes that
+// round's chunk sums -- the same fp32 additions of the same values -- finds
+// the lane, and the lane walks its elements.  Returns the token (uniform),
+// or -1 if there is no mass at all.  All threads call it.
+template <int W, int CPT, int EPC, typename MassFn, typename MassAtFn>
+__device__ int draw_cached(MassFn mass, MassAtFn mass_at, bool residual, float u, unsigned long long* s_cell,
+                           unsigned long long* s_z, int* s_tok) {
+    constexpr int NW = W / kWave, CELLS = CPT * NW;
+    static_assert(CELLS <= kWave, "one wave scans the cells");
+    const int tid = opaque_tid(), lane = tid & (kWave - 1), wid = tid / kWave;
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        float sm = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) sm = sm + mass(r, e, residual);
+        const uint64_t incl = wave_scan_add(to_fixed<kFixedShift>(sm));
+        if (lane == kWave - 1) s_cell[r * NW + wid] = incl;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    if (wid == 0) {
+        const uint64_t cv = lane < CELLS ? uint64_t(s_cell[lane]) : 0;
+        const uint64_t ci = wave_scan_add(cv);
+        if (lane < CELLS) s_cell[lane] = ci - cv;  // exclusive prefix
+        if (lane == kWave - 1) *s_z = ci;
+        if (lane == 0) *s_tok = -1;
+    }
+    __syncthreads();
+    const uint64_t Z = *s_z;
+    int tok = -1;
+    if (Z > 0) {
+        uint64_t target = static_cast<uint64_t>(double(u) * double(Z));
+        if (target >= Z) target = Z - 1;
+        // The round whose cell of this wave holds the target (uniform).
+        int rr = -1;
+        uint64_t lo = 0;
+        for (int r = 0; r < CPT; ++r) {
+            const int c = r * NW + wid;
+            const uint64_t l = s_cell[c];
+            const uint64_t h = c + 1 < CELLS ? uint64_t(s_cell[c + 1]) : Z;
+            if (l <= target && target < h) {
+                rr = r;
+                lo = l;
+            }
+        }
+        if (rr >= 0) {
+            float m[EPC];
+            float sm = 0.0f;
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                m[e] = mass_at(rr, e, residual);
+                sm = sm + m[e];
+            }
+            const uint64_t f = to_fixed<kFixedShift>(sm);
+            const uint64_t mylo = lo + wave_scan_add(f) - f;
+            if (f > 0 && mylo <= target && target < mylo + f) {
+                const uint64_t want = target - mylo;
+                float racc = 0.0f;
+                int pick = -1, last_pos = -1;
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    racc = racc + m[e];
+                    if (m[e] > 0.0f) last_pos = e;
+                    if (pick < 0 && to_fixed<kFixedShift>(racc) > want) pick = e;
+                }
+                if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+                *s_tok = (rr * W + tid) * EPC + pick;
+            }
+        }
+        __syncthreads();
+        tok = *s_tok;
+    }
+    __syncthreads();  // s_cell, s_z and s_tok are rewritten by the next draw
+    return tok;
+}
+
+// What the last workgroup needs, staged in LDS at kernel start so that none
+// of it stays in registers across the item loop.
+struct FusedTail {
+    double* part_ws;
+    uint32_t* done;
+    float* loss_out;
+    const uint8_t* mask;
+    int nrows;
+    uint32_t* records;
+    const int32_t* draft_len;
+    const int32_t* tokens;
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    int B, K;
+};
+
+// Every workgroup posts its loss partial and arrives; the last one
+//  - adds the partials in workgroup order and counts the mask (fixed order,
+//    fp64), writing {mean, sum};
+//  - turns each sequence's records into the outputs (one wave per sequence,
+//    lane j = position j): the first position whose record is not an
+//    acceptance ends the test; a proposal outside the vocabulary invalidates
+//    the sequence wherever it sits, a row without finite logits only if the
+//    test reaches it;
+//  - reads every record and partial with an exchange that leaves zero.
+template <int W>
+__device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
+    constexpr int NW = W / kWave;
+    __shared__ int s_last;
+    __shared__ double s_sum[NW], s_cnt[NW];
+    // Thread indices from an opaque copy: nothing derived from them before
+    // the item loop is kept alive across it.
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & (kWave - 1), wid = tid / kWave;
+    const int G = gridDim.x;
+    __syncthreads();
+    if (tid == 0) {
+        __hip_atomic_exchange(&a.part_ws[blockIdx.x], s_part[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = int(arrive(a.done)) == G - 1;  // after this workgroup's posts completed
+    }
+    __syncthreads();
+    if (!s_last) return;
+    double sm = 0.0, cn = 0.0;
+    for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
+    for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
+    sm = wave_sum(sm);
+    cn = wave_sum(cn);
+    if (lane == 0) {
+        s_sum[wid] = sm;
+        s_cnt[wid] = cn;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double ts = 0.0, tc = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            ts += s_sum[w];
+            tc += s_cnt[w];
+        }
+        a.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
+        a.loss_out[1] = float(ts);
+    }
+    const int K = a.K;
+    for (int b = wid; b < a.B; b += NW) {
+        const int kb = a.draft_len ? a.draft_len[b] : K;
+        int32_t* ot = a.out_tokens + int64_t(b) * (K + 1);
+        uint8_t* rm = a.reject_mask ? a.reject_mask + int64_t(b) * K : nullptr;
+        if (kb < 1 || kb > K) {
+            if (lane <= K) ot[lane] = -1;
+            if (rm && lane < K) rm[lane] = 0;
+            if (lane == 0) a.accepted_len[b] = -1;
+            continue;
+        }
+        const uint32_t r = lane <= kb ? take_u32(&a.records[int64_t(b) * (K + 1) + lane]) : 0u;
+        const uint32_t st = r >> 28;
+        const bool bad_token = __ballot(lane < kb && st == kRecBadToken) != 0;
+        const uint64_t stop = __ballot(lane < kb && st != kRecAccept);
+        const int acc = stop ? __builtin_ctzll(stop) : kb;
+        const uint32_t ra = __shfl(r, acc, kWave);
+        const uint32_t sa = ra >> 28;
+        bool bad = bad_token;
+        int extra = -1;
+        if (!bad) {
+            if (acc < kb ? sa == kRecReject : sa == kRecBonus)
+                extra = int(ra & 0x0FFFFFFFu);
+            else
+                bad = true;  // a row without finite logits where the test stopped
+        }
+        if (lane <= K) {
+            int32_t o = -1;
+            if (!bad) o = lane < acc ? a.tokens[int64_t(b) * K + lane] : (lane == acc ? extra : -1);
+            ot[lane] = o;
+            if (rm && lane < K) rm[lane] = (!bad && lane == acc && acc < kb) ? 1 : 0;
+        }
+        if (lane == 0) a.accepted_len[b] = bad ? -1 : acc;
+    }
+    if (tid == 0) take_u32(a.done);
+}
+
+template <typename Fmt, int W, int CPT, int KIND>
+__global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
+    constexpr int NW = W / kWave, EPC = Fmt::kPerChunk, NG = EPC / 4;
+    __shared__ float s_k[2 * NW];
+    __shared__ double s_s[2 * NW];
+    __shared__ double s_a[2 * NW];
+    __shared__ Meta s_meta[kMaxItems];
+    __shared__ uint8_t s_rej[kMaxItems];
+    __shared__ float s_y[2];
+    __shared__ unsigned long long s_cell[CPT * NW];
+    __shared__ unsigned long long s_z;
+    __shared__ int s_tok;
+    __shared__ double s_part[1];
+    __shared__ FusedTail s_tail;
+    __shared__ f32x4_t s_c0[CPT * NG * W];
+    const LdsCache<W, EPC> lc{s_c0};
+
+    const int tid = threadIdx.x;
+    const int G = gridDim.x;
+    const float c2 = a.c2;
+    const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
+    const float beta = a.beta, omb = 1.0f - a.beta;
+
+    chunk_t rt[CPT], rs[CPT];
+    float c1[CPT][EPC];
+
+    const int nk = (a.nitems - int(blockIdx.x) + G - 1) / G;
+    if (tid == 0) {
+        s_part[0] = 0.0;  // read and written by thread 0 only
+        s_tail.part_ws = a.part_ws;
+        s_tail.done = a.done;
+        s_tail.loss_out = a.loss_out;
+        s_tail.mask = a.mask;
+        s_tail.nrows = a.B * a.K;
+        s_tail.records = a.records;
+        s_tail.draft_len = a.draft_len;
+        s_tail.tokens = a.tokens;
+        s_tail.accepted_len = a.accepted_len;
+        s_tail.out_tokens = a.out_tokens;
+        s_tail.reject_mask = a.reject_mask;
+        s_tail.B = a.B;
+        s_tail.K = a.K;
+    }
+    Meta mine;
+    mine.kb = 0;
+    mine.y = 0;
+    mine.u = 0.0f;
+    mine.u_res = 0.0f;
+    mine.on = 0;
+    if (tid < nk) mine = load_meta(a, int(blockIdx.x) + tid * G);
+
+    // The pipeline starts one step early: step -1 computes nothing; it issues
+    // the loads of the first item from the same code as every later step and
+    // stages the item arguments.  The first item's rows are read before its
+    // arguments are known (in bounds either way; a bonus row, whose index is
+    // k_b, reads k_b directly).
+    Item cur;
+    cur.vkind = kItemNone;
+    cur.dist = false;
+    cur.bonus = false;
+    cur.b = 0;
+    cur.i = 0;
+    cur.y = 0;
+    cur.u = 0.0f;
+    cur.u_res = 0.0f;
+    cur.trow = nullptr;
+    cur.drow = nullptr;
+    cur.grow = -1;
+    int cur_skip = 0;
+    for (int k = -1, it = int(blockIdx.x) - G; it < a.nitems; it += G, ++k) {
+        Item nxt;
+        bool nload;
+        int nxt_skip = 0;
+        if (k < 0) {
+            Meta m0;
+            m0.kb = a.K;
+            m0.y = 0;
+            m0.u = 0.0f;
+            m0.u_res = 0.0f;
+            m0.on = 1;
+            if (it + G >= a.B * a.K && it + G < a.nitems && a.draft_len)
+                m0.kb = scalar_load(a.draft_len + (it + G - a.B * a.K));
+            nxt = decode_item<Fmt>(a, it + G, m0);
+            nload = nxt.trow != nullptr;
+        } else {
+            Meta mn;
+            mn.kb = 0;
+            mn.y = 0;
+            mn.u = 0.0f;
+            mn.u_res = 0.0f;
+            mn.on = 0;
+            if (k + 1 < nk) mn = meta_at(s_meta, k + 1);
+            nxt = decode_item<Fmt>(a, it + G, mn);
+            nload = nxt.trow != nullptr;
+            // A bonus row whose sequence already stopped here is not read
+            // (the current item's outcome is not known yet).
+            if (nload && nxt.bonus && a.seq_step > 1 && known_rejection(s_rej, k + 1, a.seq_step)) {
+                nload = false;
+                nxt_skip = 1;
+            }
+        }
+        const rsrc_t ntr = make_rsrc(nload ? nxt.trow : a.target, nload ? a.row_bytes : 0u);
+        const rsrc_t nsr = make_rsrc(nload && nxt.drow ? nxt.drow : a.target, nload && nxt.drow ? a.row_bytes : 0u);
+        if (k >= 0) cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
+        const bool vlive = cur.vkind == kItemLive && !cur_skip;
+        const bool live = vlive || cur.dist;
+        const int ychunk = cur.y / EPC;
+        const rsrc_t gr = make_rsrc(a.grad_out && cur.grow >= 0 && k >= 0
+                                        ? static_cast<char*>(a.grad_out) + int64_t(cur.grow) * a.row_bytes
+                                        : static_cast<char*>(nullptr),
+                                    a.grad_out && cur.grow >= 0 && k >= 0 ? a.row_bytes : 0u);
+        double D = 0.0;
+        // ---- statistics pass: consumes the raw chunks and reloads each with
+        // the next item's (one load sequence for every item: a branch around
+        // the loads would make the compiler wait for all of them) ----
+        float kc_t = 0.0f, kc_s = 0.0f;
+        double S_t = 0.0, S_s = 0.0;
+#pragma unroll
+        for (int r = 0; r < CPT; ++r) {
+            if (live) {
+                chunk_t xt = rt[r], xs = rs[r];
+                if (r == CPT - 1 && !last_ok) {
+                    xt = pad_chunk<Fmt>();
+                    xs = pad_chunk<Fmt>();
+                }
+                if (vlive && !cur.bonus && r * W + tid == ychunk) {
+                    s_y[0] = Fmt::get(xt, cur.y - ychunk * EPC);
+                    s_y[1] = Fmt::get(xs, cur.y - ychunk * EPC);
+                }
+                if (r == 0) {
+                    kc_t = first_chunk_shift<Fmt>(xt, c2);
+                    kc_s = first_chunk_shift<Fmt>(xs, c2);
+                }
+                float st = 0.0f, ss = 0.0f;
+#pragma unroll
+                for (int g = 0; g < NG; ++g) {
+                    float c0v[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int e = 4 * g + j;
+                        const float t = Fmt::get(xt, e), s = Fmt::get(xs, e);
+                        const float vt = __builtin_fmaf(t, c2, -kc_t);
+                        const float vs = __builtin_fmaf(s, c2, -kc_s);
+                        st = st + exp2_fast(vt);
+                        ss = ss + exp2_fast(vs);
+                        if constexpr (KIND == 2) {
+                            c0v[j] = fmaxf(vt, kLogFloor);
+                            c1[r][e] = fmaxf(vs, kLogFloor);
+                        } else {
+                            c0v[j] = t - s;
+                            c1[r][e] = KIND == 0 ? vt : vs;
+                        }
+                    }
+                    lc.store(r, g, f32x4_t{c0v[0], c0v[1], c0v[2], c0v[3]});
+                }
+                // Keep each round's sums in the round.
+                asm volatile("" : "+v"(st), "+v"(ss));
+                S_t += double(st);
+                S_s += double(ss);
+            }
+            rt[r] = load_chunk<W>(ntr, r);
+            rs[r] = load_chunk<W>(nsr, r);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (k < 0) {  // step -1: stage the item arguments
+            if (tid < nk) s_meta[tid] = mine;
+            __syncthreads();
+        }
+        // The record of an item that is not tested (a proposal outside the
+        // vocabulary, or a bonus row known to be unneeded); a tested item
+        // replaces it below.  Its row may still be distilled.
+        uint32_t record = 0u;
+        bool stopped = false;  // this item ended the test (or could not be tested)
+        if (cur.vkind == kItemBadToken) {
+            record = make_rec(kRecBadToken, 0);
+            stopped = true;
+        } else if (cur.vkind == kItemLive && !vlive) {
+            record = make_rec(kRecBonusSkipped, 0);
+            stopped = true;
+        }
+        if (!live) {
+            if (cur.grow >= 0 && a.grad_out) {
+#pragma unroll
+                for (int r = 0; r < CPT; ++r) store_chunk<W>(gr, r, chunk_t{0u, 0u, 0u, 0u});
+            }
+        } else {
+            // Exponent range exceeded by an element far above the first
+            // chunk's maximum: rescale exactly from the cache.
+            float ks_t = kc_t, ks_s = kc_s;
+            if (!(S_t < 1.0e300)) {
+                ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float {
+                    if constexpr (KIND == 2) return lc.load(r, e / 4)[e % 4];
+                    else if constexpr (KIND == 0) return c1[r][e];
+                    else return c1[r][e] + (kc_s - kc_t) + lc.load(r, e / 4)[e % 4] * c2;
+                });
+            }
+            if (!(S_s < 1.0e300)) {
+                ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float {
+                    if constexpr (KIND == 2) return c1[r][e];
+                    else if constexpr (KIND == 1) return c1[r][e];
+                    else return c1[r][e] + (kc_t - kc_s) - lc.load(r, e / 4)[e % 4] * c2;
+                });
+            }
+            float Kt = ks_t, Ks = ks_s;
+            double St = S_t, Ss = S_s;
+            block_merge2<NW>(Kt, St, Ks, Ss, s_k, s_s);
+            // log2 p_j = (t_j c2 - K_t) - (K_row_t - K_t + log2 S_t) = c - ct, likewise q.
+            const double Tt = double(Kt) + log2(St), Ts = double(Ks) + log2(Ss);
+            const float ct = float(Tt - double(kc_t)), cs = float(Ts - double(kc_s));
+            const float dT = float(Tt - Ts);  // log2 p - log2 q = (t - s) c2 - dT
+
+            // ---- verification ----
+            if (vlive) {
+                const bool bad = !(St > 0.0 && St < 1.0e300) || (!cur.bonus && !(Ss > 0.0 && Ss < 1.0e300));
+                const bool earlier = known_rejection(s_rej, k, a.seq_step);
+                bool want_draw = false;
+                if (bad) {
+                    record = make_rec(kRecBadRow, 0);
+                    stopped = true;
+                } else if (!cur.bonus) {
+                    // p(y)/q(y) = 2^e with e = (t_y c2 - T_t) - (d_y c2 - T_s)
+                    // in fp64 (T: the rows' log2 normalisers); 2^e is split
+                    // into an exact power of two and 2^frac (v_exp_f32).
+                    const double e = (double(s_y[0]) * a.c2d - Tt) - (double(s_y[1]) * a.c2d - Ts);
+                    double ratio;
+                    if (!(e > -2000.0)) {
+                        ratio = 0.0;  // p(y) = 0
+                    } else if (e > 2000.0) {
+                        ratio = __builtin_huge_val();
+                    } else {
+                        const double fl = floor(e);
+                        ratio = __builtin_ldexp(double(exp2_fast(float(e - fl))), int(fl));
+                    }
+                    const bool accept = double(cur.u) < ratio;
+                    stopped = !accept;
+                    want_draw = !accept && !earlier;
+                    record = accept ? make_rec(kRecAccept, 0) : make_rec(kRecRejectSkipped, 0);
+                } else {
+                    stopped = true;
+                    want_draw = !earlier;
+                    record = make_rec(kRecBonusSkipped, 0);
+                }
+                if (want_draw) {
+                    // Element masses from the cache; the sums and the walk
+                    // evaluate exactly this formula on the same values.
+                    auto formula = [&](float c0, float cc1, bool residual) -> float {
+                        float lp, lq;
+                        if constexpr (KIND == 2) {
+                            lp = c0 - ct;
+                            lq = cc1 - cs;
+                        } else {
+                            const float lr = fmaxf(fminf(__builtin_fmaf(c0, c2, -dT), -kLogFloor), kLogFloor);
+                            if constexpr (KIND == 0) {
+                                lp = cc1 - ct;
+                                lq = lp - lr;
+                            } else {
+                                lq = cc1 - cs;
+                                lp = lq + lr;
+                            }
+                        }
+                        const float p = exp2_fast(lp);
+                        if (!residual) return p;
+                        return fmaxf(p - exp2_fast(lq), 0.0f);
+                    };
+                    auto mass = [&](int r, int e, bool residual) -> float {
+                        return formula(lc.load(r, e / 4)[e % 4], c1[r][e], residual);
+                    };
+                    // Round rr known at run time: the register half of the
+                    // cache is picked with opaque bit masks, so that the
+                    // compiler cannot turn the pick into an indexed access
+                    // (which would move the whole cache to scratch memory).
+                    auto mass_at = [&](int rr, int e, bool residual) -> float {
+                        uint32_t bits = 0u;
+#pragma unroll
+                        for (int r = 0; r < CPT; ++r) {
+                            uint32_t m = 0u - uint32_t(rr == r);
+                            asm volatile("" : "+v"(m));
+                            bits |= __float_as_uint(c1[r][e]) & m;
+                        }
+                        return formula(lc.load(rr, e / 4)[e % 4], __uint_as_float(bits), residual);
+                    };
+                    // No residual mass left after rounding (p = q to fp32
+                    // accuracy): draw from p.
+                    int tok = -1;
+                    for (int pass = cur.bonus ? 1 : 0; pass < 2 && tok < 0; ++pass)
+                        tok = draw_cached<W, CPT, EPC>(mass, mass_at, pass == 0, cur.u_res, s_cell, &s_z, &s_tok);
+                    if (tok < 0 || tok >= a.V)
+                        record = make_rec(kRecBadRow, 0);
+                    else
+                        record = make_rec(cur.bonus ? kRecBonus : kRecReject, uint32_t(tok));
+                }
+                stopped = stopped || earlier;
+            }
+
+            // ---- distillation ----
+            if (cur.dist) {
+                float acc0 = 0.0f, acc1 = 0.0f;
+#pragma unroll
+                for (int r = 0; r < CPT; ++r) {
+                    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+                    for (int g = 0; g < NG; ++g) {
+                        const f32x4_t v = lc.load(r, g);
+                        float c0v[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const int e = 4 * g + j;
+                            if constexpr (KIND == 2) {
+                                const float lp = c0v[j] - ct, lq = c1[r][e] - cs;
+                                const float p = exp2_fast(lp), q = exp2_fast(lq);
+                                const float lm = log2_fast(__builtin_fmaf(beta, p, __builtin_fmaf(omb, q, kMixFloor)));
+                                const float x = lq - lm;
+                                a0 = __builtin_fmaf(p, lp - lm, a0);
+                                a1 = __builtin_fmaf(q, x, a1);
+                                c0v[j] = x;
+                                c1[r][e] = q;
+                            } else {
+                                // log2(p/q), clamped so that a zero probability
+                                // times an infinite log-ratio stays 0.
+                                const float lr = fmaxf(fminf(__builtin_fmaf(c0v[j], c2, -dT), -kLogFloor), kLogFloor);
+                                if constexpr (KIND == 0) {
+                                    const float lp = c1[r][e] - ct;
+                                    const float p = exp2_fast(lp);
+                                    a0 = __builtin_fmaf(p, lr, a0);
+                                    c0v[j] = p;
+                                    c1[r][e] = lp - lr;
+                                } else {
+                                    const float q = exp2_fast(c1[r][e] - cs);
+                                    a0 = __builtin_fmaf(q, lr, a0);
+                                    c0v[j] = lr;
+                                    c1[r][e] = q;
+                                }
+                            }
+                        }
+                        lc.store(r, g, f32x4_t{c0v[0], c0v[1], c0v[2], c0v[3]});
+                    }
+                    acc0 = acc0 + a0;
+                    acc1 = acc1 + a1;
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                double A0 = double(acc0), A1 = KIND == 2 ? double(acc1) : 0.0;
+                block_sum2<NW>(A0, A1, s_a);
+                // Terms were accumulated in log2 units.
+                if constexpr (KIND == 2)
+                    D = kLn2 * (double(a.beta) * A0 + (1.0 - double(a.beta)) * A1);
+                else if constexpr (KIND == 0)
+                    D = kLn2 * A0;
+                else
+                    D = -kLn2 * A0;
+
+                if (a.grad_out) {
+                    const float ln2 = float(kLn2);
+                    // JSD: (1-beta) ln2/tau * q * (x - KL2);  RKL: ln2/tau * q * (A0 - lr)
+                    const float scale = KIND == 2 ? omb * ln2 * a.inv_tau : ln2 * a.inv_tau;
+                    const float shift = KIND == 2 ? float(A1) : float(A0);
+#pragma unroll
+                    for (int r = 0; r < CPT; ++r) {
+                        float g[EPC];
+#pragma unroll
+                        for (int q4 = 0; q4 < NG; ++q4) {
+                            const f32x4_t v = lc.load(r, q4);
+                            const float c0v[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                const int e = 4 * q4 + j;
+                                if constexpr (KIND == 0)
+                                    g[e] = (exp2_fast(c1[r][e]) - c0v[j]) * a.inv_tau;
+                                else if constexpr (KIND == 2)
+                                    g[e] = (c1[r][e] * scale) * (c0v[j] - shift);
+                                else
+                                    g[e] = (c1[r][e] * scale) * (shift - c0v[j]);
+                            }
+                        }
+                        store_chunk<W>(gr, r, pack_grad<Fmt>(g));
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            } else if (cur.grow >= 0 && a.grad_out) {
+#pragma unroll
+                for (int r = 0; r < CPT; ++r) store_chunk<W>(gr, r, chunk_t{0u, 0u, 0u, 0u});
+            }
+        }
+        if (tid == 0 && k >= 0) {
+            if (cur.grow >= 0) {
+                if (a.row_loss_out) a.row_loss_out[cur.grow] = float(D);
+                s_part[0] += D;  // this workgroup's rows, in item order
+            }
+            if (cur.vkind != kItemNone)  // posted at the coherence point; waited for once, at the end
+                __hip_atomic_exchange(&a.records[int64_t(cur.b) * (a.K + 1) + cur.i], record, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+            if (k < kMaxItems) s_rej[k] = (stopped || known_rejection(s_rej, k, a.seq_step)) ? 1 : 0;
+        }
+        __syncthreads();  // s_y, s_rej and the draw cells are reused by the next item
+        cur_skip = nxt_skip;
+    }
+    finish_fused<W>(s_tail, s_part);
+}
+
+template <typename Fmt, int W, int CPT, int KIND>
+int blocks_per_cu() {
+    static const int v = [] {
+        int nb = 0;
+        const hipError_t e =
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_distill_kernel<Fmt, W, CPT, KIND>, W, 0);
+        return (e != hipSuccess || nb < 1) ? 1 : nb;
+    }();
+    return v;
+}
+
+template <typename Fmt, int W, int CPT, int KIND>
+hipError_t launch_kind(const FusedLaunch& L, FusedArgs a) {
+    int64_t want = int64_t(L.cus) * blocks_per_cu<Fmt, W, CPT, KIND>();
+    const int64_t min_grid = (int64_t(a.nitems) + kMaxItems - 1) / kMaxItems;
+    if (want < min_grid) want = min_grid;
+    const unsigned grid = unsigned(want < a.nitems ? want : a.nitems);
+    int g = int(grid), r = a.B;
+    while (r != 0) {
+        const int t = g % r;
+        g = r;
+        r = t;
+    }
+    a.seq_step = a.B / g;
+    hipLaunchKernelGGL((verify_distill_kernel<Fmt, W, CPT, KIND>), dim3(grid), dim3(W), 0, L.stream, a);
+    return hipGetLastError();
+}
+
+template <typename Fmt, int W, int CPT>
+hipError_t launch_tile(const FusedLaunch& L, const FusedArgs& a) {
+    switch (L.kind) {
+        case 0: return launch_kind<Fmt, W, CPT, 0>(L, a);
+        case 1: return launch_kind<Fmt, W, CPT, 1>(L, a);
+        default: return launch_kind<Fmt, W, CPT, 2>(L, a);
+    }
+}
+
+template <typename Fmt>
+hipError_t launch_fmt(const FusedLaunch& L, const FusedArgs& a) {
+    RowTile t;
+    if (!pick_stream_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    switch (t.W * 100 + t.CPT) {
+        case 25601: return launch_tile<Fmt, 256, 1>(L, a);
+        case 51201: return launch_tile<Fmt, 512, 1>(L, a);
+        case 102401: return launch_tile<Fmt, 1024, 1>(L, a);
+        case 102402: return launch_tile<Fmt, 1024, 2>(L, a);
+        case 102403: return launch_tile<Fmt, 1024, 3>(L, a);
+        case 102404: return launch_tile<Fmt, 1024, 4>(L, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_verify_distill(const FusedLaunch& L) {
+    FusedArgs a;
+    a.target = L.target;
+    a.draft = L.draft;
+    a.B = L.B;
+    a.K = L.K;
+    a.V = L.V;
+    a.tokens = L.tokens;
+    a.draft_len = L.draft_len;
+    a.u_accept = L.u_accept;
+    a.u_resample = L.u_resample;
+    a.mask = L.mask;
+    a.c2 = float(1.4426950408889634 / double(L.temperature));
+    a.c2d = double(a.c2);
+    a.inv_tau = float(1.0 / double(L.temperature));
+    a.beta = L.beta;
+    a.records = L.records;
+    a.accepted_len = L.accepted_len;
+    a.out_tokens = L.out_tokens;
+    a.reject_mask = L.reject_mask;
+    a.row_loss_out = L.row_loss_out;
+    a.grad_out = L.grad_out;
+    a.part_ws = L.part_ws;
+    a.done = L.done;
+    a.loss_out = L.loss_out;
+    a.nitems = L.B * L.K + L.B;
+    const int eb = L.dtype == 1 ? 2 : 4;
+    a.nchunks = int((int64_t(L.V) * eb) / 16);
+    a.row_bytes = uint32_t(int64_t(L.V) * eb);
+    a.seq_step = 1;
+    return L.dtype == 1 ? launch_fmt<BF16>(L, a) : launch_fmt<F32>(L, a);
+}
+
+}  // namespace osd

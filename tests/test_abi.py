@@ -103,3 +103,36 @@ def test_binding_fails_loudly_without_gpu_tensors():
     with pytest.raises(ValueError):
         osd.osd_verify(t, t[:, :1].contiguous(), torch.zeros(1, 1, dtype=torch.int32),
                        torch.zeros(1, 1), torch.zeros(1), 1.0)
+
+
+def fused(**kw):
+    a = dict(target=FAKE, draft=FAKE, dtype=1, B=2, K=3, V=64, tokens=FAKE, dlen=None, ua=FAKE, ur=FAKE,
+             T=0.8, acc=FAKE, toks=FAKE, rmask=None, mask=None, kind=2, beta=0.5, loss=FAKE, rows=None,
+             grad=None, ws=FAKE, wsb=1 << 20, stream=None)
+    a.update(kw)
+    return osd.lib().osd_verify_distill(a["target"], a["draft"], a["dtype"], a["B"], a["K"], a["V"],
+                                        a["tokens"], a["dlen"], a["ua"], a["ur"], a["T"], a["acc"],
+                                        a["toks"], a["rmask"], a["mask"], a["kind"], a["beta"], a["loss"],
+                                        a["rows"], a["grad"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(target=None), -1), (dict(draft=None), -1), (dict(tokens=None), -1), (dict(ua=None), -1),
+    (dict(ur=None), -1), (dict(acc=None), -1), (dict(toks=None), -1), (dict(loss=None), -1),
+    (dict(B=0), -1), (dict(K=0), -1), (dict(K=17), -1), (dict(V=0), -1), (dict(dtype=2), -1),
+    (dict(V=1 << 20), -2),
+    (dict(T=0.0), -1), (dict(T=-1.0), -1), (dict(T=float("nan")), -1), (dict(T=float("inf")), -1),
+    (dict(kind=3), -1), (dict(beta=1.01), -1), (dict(beta=float("nan")), -1),
+    (dict(ws=None), -4), (dict(wsb=64), -4), (dict(ws=ctypes.c_void_p(0x1008)), -4),
+])
+def test_fused_rejects_bad_arguments(kw, status):
+    assert fused(**kw) == status
+
+
+def test_fused_workspace_covers_both_entry_points():
+    L = osd.lib()
+    for B, K in [(1, 1), (64, 8), (256, 16)]:
+        assert L.osd_verify_distill_workspace_bytes(B, K) >= (L.osd_verify_workspace_bytes(B, K)
+                                                             + L.osd_distill_workspace_bytes(B, K))
+    assert L.osd_verify_distill_workspace_bytes(4, 17) == 0
+    assert L.osd_verify_distill_workspace_bytes(0, 4) == 0
