@@ -173,6 +173,13 @@ __device__ inline bool known_rejection(const uint8_t* s_rej, int k, int seq_step
     const int kk = k - seq_step;
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
 }
+// The same, asked while item k - 1 is still being computed (its entry is not
+// written yet): the latest finished item of item k's sequence is consulted.
+__device__ inline bool known_rejection_ahead(const uint8_t* s_rej, int k, int seq_step) {
+    int kk = k - seq_step;
+    if (kk >= k - 1) kk -= seq_step;
+    return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
+}
 
 // Inverse-CDF draw over the cached row pair.  mass(r, e, residual) gives the
 // fp32 mass of element e of round r (residual: max(0, p - q); else p) and
@@ -364,6 +371,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ double s_a[2 * NW];
     __shared__ Meta s_meta[kMaxItems];
     __shared__ uint8_t s_rej[kMaxItems];
+    __shared__ int s_flag;
     __shared__ float s_y[2];
     __shared__ unsigned long long s_cell[CPT * NW];
     __shared__ unsigned long long s_z;
@@ -383,6 +391,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     float c1[CPT][EPC];
 
     const int nk = (a.nitems - int(blockIdx.x) + G - 1) / G;
+    for (int j = tid; j < kMaxItems; j += W) s_rej[j] = 0;  // ordered before any read by the staging barrier
     if (tid == 0) {
         s_part[0] = 0.0;  // read and written by thread 0 only
         s_tail.part_ws = a.part_ws;
@@ -399,17 +408,9 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         s_tail.B = a.B;
         s_tail.K = a.K;
     }
-    Meta mine;
-    mine.kb = 0;
-    mine.y = 0;
-    mine.u = 0.0f;
-    mine.u_res = 0.0f;
-    mine.on = 0;
-    if (tid < nk) mine = load_meta(a, int(blockIdx.x) + tid * G);
-
     // The pipeline starts one step early: step -1 computes nothing; it issues
     // the loads of the first item from the same code as every later step and
-    // stages the item arguments.  The first item's rows are read before its
+    // then stages the item arguments.  The first item's rows are read before its
     // arguments are known (in bounds either way; a bonus row, whose index is
     // k_b, reads k_b directly).
     Item cur;
@@ -452,7 +453,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             nload = nxt.trow != nullptr;
             // A bonus row whose sequence already stopped here is not read
             // (the current item's outcome is not known yet).
-            if (nload && nxt.bonus && a.seq_step > 1 && known_rejection(s_rej, k + 1, a.seq_step)) {
+            if (nload && nxt.bonus && known_rejection_ahead(s_rej, k + 1, a.seq_step)) {
                 nload = false;
                 nxt_skip = 1;
             }
@@ -460,7 +461,27 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         const rsrc_t ntr = make_rsrc(nload ? nxt.trow : a.target, nload ? a.row_bytes : 0u);
         const rsrc_t nsr = make_rsrc(nload && nxt.drow ? nxt.drow : a.target, nload && nxt.drow ? a.row_bytes : 0u);
         if (k >= 0) cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
-        const bool vlive = cur.vkind == kItemLive && !cur_skip;
+        // A bonus row is needed only if every proposal of its sequence is
+        // accepted.  Besides this workgroup's own outcomes, the records that
+        // any workgroup has posted so far are consulted (each is written
+        // once per call; zero: not posted yet): one that is not an
+        // acceptance means the row is not needed.  Wave 0 reads them
+        // (k_b <= 16 lanes); the bonus rows come last, when most are posted.
+        bool bonus_stop = false;
+        if (cur.bonus && cur.vkind == kItemLive && !cur_skip && k >= 0) {
+            const int t = opaque_tid();  // nothing tid-derived is kept across the loop
+            if (t < kWave) {
+                uint32_t r = 0u;
+                if (t < cur.i)
+                    r = __hip_atomic_load(&a.records[int64_t(cur.b) * (a.K + 1) + t], __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t m = __ballot(r != 0u && (r >> 28) != kRecAccept);
+                if (t == 0) s_flag = m != 0 ? 1 : 0;
+            }
+            __syncthreads();
+            bonus_stop = s_flag != 0 || known_rejection(s_rej, k, a.seq_step);
+        }
+        const bool vlive = cur.vkind == kItemLive && !cur_skip && !bonus_stop;
         const bool live = vlive || cur.dist;
         const int ychunk = cur.y / EPC;
         const rsrc_t gr = make_rsrc(a.grad_out && cur.grow >= 0 && k >= 0
@@ -520,8 +541,9 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             rs[r] = load_chunk<W>(nsr, r);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (k < 0) {  // step -1: stage the item arguments
-            if (tid < nk) s_meta[tid] = mine;
+        if (k < 0) {  // step -1: stage the item arguments (read after the first rows were requested)
+            const int t = opaque_tid();
+            if (t < nk) s_meta[t] = load_meta(a, int(blockIdx.x) + t * G);
             __syncthreads();
         }
         // The record of an item that is not tested (a proposal outside the
