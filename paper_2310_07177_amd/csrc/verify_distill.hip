@@ -281,14 +281,16 @@ struct FusedTail {
 };
 
 // Every workgroup posts its loss partial and arrives; the last one
+//  - turns each sequence's records into the outputs (one segment of 16 or
+//    32 lanes per sequence, lane j = position j): the first position whose
+//    record is not an acceptance ends the test; a proposal outside the
+//    vocabulary invalidates the sequence wherever it sits, a row without
+//    finite logits only if the test reaches it;
 //  - adds the partials in workgroup order and counts the mask (fixed order,
 //    fp64), writing {mean, sum};
-//  - turns each sequence's records into the outputs (one wave per sequence,
-//    lane j = position j): the first position whose record is not an
-//    acceptance ends the test; a proposal outside the vocabulary invalidates
-//    the sequence wherever it sits, a row without finite logits only if the
-//    test reaches it;
 //  - reads every record and partial with an exchange that leaves zero.
+// All of a pass's reads are issued before any is used (one round trip per
+// pass; positions beyond k_b were never posted and read as zero).
 template <int W>
 __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     constexpr int NW = W / kWave;
@@ -307,6 +309,40 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     }
     __syncthreads();
     if (!s_last) return;
+    const int K = a.K;
+    const int seg = K + 1 <= 16 ? 16 : 32;  // K <= 16
+    const int per_pass = W / seg;
+    const int j = tid & (seg - 1), base = lane & ~(seg - 1);
+    const uint64_t segmask = (seg == 32 ? 0xFFFFFFFFull : 0xFFFFull) << base;
+    for (int b0 = 0; b0 < a.B; b0 += per_pass) {
+        const int b = b0 + tid / seg;
+        const bool on = b < a.B;
+        const int kb = on ? (a.draft_len ? a.draft_len[b] : K) : 0;
+        const uint32_t r = on && j <= K ? take_u32(&a.records[int64_t(b) * (K + 1) + j]) : 0u;
+        const int32_t tk = on && j < K ? a.tokens[int64_t(b) * K + j] : -1;
+        const bool kb_ok = kb >= 1 && kb <= K;
+        const uint32_t st = r >> 28;
+        const bool bad_token = (__ballot(j < kb && st == kRecBadToken) & segmask) != 0;
+        const uint64_t stop = (__ballot(j < kb && st != kRecAccept) & segmask) >> base;
+        const int acc = stop ? __builtin_ctzll(stop) : kb;
+        const uint32_t ra = __shfl(r, base + (kb_ok ? acc : 0), kWave);
+        const uint32_t sa = ra >> 28;
+        bool bad = !kb_ok || bad_token;
+        int extra = -1;
+        if (!bad) {
+            if (acc < kb ? sa == kRecReject : sa == kRecBonus)
+                extra = int(ra & 0x0FFFFFFFu);
+            else
+                bad = true;  // a row without finite logits where the test stopped
+        }
+        if (on && j <= K) {
+            const int32_t o = bad ? -1 : (j < acc ? tk : (j == acc ? extra : -1));
+            a.out_tokens[int64_t(b) * (K + 1) + j] = o;
+            if (a.reject_mask && j < K)
+                a.reject_mask[int64_t(b) * K + j] = (!bad && j == acc && acc < kb) ? 1 : 0;
+            if (j == 0) a.accepted_len[b] = bad ? -1 : acc;
+        }
+    }
     double sm = 0.0, cn = 0.0;
     for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
     for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
@@ -325,42 +361,8 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
         }
         a.loss_out[0] = tc > 0.0 ? float(ts / tc) : 0.0f;
         a.loss_out[1] = float(ts);
+        take_u32(a.done);
     }
-    const int K = a.K;
-    for (int b = wid; b < a.B; b += NW) {
-        const int kb = a.draft_len ? a.draft_len[b] : K;
-        int32_t* ot = a.out_tokens + int64_t(b) * (K + 1);
-        uint8_t* rm = a.reject_mask ? a.reject_mask + int64_t(b) * K : nullptr;
-        if (kb < 1 || kb > K) {
-            if (lane <= K) ot[lane] = -1;
-            if (rm && lane < K) rm[lane] = 0;
-            if (lane == 0) a.accepted_len[b] = -1;
-            continue;
-        }
-        const uint32_t r = lane <= kb ? take_u32(&a.records[int64_t(b) * (K + 1) + lane]) : 0u;
-        const uint32_t st = r >> 28;
-        const bool bad_token = __ballot(lane < kb && st == kRecBadToken) != 0;
-        const uint64_t stop = __ballot(lane < kb && st != kRecAccept);
-        const int acc = stop ? __builtin_ctzll(stop) : kb;
-        const uint32_t ra = __shfl(r, acc, kWave);
-        const uint32_t sa = ra >> 28;
-        bool bad = bad_token;
-        int extra = -1;
-        if (!bad) {
-            if (acc < kb ? sa == kRecReject : sa == kRecBonus)
-                extra = int(ra & 0x0FFFFFFFu);
-            else
-                bad = true;  // a row without finite logits where the test stopped
-        }
-        if (lane <= K) {
-            int32_t o = -1;
-            if (!bad) o = lane < acc ? a.tokens[int64_t(b) * K + lane] : (lane == acc ? extra : -1);
-            ot[lane] = o;
-            if (rm && lane < K) rm[lane] = (!bad && lane == acc && acc < kb) ? 1 : 0;
-        }
-        if (lane == 0) a.accepted_len[b] = bad ? -1 : acc;
-    }
-    if (tid == 0) take_u32(a.done);
 }
 
 template <typename Fmt, int W, int CPT, int KIND>
