@@ -1,10 +1,13 @@
 """Throughput of the OSD logits path on one MI355X.
 
-A step is one pass of the whole hot path over one batch: osd_verify
-(speculative-sampling verification at T = 0.7) followed by
-osd_distill_loss_grad (JSD, beta = 0.5, tau = 0.7, with the bf16 gradient)
-on the T5-vocabulary workload: B = 64 sequences, k = 8 proposals, V = 32128,
-bf16 logits, target ~ N(0, 2.5^2), draft = 0.7 target + N(0, 1.5^2).
+A step is one pass of the whole hot path over one batch: one
+osd_verify_distill call, which takes the speculative-sampling verification
+(T = 0.7) and the JSD distillation (beta = 0.5, tau = 0.7, loss and bf16
+gradient) of the step in one pass over the row pairs, on the T5-vocabulary
+workload: B = 64 sequences, k = 8 proposals, V = 32128, bf16 logits,
+target ~ N(0, 2.5^2), draft = 0.7 target + N(0, 1.5^2).  The same step
+through the two separate entry points (osd_verify, then
+osd_distill_loss_grad) is timed too and reported beside it.
 
 Inputs are synthetic and seeded; R copies of the batch rotate through the
 timed loop so that consecutive launches never find their inputs in the 256 MB
@@ -198,6 +201,9 @@ def main():
             raise RuntimeError(L.osd_status_string(st).decode())
 
     def step(r):
+        call(ff, fused_args[r % R])
+
+    def step_separate(r):
         call(fv, verify_args[r % R])
         call(fd, jsd_args[r % R])
 
@@ -265,9 +271,14 @@ def main():
     ms_step = time_graph(capture(step, args.steps), args.steps)
     print(f"# timed {args.steps} steps: {ms_step * 1e3:.2f} us/step", file=sys.stderr, flush=True)
 
+    ms_sep = time_loop(step_separate, args.steps)
+    print(f"# the same step as osd_verify + osd_distill_loss_grad: {ms_sep * 1e3:.2f} us/step",
+          file=sys.stderr, flush=True)
+
     kernels = {}
     masked = int(x["mask"].sum())
     for name, f, argl, nbytes in (
+            ("verify_distill", ff, fused_args, fused_bytes(B, K, V, masked)),
             ("verify", fv, verify_args, verify_bytes(B, K, V)),
             ("verify_greedy", fv, greedy_args, verify_bytes(B, K, V, greedy=True)),
             ("distill_jsd", fd, jsd_args, distill_bytes(B, K, V, masked)),
@@ -279,8 +290,8 @@ def main():
         print(f"# {name}: {ms * 1e3:.2f} us/launch, {gbs:.0f} GB/s ({100 * gbs / PEAK_HBM_GBS:.1f}% of peak)",
               file=sys.stderr, flush=True)
 
-    # The dominant kernel of a step: the one with the longer launch.
-    dom = max(("verify", "distill_jsd"), key=lambda k: kernels[k]["us_per_launch"])
+    # The step is one kernel.
+    dom = "verify_distill"
     kd = kernels[dom]
     traffic = traffic_from_profiles(dom, kd["algorithmic_bytes"])
     positions_per_s = B * K / (ms_step * 1e-3)
@@ -297,15 +308,15 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded; target ~ N(0,2.5^2), draft = 0.7 target + N(0,1.5^2))",
-        "config": {"workload": "T5-vocab verify + JSD distill step", "B": B, "k": K, "V": V,
+        "config": {"workload": "T5-vocab verify + JSD distill step (fused entry point)", "B": B, "k": K, "V": V,
                    "logits": "bf16", "T": T_VERIFY, "tau": TAU, "beta": BETA, "mask": "all ones",
                    "rotating_input_sets": R},
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": kd["achieved_GBps"],
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kd["frac_of_peak"],
                      "traffic": traffic},
         "kernels": kernels,
-        "step_GBps": round((kernels["verify"]["algorithmic_bytes"] + kernels["distill_jsd"]["algorithmic_bytes"])
-                           / (ms_step * 1e-3) / 1e9, 1),
+        "step_GBps": round(kernels["verify_distill"]["algorithmic_bytes"] / (ms_step * 1e-3) / 1e9, 1),
+        "separate_calls_ms_per_step": round(ms_sep, 6),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()

@@ -88,3 +88,64 @@ def test_graph_replays_match_eager():
                 step(b, T)
             torch.cuda.synchronize()
         assert int(vws.count_nonzero()) == 0 and int(dws.count_nonzero()) == 0
+
+
+def test_graph_replays_match_eager_fused():
+    """The same for the fused entry point (osd_verify_distill)."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    dev = torch.device("cuda:0")
+    L = binding.lib()
+    B, K, V = 16, 5, 8192
+    sets = []
+    for seed in (5, 6):
+        x = synth.verify_inputs(B, K, V, "bf16", T=0.8, seed=seed, target_std=2.5, draft_noise=1.0)
+        s = {k: _dev(x[k], dev) for k in ("target", "draft", "u_accept", "u_resample")}
+        s["tokens"] = _dev(x["tokens"].astype(np.int32), dev)
+        s["mask"] = _dev((np.random.default_rng(seed).random((B, K)) < 0.7).astype(np.uint8), dev)
+        s["acc"] = torch.empty(B, dtype=torch.int32, device=dev)
+        s["toks"] = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+        s["rmask"] = torch.empty(B, K, dtype=torch.uint8, device=dev)
+        s["loss"] = torch.empty(2, dtype=torch.float32, device=dev)
+        s["rows"] = torch.empty(B, K, dtype=torch.float32, device=dev)
+        s["grad"] = torch.empty(B, K, V, dtype=torch.bfloat16, device=dev)
+        sets.append(s)
+    stream = torch.cuda.Stream(dev)
+    stream.wait_stream(torch.cuda.current_stream(dev))
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    ws = torch.zeros(L.osd_verify_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def step(s):
+        st = L.osd_verify_distill(P(s["target"]), P(s["draft"]), binding.OSD_BF16, B, K, V, P(s["tokens"]), None,
+                                  P(s["u_accept"]), P(s["u_resample"]), ctypes.c_float(0.8), P(s["acc"]),
+                                  P(s["toks"]), P(s["rmask"]), P(s["mask"]), binding.OSD_JSD, ctypes.c_float(0.5),
+                                  P(s["loss"]), P(s["rows"]), P(s["grad"]), P(ws), ws.numel(), hs)
+        assert st == 0
+
+    def outputs(s):
+        return [s[k].clone() for k in ("acc", "toks", "rmask", "loss", "rows", "grad")]
+
+    a, b = sets
+    with torch.cuda.stream(stream):
+        step(a)
+    torch.cuda.synchronize()
+    eager = outputs(a)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        step(a)
+    for rep in range(3):
+        for k in ("acc", "toks", "rmask", "loss", "rows", "grad"):
+            a[k].zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            g.replay()
+        torch.cuda.synchronize()
+        for e, o in zip(eager, outputs(a)):
+            assert torch.equal(e, o), f"replay {rep}"
+        with torch.cuda.stream(stream):
+            step(b)
+        torch.cuda.synchronize()
+    assert int(ws.count_nonzero()) == 0
