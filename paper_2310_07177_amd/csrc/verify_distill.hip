@@ -168,16 +168,19 @@ __device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
 
 // s_rej[k] = 1 if item k of this workgroup or an earlier item of the same
 // sequence ended the test (or could not be tested).  The previous item of
-// the same sequence is k - seq_step.
+// the same sequence is k - seq_step.  Read after a barrier of item k (every
+// item has one), the entries up to k - 1 are visible.
 __device__ inline bool known_rejection(const uint8_t* s_rej, int k, int seq_step) {
     const int kk = k - seq_step;
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
 }
-// The same, asked while item k - 1 is still being computed (its entry is not
-// written yet): the latest finished item of item k's sequence is consulted.
+// The same, asked at the start of item k - 1 (to decide whether item k's
+// rows are read).  Items end without a workgroup barrier, so only entries up
+// to k - 3 are certainly visible to every wave then (entry j is written by
+// thread 0 at the end of item j, before it reaches a barrier of item j + 1).
 __device__ inline bool known_rejection_ahead(const uint8_t* s_rej, int k, int seq_step) {
     int kk = k - seq_step;
-    if (kk >= k - 1) kk -= seq_step;
+    while (kk > k - 3) kk -= seq_step;
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
 }
 
@@ -368,13 +371,16 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
 template <typename Fmt, int W, int CPT, int KIND>
 __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     constexpr int NW = W / kWave, EPC = Fmt::kPerChunk, NG = EPC / 4;
-    __shared__ float s_k[2 * NW];
-    __shared__ double s_s[2 * NW];
+    // Items end without a barrier, so a wave can be one item ahead of
+    // another: the scratch written once per item is double-buffered by item
+    // parity (every item has at least one barrier, so never two ahead).
+    __shared__ float s_k[2][2 * NW];
+    __shared__ double s_s[2][2 * NW];
     __shared__ double s_a[2 * NW];
     __shared__ Meta s_meta[kMaxItems];
     __shared__ uint8_t s_rej[kMaxItems];
-    __shared__ int s_flag;
-    __shared__ float s_y[2];
+    __shared__ int s_flag[2];
+    __shared__ float s_y[2][2];
     __shared__ unsigned long long s_cell[CPT * NW];
     __shared__ unsigned long long s_z;
     __shared__ int s_tok;
@@ -478,10 +484,10 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     r = __hip_atomic_load(&a.records[int64_t(cur.b) * (a.K + 1) + t], __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT);
                 const uint64_t m = __ballot(r != 0u && (r >> 28) != kRecAccept);
-                if (t == 0) s_flag = m != 0 ? 1 : 0;
+                if (t == 0) s_flag[k & 1] = m != 0 ? 1 : 0;
             }
             __syncthreads();
-            bonus_stop = s_flag != 0 || known_rejection(s_rej, k, a.seq_step);
+            bonus_stop = s_flag[k & 1] != 0 || known_rejection(s_rej, k, a.seq_step);
         }
         const bool vlive = cur.vkind == kItemLive && !cur_skip && !bonus_stop;
         const bool live = vlive || cur.dist;
@@ -505,8 +511,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     xs = pad_chunk<Fmt>();
                 }
                 if (vlive && !cur.bonus && r * W + tid == ychunk) {
-                    s_y[0] = Fmt::get(xt, cur.y - ychunk * EPC);
-                    s_y[1] = Fmt::get(xs, cur.y - ychunk * EPC);
+                    s_y[k & 1][0] = Fmt::get(xt, cur.y - ychunk * EPC);
+                    s_y[k & 1][1] = Fmt::get(xs, cur.y - ychunk * EPC);
                 }
                 if (r == 0) {
                     kc_t = first_chunk_shift<Fmt>(xt, c2);
@@ -565,6 +571,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
 #pragma unroll
                 for (int r = 0; r < CPT; ++r) store_chunk<W>(gr, r, chunk_t{0u, 0u, 0u, 0u});
             }
+            __syncthreads();  // every item has a barrier (the live ones: the merge)
         } else {
             // Exponent range exceeded by an element far above the first
             // chunk's maximum: rescale exactly from the cache.
@@ -585,7 +592,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             }
             float Kt = ks_t, Ks = ks_s;
             double St = S_t, Ss = S_s;
-            block_merge2<NW>(Kt, St, Ks, Ss, s_k, s_s);
+            block_merge2<NW>(Kt, St, Ks, Ss, s_k[k & 1], s_s[k & 1]);
             // log2 p_j = (t_j c2 - K_t) - (K_row_t - K_t + log2 S_t) = c - ct, likewise q.
             const double Tt = double(Kt) + log2(St), Ts = double(Ks) + log2(Ss);
             const float ct = float(Tt - double(kc_t)), cs = float(Ts - double(kc_s));
@@ -603,7 +610,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     // p(y)/q(y) = 2^e with e = (t_y c2 - T_t) - (d_y c2 - T_s)
                     // in fp64 (T: the rows' log2 normalisers); 2^e is split
                     // into an exact power of two and 2^frac (v_exp_f32).
-                    const double e = (double(s_y[0]) * a.c2d - Tt) - (double(s_y[1]) * a.c2d - Ts);
+                    const double e = (double(s_y[k & 1][0]) * a.c2d - Tt) - (double(s_y[k & 1][1]) * a.c2d - Ts);
                     double ratio;
                     if (!(e > -2000.0)) {
                         ratio = 0.0;  // p(y) = 0
@@ -772,7 +779,6 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                                       __HIP_MEMORY_SCOPE_AGENT);
             if (k < kMaxItems) s_rej[k] = (stopped || known_rejection(s_rej, k, a.seq_step)) ? 1 : 0;
         }
-        __syncthreads();  // s_y, s_rej and the draw cells are reused by the next item
         cur_skip = nxt_skip;
     }
     finish_fused<W>(s_tail, s_part);
