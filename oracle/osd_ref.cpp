@@ -388,6 +388,56 @@ extern "C" int osd_ref_distill_loss_grad(const void* teacher,
     return 0;
 }
 
+/*
+ * Token sampling: the draft's proposals y ~ q (Algorithm 1) and the mixed
+ * sampling y ~ beta p + (1 - beta) q of Section 4.1.  Per row n the
+ * distribution is pi = beta softmax(p_n / T) + (1 - beta) softmax(q_n / T)
+ * (a row whose weight is 0 is not read), and the token is drawn by the same
+ * inverse CDF as the verification's extra token: ascending token ids, the
+ * first running sum strictly above u * Z.  T == 0 takes the argmax of the
+ * one row with weight 1.
+ */
+extern "C" int osd_ref_sample(const void* p, int64_t p_stride, const void* q, int64_t q_stride,
+                              int dtype, int N, int V, float temperature, double beta,
+                              const float* u, int32_t* out, double* margin) {
+    if (N <= 0 || V <= 0 || !out) return -1;
+    if (!(temperature >= 0.0f) || !(beta >= 0.0 && beta <= 1.0)) return -1;
+    const bool use_p = beta > 0.0, use_q = beta < 1.0;
+    if ((use_p && (!p || p_stride < V)) || (use_q && (!q || q_stride < V))) return -1;
+    const bool greedy = temperature == 0.0f;
+    if (greedy && use_p && use_q) return -1;  /* argmax of a mixture: not defined here */
+    if (!greedy && !u) return -1;
+    const double T = (double)temperature;
+    for (int n = 0; n < N; ++n) {
+        out[n] = -1;
+        if (margin) margin[n] = kNaN;
+        if (greedy) {
+            const std::vector<double> z = use_p ? load_row(p, dtype, (int64_t)n * p_stride, V)
+                                                : load_row(q, dtype, (int64_t)n * q_stride, V);
+            out[n] = row_argmax(z);
+            continue;
+        }
+        std::vector<double> P, logP, Q, logQ;
+        if (use_p && !temperature_softmax(load_row(p, dtype, (int64_t)n * p_stride, V), T, P, logP))
+            continue;
+        if (use_q && !temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), T, Q, logQ))
+            continue;
+        std::vector<double> pi((size_t)V, 0.0);
+        double Z = 0.0;
+        for (int j = 0; j < V; ++j) {
+            double w = 0.0;
+            if (use_p) w += beta * P[(size_t)j];
+            if (use_q) w += (1.0 - beta) * Q[(size_t)j];
+            pi[(size_t)j] = w;
+            Z += w;
+        }
+        double m = 0.0;
+        out[n] = inverse_cdf(pi, Z, u[n], &m);
+        if (margin) margin[n] = m;
+    }
+    return 0;
+}
+
 namespace {
 
 /* Spacing of bf16 values around |x| (8 significant bits; the subnormal

@@ -82,6 +82,28 @@ int osd_ref_distill_loss_grad(const void* teacher, int64_t teacher_batch_stride,
                               double* loss_out, double* row_loss,
                               double* grad);
 
+/*
+ * Token sampling: the draft's proposals y ~ q (Algorithm 1) and mixed
+ * sampling y ~ beta p + (1 - beta) q (Section 4.1).
+ *
+ * p, q        [N, V] rows, row strides p_stride, q_stride (elements, >= V);
+ *             a row set whose weight is 0 (p when beta == 0, q when
+ *             beta == 1) is not read and may be NULL
+ * temperature T > 0: pi = beta softmax(p_n / T) + (1 - beta) softmax(q_n / T),
+ *             token = smallest j whose running sum (ascending j) exceeds
+ *             u[n] * Z, Z = sum pi; T == 0: argmax of the row with weight 1
+ *             (lowest index on ties), beta must then be 0 or 1
+ * u           [N] in [0, 1); unused (may be NULL) when T == 0
+ * out         [N] the token, -1 when a row with non-zero weight has no
+ *             finite logit
+ * margin      [N] nullable; distance in probability mass from u*Z to the
+ *             nearer edge of the chosen token's interval (NaN for greedy and
+ *             invalid rows)
+ */
+int osd_ref_sample(const void* p, int64_t p_stride, const void* q, int64_t q_stride,
+                   int dtype, int N, int V, float temperature, double beta,
+                   const float* u, int32_t* out, double* margin);
+
 /* Round fp64 values to bf16 bit patterns, round-to-nearest-even, directly
  * (no intermediate fp32 rounding). */
 void osd_ref_round_bf16(const double* x, uint16_t* out, int64_t n);

@@ -36,6 +36,8 @@ def lib():
         L.osd_ref_distill_loss_grad.restype = i32
         L.osd_ref_distill_loss_grad.argtypes = [vp, i64, vp, i64, i32, i32, i32,
                                                 i32, vp, i32, f64, f64, vp, vp, vp]
+        L.osd_ref_sample.restype = i32
+        L.osd_ref_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f64, vp, vp, vp]
         L.osd_ref_round_bf16.restype = None
         L.osd_ref_round_bf16.argtypes = [vp, vp, i64]
         L.osd_ref_round_f32.restype = None
@@ -128,6 +130,34 @@ def distill(teacher, student, kind, beta=0.5, tau=1.0, mask=None, grad=True,
     if rc != 0:
         raise ValueError(f"osd_ref_distill_loss_grad rejected its arguments (rc={rc})")
     return dict(loss_mean=loss[0], loss_sum=loss[1], row_loss=rows, grad=g)
+
+
+def sample(p, q, temperature, beta, u=None):
+    """Oracle token sampling.  p and q are [N, V] (either may be None when its
+    weight is 0: p needs beta > 0, q needs beta < 1); rows may be views with a
+    row stride (the leading axis stride is passed through).  Returns a dict:
+    tokens [N] int32 (-1 for an invalid row) and margin [N] (NaN for greedy
+    and invalid rows)."""
+    def rows(a):
+        if a is None:
+            return None, 0
+        a = np.asarray(a)
+        assert a.ndim == 2 and a.strides[1] == a.itemsize, "rows must be contiguous along V"
+        return a, (a.strides[0] // a.itemsize if a.shape[0] > 1 else a.shape[1])
+    p, ps = rows(p)
+    q, qs = rows(q)
+    ref = p if p is not None else q
+    N, V = ref.shape
+    uu = _c(u, np.float32)
+    out = np.empty(N, np.int32)
+    mg = np.empty(N, np.float64)
+    pp = None if p is None else ctypes.c_void_p(p.ctypes.data)
+    qp = None if q is None else ctypes.c_void_p(q.ctypes.data)
+    rc = lib().osd_ref_sample(pp, int(ps), qp, int(qs), _dtype_code(ref), N, V, float(temperature),
+                              float(beta), _ptr(uu), _ptr(out), _ptr(mg))
+    if rc != 0:
+        raise ValueError(f"osd_ref_sample rejected its arguments (rc={rc})")
+    return dict(tokens=out, margin=mg)
 
 
 def round_bf16(x):

@@ -39,6 +39,12 @@ MUTATIONS = {
     "argmax_last_on_ties": ("if (z[j] > bv) {", "if (z[j] >= bv) {"),
     "bf16_round_truncates": ("double r = std::nearbyint(v / q) * q;",
                              "double r = std::trunc(v / q) * q;"),
+    "sample_mixture_weights_swapped": ("if (use_p) w += beta * P[(size_t)j];",
+                                       "if (use_p) w += (1.0 - beta) * P[(size_t)j];"),
+    "sample_temperature_ignored": ("load_row(p, dtype, (int64_t)n * p_stride, V), T, P, logP)",
+                                   "load_row(p, dtype, (int64_t)n * p_stride, V), 1.0, P, logP)"),
+    "sample_row_stride_ignored": ("temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), T, Q, logQ)",
+                                  "temperature_softmax(load_row(q, dtype, (int64_t)n * V, V), T, Q, logQ)"),
 }
 
 
@@ -56,6 +62,7 @@ def test_pins_catch_planted_mistake(name, tmp_path):
     env = dict(os.environ, OSD_REF_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_verify_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_distill_pins.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_distill_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_sample_pins.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"
