@@ -181,6 +181,42 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
                        float* loss_out, float* row_loss_out, void* grad_out,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * osd_sample -- token sampling: the draft model's proposals y ~ q
+ * (Algorithm 1) and the mixed sampling y ~ beta p + (1 - beta) q that
+ * Section 4.1 uses to generate distillation data (beta weights the target
+ * p).  For each row n:
+ *   pi_n = beta softmax(p_n / T) + (1 - beta) softmax(q_n / T)
+ * and out_tokens[n] is the smallest token id j whose running sum of pi_n
+ * (ascending j) exceeds u[n] * sum(pi_n) -- the inverse CDF of osd_verify's
+ * extra token.  T == 0 takes the argmax (lowest index on ties) of the row
+ * with weight 1.
+ *
+ * p_logits      [N, V] dtype rows, row n at element offset n * p_row_stride;
+ *               not read (may be NULL) when beta == 0
+ * q_logits      [N, V] dtype rows, row stride q_row_stride elements; not read
+ *               (may be NULL) when beta == 1
+ * p_row_stride, q_row_stride  elements between rows, >= V (e.g. V for
+ *               [N, V], or (K+1)*V for one position of every sequence of a
+ *               [B, K+1, V] tensor)
+ * temperature   T > 0 samples; T == 0 needs beta == 0 or beta == 1
+ * beta          in [0, 1]
+ * u             [N] float uniforms in [0, 1) (unused, may be NULL, at T == 0)
+ * out_tokens    out [N] int32: the token, or -1 for a row with weight > 0
+ *               that has no finite logit
+ *
+ * Errors: OSD_ERR_INVALID_ARG for N <= 0, V <= 0, a bad dtype, T < 0, inf
+ * or NaN, beta outside [0, 1], T == 0 with 0 < beta < 1, a needed pointer
+ * NULL or a row stride < V; OSD_ERR_UNSUPPORTED for V > osd_max_vocab(dtype);
+ * OSD_ERR_DEVICE if the launch fails.  Nothing is enqueued on an error.
+ * No workspace; one workgroup per row.  Rows that are 16-byte aligned with
+ * 16-byte multiple strides and lengths take 16-byte loads.
+ */
+int osd_sample(const void* p_logits, int64_t p_row_stride,
+               const void* q_logits, int64_t q_row_stride,
+               int dtype, int N, int V, float temperature, float beta,
+               const float* u, int32_t* out_tokens, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -407,7 +407,7 @@ extern "C" int osd_ref_sample(const void* p, int64_t p_stride, const void* q, in
     const bool greedy = temperature == 0.0f;
     if (greedy && use_p && use_q) return -1;  /* argmax of a mixture: not defined here */
     if (!greedy && !u) return -1;
-    const double T = (double)temperature;
+    const double temp = (double)temperature;
     for (int n = 0; n < N; ++n) {
         out[n] = -1;
         if (margin) margin[n] = kNaN;
@@ -418,9 +418,9 @@ extern "C" int osd_ref_sample(const void* p, int64_t p_stride, const void* q, in
             continue;
         }
         std::vector<double> P, logP, Q, logQ;
-        if (use_p && !temperature_softmax(load_row(p, dtype, (int64_t)n * p_stride, V), T, P, logP))
+        if (use_p && !temperature_softmax(load_row(p, dtype, (int64_t)n * p_stride, V), temp, P, logP))
             continue;
-        if (use_q && !temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), T, Q, logQ))
+        if (use_q && !temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), temp, Q, logQ))
             continue;
         std::vector<double> pi((size_t)V, 0.0);
         double Z = 0.0;

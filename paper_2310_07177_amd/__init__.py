@@ -5,9 +5,12 @@ speculative decoding (Liu et al., arXiv:2310.07177).
     osd_distill_loss_grad  FKL / RKL / JSD[beta] distillation loss and gradient
                            with respect to the draft logits (Section 4.1, Eq. 2-4)
     osd_verify_distill     both of one step in one pass over the row pairs
+    osd_sample             proposal sampling y ~ q and mixed sampling
+                           y ~ beta p + (1 - beta) q (Algorithm 1; Section 4.1)
 
 The computation lives in libosd.so (C ABI: include/osd.h); this package is
 argument marshalling over it.  Build with ``python -m paper_2310_07177_amd.build``.
 """
 from .binding import (OSD_BF16, OSD_F32, OSD_FKL, OSD_JSD, OSD_MAX_K, OSD_RKL, OsdError,  # noqa: F401
-                      lib, osd_distill_loss_grad, osd_max_vocab, osd_verify, osd_verify_distill)
+                      lib, osd_distill_loss_grad, osd_max_vocab, osd_sample, osd_verify,
+                      osd_verify_distill)

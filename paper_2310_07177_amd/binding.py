@@ -22,7 +22,7 @@ KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
 EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify",
            "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
-           "osd_verify_distill")
+           "osd_verify_distill", "osd_sample")
 
 _lib = None
 _lock = threading.Lock()
@@ -64,6 +64,8 @@ def lib():
             L.osd_verify_distill.restype = i32
             L.osd_verify_distill.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp,
                                              vp, i32, f32, vp, vp, vp, vp, sz, vp]
+            L.osd_sample.restype = i32
+            L.osd_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f32, vp, vp, vp]
             _lib = L
     return _lib
 
@@ -234,3 +236,33 @@ def osd_verify_distill(target_logits, draft_logits, draft_tokens, u_accept, u_re
     if st != OSD_OK:
         raise OsdError("osd_verify_distill", st)
     return acc, toks, rmask, loss, rows, g
+
+
+def osd_sample(p_logits, q_logits, temperature, beta, u=None, out=None):
+    """Token sampling through the C ABI: pi = beta softmax(p/T) +
+    (1 - beta) softmax(q/T) per row, inverse CDF with u (argmax at T == 0).
+
+    p_logits, q_logits: [N, V] bf16 or fp32 GPU tensors whose rows are
+    contiguous (a row stride other than V is passed through, e.g. a slice
+    [:, i, :] of a [B, K+1, V] tensor); either may be None when its weight is
+    0.  u: [N] float32 (None at T == 0).  Returns out_tokens [N] int32."""
+    torch = _torch()
+    ref = p_logits if p_logits is not None else q_logits
+    if ref is None:
+        raise ValueError("p_logits or q_logits is needed")
+    _check_cuda(p_logits, q_logits, u)
+    for t in (p_logits, q_logits):
+        if t is not None and (t.dim() != 2 or t.stride(1) != 1 or t.dtype != ref.dtype or t.shape != ref.shape):
+            raise ValueError("logit rows must be [N, V] views of one dtype with contiguous rows")
+    if u is not None and (u.dtype != torch.float32 or not u.is_contiguous()):
+        raise TypeError("u must be a contiguous float32 tensor")
+    N, V = ref.shape
+    if out is None:
+        out = torch.empty(N, dtype=torch.int32, device=ref.device)
+    stride = lambda t: 0 if t is None else (t.stride(0) if N > 1 else V)
+    st = lib().osd_sample(_ptr(p_logits), stride(p_logits), _ptr(q_logits), stride(q_logits),
+                          _dtype_code(ref), N, V, float(temperature), float(beta), _ptr(u), _ptr(out),
+                          _stream_handle(ref.device))
+    if st != OSD_OK:
+        raise OsdError("osd_sample", st)
+    return out

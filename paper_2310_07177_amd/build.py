@@ -13,7 +13,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libosd.so")
-SOURCES = ["osd_api.hip", "verify.hip", "distill.hip", "verify_greedy.hip", "distill_stream.hip", "verify_distill.hip"]
+SOURCES = ["osd_api.hip", "verify.hip", "distill.hip", "verify_greedy.hip", "distill_stream.hip", "verify_distill.hip",
+           "sample.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -290,4 +290,37 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
     return osd::launch_verify_distill(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 
+int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits, int64_t q_row_stride,
+               int dtype, int N, int V, float temperature, float beta, const float* u,
+               int32_t* out_tokens, void* stream) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (N <= 0 || V <= 0) return OSD_ERR_INVALID_ARG;
+    if (V > osd_max_vocab(dtype)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    if (!(beta >= 0.0f && beta <= 1.0f)) return OSD_ERR_INVALID_ARG;
+    const bool greedy = temperature == 0.0f;
+    const bool use_p = beta > 0.0f, use_q = beta < 1.0f;
+    if (greedy && use_p && use_q) return OSD_ERR_INVALID_ARG;
+    if (!out_tokens || (!greedy && !u)) return OSD_ERR_INVALID_ARG;
+    if (use_p && (!p_logits || p_row_stride < V)) return OSD_ERR_INVALID_ARG;
+    if (use_q && (!q_logits || q_row_stride < V)) return OSD_ERR_INVALID_ARG;
+    const int64_t eb = elem_bytes(dtype);
+    osd::SampleLaunch L;
+    L.p = use_p ? p_logits : nullptr;
+    L.p_stride = use_p ? p_row_stride : 0;
+    L.q = use_q ? q_logits : nullptr;
+    L.q_stride = use_q ? q_row_stride : 0;
+    L.dtype = dtype;
+    L.N = N;
+    L.V = V;
+    L.temperature = temperature;
+    L.beta = beta;
+    L.u = u;
+    L.out = out_tokens;
+    L.vec = (int64_t(V) * eb) % 16 == 0 && (!use_p || (aligned16(p_logits) && (p_row_stride * eb) % 16 == 0)) &&
+            (!use_q || (aligned16(q_logits) && (q_row_stride * eb) % 16 == 0));
+    L.stream = static_cast<hipStream_t>(stream);
+    return osd::launch_sample(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
 }  // extern "C"

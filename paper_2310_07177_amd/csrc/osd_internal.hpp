@@ -119,6 +119,25 @@ struct FusedLaunch {
 };
 hipError_t launch_verify_distill(const FusedLaunch& L);
 
+// Token sampling: one workgroup per row, pi = beta softmax(p/T) +
+// (1 - beta) softmax(q/T) (a row with weight 0 is not read); T == 0 takes
+// the argmax of the row with weight 1.
+struct SampleLaunch {
+    const void* p;
+    int64_t p_stride;  // elements
+    const void* q;
+    int64_t q_stride;
+    int dtype;
+    int N, V;
+    float temperature;
+    float beta;
+    const float* u;
+    int32_t* out;
+    bool vec;  // every row 16-byte aligned and V a whole number of chunks
+    hipStream_t stream;
+};
+hipError_t launch_sample(const SampleLaunch& L);
+
 // Streaming (persistent-workgroup) distillation: rows whose byte length and
 // base are 16-byte multiples and whose V fits one of the streaming tiles.
 bool pick_stream_tile(int V, int per_chunk, RowTile* t);

@@ -1,0 +1,115 @@
+// row_draw.hpp -- inverse-CDF draw over a register-resident row (pair), the
+// sampling rule of the verification's extra token (Eq. 5 of
+// arXiv:2310.07177, Appendix A.1) and of token sampling.
+//
+// Element masses are fp32; each thread's chunk sums are converted exactly to
+// 2^-SH fixed point, so every partial sum of the CDF is an exact integer and
+// the cells partition [0, Z) without gaps or overlaps whatever the reduction
+// order.  The token is the first element (ascending id) whose running sum
+// exceeds u*Z.
+#pragma once
+
+#include "osd_device.hpp"
+
+namespace osd {
+
+struct DrawShared {
+    int cell_round, cell_wave;
+    unsigned long long target;  // offset of u*Z inside the winning cell
+};
+
+// Inverse-CDF draw over a register-resident row pair.  mass(t, d, e) returns
+// the non-negative fp32 mass of element e of the chunks t, d (0 for padding).
+// Returns the drawn token on exactly one thread and -1 on every other thread;
+// *z_zero is set (uniformly) when the total mass is zero.
+//
+// Token order is (round n, wave w, lane, element e).  Chunk masses are summed
+// left to right in fp32 and converted exactly to fixed point, so every partial
+// sum below is an exact integer and the CDF cells (n, w) partition [0, Z)
+// without gaps or overlaps whatever the reduction order.  The winning wave
+// stages its chunks through LDS (s_stage, 2*CPT*64 chunks) so that the
+// winning round is selected by address, never by register index.
+template <int SH, int W, int CPT, int EPC, typename MassFn>
+__device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CPT], MassFn mass,
+                                float u, unsigned long long* s_tot, DrawShared* s_draw,
+                                chunk_t* s_stage, bool* z_zero) {
+    constexpr int NW = W / kWave;
+    constexpr int CELLS = CPT * NW;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) s = s + mass(tv[n], dv[n], e);
+        const uint64_t t = wave_sum(mass_to_fixed<SH>(s));
+        if (lane == 0) s_tot[n * NW + wid] = t;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    if (wid == 0) {
+        uint64_t z = 0;
+        for (int c0 = lane; c0 < CELLS; c0 += kWave) z += s_tot[c0];
+        z = wave_sum(z);
+        if (lane == 0) s_draw->cell_round = -1;
+        if (z > 0) {
+            uint64_t c = static_cast<uint64_t>(double(u) * double(z));
+            if (c >= z) c = z - 1;
+            uint64_t carry = 0;
+            for (int base = 0; base < CELLS; base += kWave) {
+                const int idx = base + lane;
+                const uint64_t v = idx < CELLS ? uint64_t(s_tot[idx]) : 0;
+                const uint64_t incl = wave_inclusive_scan(v) + carry;
+                const uint64_t lo = incl - v;
+                if (v > 0 && lo <= c && c < incl) {
+                    s_draw->cell_round = idx / NW;
+                    s_draw->cell_wave = idx % NW;
+                    s_draw->target = c - lo;
+                }
+                carry = static_cast<uint64_t>(__shfl(static_cast<unsigned long long>(incl), kWave - 1, kWave));
+            }
+        }
+    }
+    __syncthreads();
+    const int nstar = s_draw->cell_round;
+    *z_zero = nstar < 0;
+    if (nstar < 0 || wid != s_draw->cell_wave) return -1;
+
+    // Winning wave: stage every round through LDS, pick round nstar by address.
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        s_stage[n * kWave + lane] = tv[n];
+        s_stage[(CPT + n) * kWave + lane] = dv[n];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const chunk_t tc = s_stage[nstar * kWave + lane];
+    const chunk_t dc = s_stage[(CPT + nstar) * kWave + lane];
+    float m[EPC];
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        m[e] = mass(tc, dc, e);
+        s = s + m[e];
+    }
+    const uint64_t v = mass_to_fixed<SH>(s);
+    const uint64_t incl = wave_inclusive_scan(v);
+    const uint64_t lo = incl - v;
+    const uint64_t target = s_draw->target;
+    if (!(v > 0 && lo <= target && target < incl)) return -1;
+    // Walk the chunk with the same left-to-right fp32 sum.
+    const uint64_t want = target - lo;
+    float run = 0.0f;
+    int pick = -1, last_pos = -1;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        run = run + m[e];
+        if (m[e] > 0.0f) last_pos = e;
+        if (pick < 0 && mass_to_fixed<SH>(run) > want) pick = e;
+    }
+    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+    return (nstar * W + tid) * EPC + pick;
+}
+
+}  // namespace osd

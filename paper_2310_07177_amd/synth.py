@@ -175,6 +175,18 @@ def config_distill_buffer(N=16384, V=32000, seed=0, mask_p=0.4, chunk=1024):
                 tau=1.0, B=N, K=1, V=V, dtype="bf16")
 
 
+def sample_inputs(N, V, dtype="bf16", seed=0, p_std=3.0, q_noise=1.0, zipf=False):
+    """Rows for token sampling: p ~ N(0, p_std^2) (plus a Zipf(1.1)-ranked
+    bias when zipf), q = p + N(0, q_noise^2), and one uniform per row."""
+    gl = rng(seed * 16 + SEED_LOGITS)
+    t = normals(gl, (N, V), p_std)
+    if zipf:
+        t = t + zipf_bias(V, seed)
+    d = t + normals(gl, (N, V), q_noise)
+    u = uniforms(rng(seed * 16 + SEED_UNIFORM), N)
+    return dict(p=store(t, dtype), q=store(d, dtype), u=u, N=N, V=V, dtype=dtype)
+
+
 def config_large_vocab(seed=0, B=256, K=8, V=128256):
     """B=256 sequences with ragged proposal lengths k_b ~ U{1..8}, V=128256
     bf16; target ~ N(0, 3^2), draft = target + N(0, 1); T=0.8; forward KL at

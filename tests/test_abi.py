@@ -136,3 +136,30 @@ def test_fused_workspace_covers_both_entry_points():
                                                              + L.osd_distill_workspace_bytes(B, K))
     assert L.osd_verify_distill_workspace_bytes(4, 17) == 0
     assert L.osd_verify_distill_workspace_bytes(0, 4) == 0
+
+
+def sample(**kw):
+    a = dict(p=FAKE, ps=64, q=FAKE, qs=64, dtype=1, N=4, V=64, T=0.8, beta=0.5, u=FAKE, out=FAKE,
+             stream=None)
+    a.update(kw)
+    return osd.lib().osd_sample(a["p"], a["ps"], a["q"], a["qs"], a["dtype"], a["N"], a["V"], a["T"],
+                                a["beta"], a["u"], a["out"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=0), -1), (dict(V=0), -1), (dict(dtype=2), -1), (dict(V=1 << 20, ps=1 << 20, qs=1 << 20), -2),
+    (dict(T=-1.0), -1), (dict(T=float("nan")), -1), (dict(T=float("inf")), -1),
+    (dict(beta=-0.1), -1), (dict(beta=1.5), -1), (dict(beta=float("nan")), -1),
+    (dict(T=0.0), -1),                       # argmax of a mixture
+    (dict(p=None), -1), (dict(q=None), -1), (dict(u=None), -1), (dict(out=None), -1),
+    (dict(ps=63), -1), (dict(qs=10), -1),
+    (dict(beta=1.0, p=None), -1), (dict(beta=0.0, q=None), -1),
+])
+def test_sample_rejects_bad_arguments(kw, status):
+    assert sample(**kw) == status
+
+
+def test_binding_sample_fails_loudly_without_gpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        osd.osd_sample(torch.zeros(2, 8), None, 1.0, 1.0, torch.zeros(2))

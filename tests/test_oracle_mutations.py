@@ -41,10 +41,9 @@ MUTATIONS = {
                              "double r = std::trunc(v / q) * q;"),
     "sample_mixture_weights_swapped": ("if (use_p) w += beta * P[(size_t)j];",
                                        "if (use_p) w += (1.0 - beta) * P[(size_t)j];"),
-    "sample_temperature_ignored": ("load_row(p, dtype, (int64_t)n * p_stride, V), T, P, logP)",
-                                   "load_row(p, dtype, (int64_t)n * p_stride, V), 1.0, P, logP)"),
-    "sample_row_stride_ignored": ("temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), T, Q, logQ)",
-                                  "temperature_softmax(load_row(q, dtype, (int64_t)n * V, V), T, Q, logQ)"),
+    "sample_temperature_ignored": ("const double temp = (double)temperature;", "const double temp = 1.0;"),
+    "sample_row_stride_ignored": ("temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), temp, Q, logQ)",
+                                  "temperature_softmax(load_row(q, dtype, (int64_t)n * V, V), temp, Q, logQ)"),
 }
 
 
