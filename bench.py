@@ -48,7 +48,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--only", default=None,
                    help="profiling aid: run only the named loops, comma-separated "
-                        "(verify,greedy,jsd,rkl,fused,copy)")
+                        "(verify,greedy,jsd,rkl,fused,sample_prop,sample_mix,copy)")
     return p.parse_args()
 
 
@@ -74,6 +74,19 @@ def fused_bytes(B, K, V, masked_rows, elem=2):
     inputs and outputs, the whole gradient written once, the mask read, the
     per-row and total losses written."""
     return verify_bytes(B, K, V, elem) + B * K * V * elem + B * K + 4 * B * K + 8
+
+
+def sample_bytes(N, V, rows, elem=2):
+    """Algorithmic bytes of one osd_sample call: each of the `rows` logit rows
+    per sample read once, one uniform read and one token written."""
+    return N * rows * V * elem + 8 * N
+
+
+# Mixed sampling over a distillation buffer (Section 4.1): N rows of the
+# Llama vocabulary, teacher ~ N(0, 3^2) plus a Zipf(1.1)-ranked bias, student
+# = teacher + N(0, 1), beta = 0.5, T = 1.  0.5 GB per call, beyond the
+# Infinity Cache, so one input set suffices.
+MIX_N, MIX_V, MIX_BETA, MIX_T = 4096, 32000, 0.5, 1.0
 
 
 def kernel_source_hash():
@@ -195,6 +208,26 @@ def main():
                    P(s["rows"]), P(s["grad"]), P(fws), fws.numel(), hs) for s in sets]
     fv, fd, ff = L.osd_verify, L.osd_distill_loss_grad, L.osd_verify_distill
 
+    # Token sampling: the draft proposals of one step (draft row 0 of every
+    # sequence of the rotating sets, row stride K*V) and mixed sampling over a
+    # distillation buffer generated on the device.
+    fs = L.osd_sample
+    prop_u = [t_(synth.uniforms(synth.rng(100 + r), B)) for r in range(R)]
+    prop_out = torch.empty(B, dtype=torch.int32, device=dev)
+    prop_args = [(None, 0, P(s["draft"]), K * V, binding.OSD_BF16, B, V, ctypes.c_float(T_VERIFY),
+                  ctypes.c_float(0.0), P(prop_u[r]), P(prop_out), hs) for r, s in enumerate(sets)]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(16 + synth.SEED_LOGITS)
+    zipf = torch.from_numpy(synth.zipf_bias(MIX_V, 0)).to(dev)
+    mix_p = torch.randn(MIX_N, MIX_V, generator=gen, device=dev) * 3.0 + zipf
+    mix_q = (mix_p + torch.randn(MIX_N, MIX_V, generator=gen, device=dev)).to(torch.bfloat16)
+    mix_p = mix_p.to(torch.bfloat16)
+    mix_u = t_(synth.uniforms(synth.rng(101), MIX_N))
+    mix_out = torch.empty(MIX_N, dtype=torch.int32, device=dev)
+    mix_args = (P(mix_p), MIX_V, P(mix_q), MIX_V, binding.OSD_BF16, MIX_N, MIX_V, ctypes.c_float(MIX_T),
+                ctypes.c_float(MIX_BETA), P(mix_u), P(mix_out), hs)
+    torch.cuda.synchronize()
+
     def call(f, a):
         st = f(*a)
         if st != 0:
@@ -242,7 +275,9 @@ def main():
                  "fused": lambda r: call(ff, fused_args[r % R]),
                  "greedy": lambda r: call(fv, greedy_args[r % R]),
                  "jsd": lambda r: call(fd, jsd_args[r % R]),
-                 "rkl": lambda r: call(fd, rkl_args[r % R])}
+                 "rkl": lambda r: call(fd, rkl_args[r % R]),
+                 "sample_prop": lambda r: call(fs, prop_args[r % R]),
+                 "sample_mix": lambda r: call(fs, mix_args)}
         for name in args.only.split(","):
             if name == "copy":
                 src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -282,8 +317,11 @@ def main():
             ("verify", fv, verify_args, verify_bytes(B, K, V)),
             ("verify_greedy", fv, greedy_args, verify_bytes(B, K, V, greedy=True)),
             ("distill_jsd", fd, jsd_args, distill_bytes(B, K, V, masked)),
-            ("distill_rkl", fd, rkl_args, distill_bytes(B, K, V, masked))):
-        ms = time_loop(lambda r, f=f, argl=argl: call(f, argl[r % R]), args.kernel_iters)
+            ("distill_rkl", fd, rkl_args, distill_bytes(B, K, V, masked)),
+            ("sample_proposals", fs, prop_args, sample_bytes(B, V, 1)),
+            ("sample_mixed", fs, [mix_args], sample_bytes(MIX_N, MIX_V, 2))):
+        iters = args.kernel_iters if name != "sample_mixed" else max(10, args.kernel_iters // 20)
+        ms = time_loop(lambda r, f=f, argl=argl: call(f, argl[r % len(argl)]), iters)
         gbs = nbytes / (ms * 1e-3) / 1e9
         kernels[name] = {"us_per_launch": round(ms * 1e3, 3), "algorithmic_bytes": nbytes,
                          "achieved_GBps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}

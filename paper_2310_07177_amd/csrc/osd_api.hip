@@ -320,6 +320,7 @@ int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits,
     L.vec = (int64_t(V) * eb) % 16 == 0 && (!use_p || (aligned16(p_logits) && (p_row_stride * eb) % 16 == 0)) &&
             (!use_q || (aligned16(q_logits) && (q_row_stride * eb) % 16 == 0));
     L.stream = static_cast<hipStream_t>(stream);
+    L.cus = device_cus(L.stream);
     return osd::launch_sample(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 

@@ -134,6 +134,7 @@ struct SampleLaunch {
     const float* u;
     int32_t* out;
     bool vec;  // every row 16-byte aligned and V a whole number of chunks
+    int cus;
     hipStream_t stream;
 };
 hipError_t launch_sample(const SampleLaunch& L);

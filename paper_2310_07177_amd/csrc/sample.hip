@@ -171,7 +171,15 @@ template <typename Fmt>
 hipError_t launch_fmt(const SampleLaunch& L, const SampleArgs& a) {
     RowTile t;
     if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    // Fewer rows than two per CU: the rows' latency is the cost, so each row
+    // gets the widest workgroup (half the elements per thread).
+    if (L.N < 2 * L.cus && t.W < 1024) {
+        const int per = 1024 * Fmt::kPerChunk;
+        t = RowTile{1024, L.V <= 2 * per ? 2 : (L.V <= 4 * per ? 4 : 8)};
+    }
     switch (t.W * 100 + t.CPT) {
+        case 102402: return launch_tile<Fmt, 1024, 2>(L, a);
+        case 102404: return launch_tile<Fmt, 1024, 4>(L, a);
         case 25601: return launch_tile<Fmt, 256, 1>(L, a);
         case 25602: return launch_tile<Fmt, 256, 2>(L, a);
         case 25604: return launch_tile<Fmt, 256, 4>(L, a);
