@@ -320,7 +320,7 @@ def main():
             ("distill_rkl", fd, rkl_args, distill_bytes(B, K, V, masked)),
             ("sample_proposals", fs, prop_args, sample_bytes(B, V, 1)),
             ("sample_mixed", fs, [mix_args], sample_bytes(MIX_N, MIX_V, 2))):
-        iters = args.kernel_iters if name != "sample_mixed" else max(10, args.kernel_iters // 20)
+        iters = args.kernel_iters if name != "sample_mixed" else max(10, args.kernel_iters // 4)
         ms = time_loop(lambda r, f=f, argl=argl: call(f, argl[r % len(argl)]), iters)
         gbs = nbytes / (ms * 1e-3) / 1e9
         kernels[name] = {"us_per_launch": round(ms * 1e3, 3), "algorithmic_bytes": nbytes,
