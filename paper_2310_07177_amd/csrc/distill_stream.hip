@@ -164,8 +164,9 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                         const float t = Fmt::get(xt, e), s = Fmt::get(xs, e);
                         const float vt = __builtin_fmaf(t, c2, -kc_t);
                         const float vs = __builtin_fmaf(s, c2, -kc_s);
-                        st = st + exp2_fast(vt);
-                        ss = ss + exp2_fast(vs);
+                        // (the first term starts the sums: 0 + x would cost an add)
+                        st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
+                        ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
                         if constexpr (KIND == 2) {
                             c0v[j] = fmaxf(vt, kLogFloor);
                             c1[r][e] = fmaxf(vs, kLogFloor);
@@ -179,8 +180,8 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                 // Keep each round's sums in the round (without this the
                 // compiler may defer one row's exponentials past the loop).
                 asm volatile("" : "+v"(st), "+v"(ss));
-                S_t += double(st);
-                S_s += double(ss);
+                S_t = r == 0 ? double(st) : S_t + double(st);
+                S_s = r == 0 ? double(ss) : S_s + double(ss);
             }
             rt[r] = load_chunk<W>(ntr, r);
             rs[r] = load_chunk<W>(nsr, r);
@@ -218,9 +219,11 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             double St = S_t, Ss = S_s;
             block_merge2<NW>(Kt, St, Ks, Ss, s_k, s_s);
             // log2 p_j = (t_j c2 - K_t) - (K_row_t - K_t + log2 S_t) = c - ct, likewise q.
-            const double Tt = double(Kt) + log2(St), Ts = double(Ks) + log2(Ss);
-            const float ct = float(Tt - double(kc_t)), cs = float(Ts - double(kc_s));
-            const float dT = float(Tt - Ts);  // log2 p - log2 q = (t - s) c2 - dT
+            // T = K + log2 S, the rows' log2 normalisers; only their
+            // difference is needed in fp64 (from the ratio of the sums).
+            const double dTd = double(Kt - Ks) + (St == Ss ? 0.0 : log2_pos(St / Ss));
+            const float ct = float(double(Kt - kc_t) + log2_pos(St)), cs = float(double(Ks - kc_s) + log2_pos(Ss));
+            const float dT = float(dTd);  // log2 p - log2 q = (t - s) c2 - dT
 
             // ---- loss pass (from the cache) ----
             float acc0 = 0.0f, acc1 = 0.0f;

@@ -164,11 +164,53 @@ __device__ inline T wave_scan_add(T v) {
 __device__ inline float wave_max_u(float v) { return readlane_f32(wave_scan_max(v), kWave - 1); }
 __device__ inline double wave_sum_u(double v) { return readlane_f64(wave_scan_add(v), kWave - 1); }
 
+// log2 of a positive finite double to within about 6e-8 (absolute): the
+// binary exponent, v_log_f32 of the fp32 rounding of the mantissa taken in
+// [sqrt(1/2), sqrt(2)) (so a ratio near 1 keeps its relative accuracy; the
+// instruction is within one unit in the last place of its result there),
+// and the first-order term of that rounding.  A fraction of the fp64
+// library routine's cost.
+__device__ inline double log2_pos(double x) {
+    int ex;
+    double m = __builtin_frexp(x, &ex);  // [0.5, 1)
+    if (m < 0.70710678118654752) {
+        m *= 2.0;
+        ex -= 1;
+    }
+    const float mf = float(m);
+    const float corr = float(m - double(mf)) * (1.44269504f * __builtin_amdgcn_rcpf(mf));
+    return double(ex) + double(__builtin_amdgcn_logf(mf)) + double(corr);
+}
+
+// Totals of lanes 0..15 when every other lane holds the identity: the row
+// steps of the scans alone.  Equal, bit for bit, to the wave totals above
+// (the remaining steps only combine identities).
+__device__ inline float row0_max_u(float v) {
+    v = dpp_max_step<kDppRowShr1, 0xF>(v);
+    v = dpp_max_step<kDppRowShr2, 0xF>(v);
+    v = dpp_max_step<kDppRowShr4, 0xF>(v);
+    v = dpp_max_step<kDppRowShr8, 0xF>(v);
+    return readlane_f32(v, 15);
+}
+__device__ inline double row0_sum_u(double v) {
+    v = dpp_add_step<kDppRowShr1, 0xF>(v);
+    v = dpp_add_step<kDppRowShr2, 0xF>(v);
+    v = dpp_add_step<kDppRowShr4, 0xF>(v);
+    v = dpp_add_step<kDppRowShr8, 0xF>(v);
+    return readlane_f64(v, 15);
+}
+
 // Merge (K, S) pairs over the wave: K = max K, S = sum S 2^(K_lane - K).
 // Every lane gets the wave's pair.
 __device__ inline void wave_merge_stats_u(float& K, double& S) {
     const float kw = wave_max_u(K);
     S = wave_sum_u(rescale(S, K, kw));
+    K = kw;
+}
+// The same for pairs held by lanes 0..15 (identity elsewhere).
+__device__ inline void row0_merge_stats_u(float& K, double& S) {
+    const float kw = row0_max_u(K);
+    S = row0_sum_u(rescale(S, K, kw));
     K = kw;
 }
 
@@ -179,6 +221,7 @@ __device__ inline void wave_merge_stats_u(float& K, double& S) {
 // before the caller's next barrier.
 template <int NW>
 __device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1, float* s_k, double* s_s) {
+    static_assert(NW <= 16, "the posted pairs fit one DPP row");
     const int t = opaque_tid(), lane = t & (kWave - 1), wid = t / kWave;
     wave_merge_stats_u(K0, S0);
     wave_merge_stats_u(K1, S1);
@@ -197,8 +240,8 @@ __device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1
         t0 = s_s[lane];
         t1 = s_s[NW + lane];
     }
-    wave_merge_stats_u(k0, t0);
-    wave_merge_stats_u(k1, t1);
+    row0_merge_stats_u(k0, t0);
+    row0_merge_stats_u(k1, t1);
     K0 = k0;
     S0 = t0;
     K1 = k1;
@@ -208,6 +251,7 @@ __device__ inline void block_merge2(float& K0, double& S0, float& K1, double& S1
 // Workgroup sums of two doubles, the same way (one barrier).
 template <int NW>
 __device__ inline void block_sum2(double& A0, double& A1, double* s_a) {
+    static_assert(NW <= 16, "the posted sums fit one DPP row");
     const int t = opaque_tid(), lane = t & (kWave - 1), wid = t / kWave;
     A0 = wave_sum_u(A0);
     A1 = wave_sum_u(A1);
@@ -218,8 +262,8 @@ __device__ inline void block_sum2(double& A0, double& A1, double* s_a) {
     __syncthreads();
     double t0 = lane < NW ? s_a[lane] : 0.0;
     double t1 = lane < NW ? s_a[NW + lane] : 0.0;
-    A0 = wave_sum_u(t0);
-    A1 = wave_sum_u(t1);
+    A0 = row0_sum_u(t0);
+    A1 = row0_sum_u(t1);
 }
 
 // Argmax step: the larger value, the lower index among equal values.

@@ -528,8 +528,9 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         const float t = Fmt::get(xt, e), s = Fmt::get(xs, e);
                         const float vt = __builtin_fmaf(t, c2, -kc_t);
                         const float vs = __builtin_fmaf(s, c2, -kc_s);
-                        st = st + exp2_fast(vt);
-                        ss = ss + exp2_fast(vs);
+                        // (the first term starts the sums: 0 + x would cost an add)
+                        st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
+                        ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
                         if constexpr (KIND == 2) {
                             c0v[j] = fmaxf(vt, kLogFloor);
                             c1[r][e] = fmaxf(vs, kLogFloor);
@@ -542,8 +543,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 }
                 // Keep each round's sums in the round.
                 asm volatile("" : "+v"(st), "+v"(ss));
-                S_t += double(st);
-                S_s += double(ss);
+                S_t = r == 0 ? double(st) : S_t + double(st);
+                S_s = r == 0 ? double(ss) : S_s + double(ss);
             }
             rt[r] = load_chunk<W>(ntr, r);
             rs[r] = load_chunk<W>(nsr, r);
@@ -594,9 +595,11 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             double St = S_t, Ss = S_s;
             block_merge2<NW>(Kt, St, Ks, Ss, s_k[k & 1], s_s[k & 1]);
             // log2 p_j = (t_j c2 - K_t) - (K_row_t - K_t + log2 S_t) = c - ct, likewise q.
-            const double Tt = double(Kt) + log2(St), Ts = double(Ks) + log2(Ss);
-            const float ct = float(Tt - double(kc_t)), cs = float(Ts - double(kc_s));
-            const float dT = float(Tt - Ts);  // log2 p - log2 q = (t - s) c2 - dT
+            // T = K + log2 S, the rows' log2 normalisers; only their
+            // difference is needed in fp64 (from the ratio of the sums).
+            const double dTd = double(Kt - Ks) + (St == Ss ? 0.0 : log2_pos(St / Ss));
+            const float ct = float(double(Kt - kc_t) + log2_pos(St)), cs = float(double(Ks - kc_s) + log2_pos(Ss));
+            const float dT = float(dTd);  // log2 p - log2 q = (t - s) c2 - dT
 
             // ---- verification ----
             if (vlive) {
@@ -607,10 +610,10 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     record = make_rec(kRecBadRow, 0);
                     stopped = true;
                 } else if (!cur.bonus) {
-                    // p(y)/q(y) = 2^e with e = (t_y c2 - T_t) - (d_y c2 - T_s)
-                    // in fp64 (T: the rows' log2 normalisers); 2^e is split
-                    // into an exact power of two and 2^frac (v_exp_f32).
-                    const double e = (double(s_y[k & 1][0]) * a.c2d - Tt) - (double(s_y[k & 1][1]) * a.c2d - Ts);
+                    // p(y)/q(y) = 2^e with e = (t_y - d_y) c2 - (T_t - T_s)
+                    // in fp64; 2^e is split into an exact power of two and
+                    // 2^frac (v_exp_f32).
+                    const double e = (double(s_y[k & 1][0]) - double(s_y[k & 1][1])) * a.c2d - dTd;
                     double ratio;
                     if (!(e > -2000.0)) {
                         ratio = 0.0;  // p(y) = 0
