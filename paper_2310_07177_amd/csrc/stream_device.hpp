@@ -127,15 +127,27 @@ __device__ inline float dpp_max_step(float v) {
     const uint32_t ninf = 0xFF800000u;
     return fmaxf(v, __uint_as_float(dpp<CTRL, ROWS>(ninf, __float_as_uint(v))));
 }
+// A 32-bit lane permutation for a sum (identity 0).  Every row enabled
+// (the row shifts): lanes whose source is outside the row read 0 through
+// the bound control, and no register has to be preset to the identity.
+template <int CTRL, int ROWS>
+__device__ inline uint32_t dpp_sum_src(uint32_t v) {
+    if constexpr (ROWS == 0xF)
+        return uint32_t(__builtin_amdgcn_mov_dpp(int(v), CTRL, 0xF, 0xF, true));
+    else
+        return dpp<CTRL, ROWS>(0u, v);
+}
 template <int CTRL, int ROWS>
 __device__ inline double dpp_add_step(double v) {
     const uint64_t b = __builtin_bit_cast(uint64_t, v);
-    const uint64_t o = uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(b))) | (uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(b >> 32))) << 32);
+    const uint64_t o = uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(b))) |
+                       (uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(b >> 32))) << 32);
     return v + __builtin_bit_cast(double, o);
 }
 template <int CTRL, int ROWS>
 __device__ inline uint64_t dpp_add_step(uint64_t v) {
-    const uint64_t o = uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(v))) | (uint64_t(dpp<CTRL, ROWS>(0u, uint32_t(v >> 32))) << 32);
+    const uint64_t o = uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(v))) |
+                       (uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(v >> 32))) << 32);
     return v + o;
 }
 
