@@ -122,10 +122,20 @@ __device__ inline double readlane_f64(double v, int lane) {
     return __builtin_bit_cast(double, readlane_u64(__builtin_bit_cast(uint64_t, v), lane));
 }
 
+// Floats as unsigned keys in the same order (no NaN): a float maximum over
+// lanes becomes an unsigned one, which the DPP move folds into (identity 0)
+// and which needs no NaN quieting of each operand.
+__device__ inline uint32_t float_key(float f) {
+    const uint32_t b = __float_as_uint(f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ inline float key_float(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
 template <int CTRL, int ROWS>
-__device__ inline float dpp_max_step(float v) {
-    const uint32_t ninf = 0xFF800000u;
-    return fmaxf(v, __uint_as_float(dpp<CTRL, ROWS>(ninf, __float_as_uint(v))));
+__device__ inline uint32_t dpp_umax_step(uint32_t k) {
+    const uint32_t o = dpp<CTRL, ROWS>(0u, k);
+    return k > o ? k : o;
 }
 // A 32-bit lane permutation for a sum (identity 0).  Every row enabled
 // (the row shifts): lanes whose source is outside the row read 0 through
@@ -152,15 +162,6 @@ __device__ inline uint64_t dpp_add_step(uint64_t v) {
 }
 
 // Inclusive scans over the wave (lane 63 holds the total).
-__device__ inline float wave_scan_max(float v) {
-    v = dpp_max_step<kDppRowShr1, 0xF>(v);
-    v = dpp_max_step<kDppRowShr2, 0xF>(v);
-    v = dpp_max_step<kDppRowShr4, 0xF>(v);
-    v = dpp_max_step<kDppRowShr8, 0xF>(v);
-    v = dpp_max_step<kDppRowBcast15, 0xA>(v);
-    v = dpp_max_step<kDppRowBcast31, 0xC>(v);
-    return v;
-}
 template <typename T>
 __device__ inline T wave_scan_add(T v) {
     v = dpp_add_step<kDppRowShr1, 0xF>(v);
@@ -172,8 +173,17 @@ __device__ inline T wave_scan_add(T v) {
     return v;
 }
 
-// Wave totals, uniform.
-__device__ inline float wave_max_u(float v) { return readlane_f32(wave_scan_max(v), kWave - 1); }
+// Wave totals, uniform.  (The maximum of values without NaN.)
+__device__ inline float wave_max_u(float v) {
+    uint32_t k = float_key(v);
+    k = dpp_umax_step<kDppRowShr1, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr2, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr4, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr8, 0xF>(k);
+    k = dpp_umax_step<kDppRowBcast15, 0xA>(k);
+    k = dpp_umax_step<kDppRowBcast31, 0xC>(k);
+    return key_float(readlane_u32(k, kWave - 1));
+}
 __device__ inline double wave_sum_u(double v) { return readlane_f64(wave_scan_add(v), kWave - 1); }
 
 // log2 of a positive finite double to within about 6e-8 (absolute): the
@@ -198,11 +208,12 @@ __device__ inline double log2_pos(double x) {
 // steps of the scans alone.  Equal, bit for bit, to the wave totals above
 // (the remaining steps only combine identities).
 __device__ inline float row0_max_u(float v) {
-    v = dpp_max_step<kDppRowShr1, 0xF>(v);
-    v = dpp_max_step<kDppRowShr2, 0xF>(v);
-    v = dpp_max_step<kDppRowShr4, 0xF>(v);
-    v = dpp_max_step<kDppRowShr8, 0xF>(v);
-    return readlane_f32(v, 15);
+    uint32_t k = float_key(v);
+    k = dpp_umax_step<kDppRowShr1, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr2, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr4, 0xF>(k);
+    k = dpp_umax_step<kDppRowShr8, 0xF>(k);
+    return key_float(readlane_u32(k, 15));
 }
 __device__ inline double row0_sum_u(double v) {
     v = dpp_add_step<kDppRowShr1, 0xF>(v);
