@@ -165,9 +165,6 @@ __device__ void reduce_loss(const DistillArgs& a, int n, double D) {
 // Largest finite fp32 magnitude used to stand in for log2(0) = -inf, so that
 // p * log2(p) stays 0 * finite = 0 for logits of -inf.
 constexpr float kLogFloor = -1.0e30f;
-// Smallest mixture probability fed to log2 (a normal fp32 number, so that
-// v_log_f32 stays finite when both p and q underflow).
-constexpr float kMixFloor = 1.0e-37f;
 
 template <typename Fmt, int W, int CPT, bool VEC, int KIND>
 __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(DistillArgs a) {
@@ -278,9 +275,12 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
                     const float lp = fmaxf(__builtin_fmaf(t, c2, -kt_c), kLogFloor);
                     const float lq = fmaxf(__builtin_fmaf(sx, c2, -ks_c), kLogFloor);
                     const float p = exp2_fast(lp), q = exp2_fast(lq);
-                    const float lm = log2_fast(fmaxf(__builtin_fmaf(beta, p, omb * q), kMixFloor));
-                    c0 = __builtin_fmaf(p, lp - lm, c0);
-                    c1 = __builtin_fmaf(q, lq - lm, c1);
+                    // log2 m = lp + L, the mixture's log relative to p (near 0
+                    // when p ~ q): its rounding does not bias a small JSD.
+                    const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                    const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                    c0 = __builtin_fmaf(p, -L, c0);
+                    c1 = __builtin_fmaf(q, d - L, c1);
                 }
                 if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);  // 4 elements in flight
             }
@@ -333,8 +333,9 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
                         if constexpr (KIND == 1) {
                             lr = lq - lp;
                         } else {
-                            const float p = exp2_fast(lp);
-                            lr = lq - log2_fast(fmaxf(__builtin_fmaf(beta, p, omb * q), kMixFloor));
+                            // log2(q/m), as in the loss pass
+                            const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                            lr = d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
                         }
                         g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
                     }

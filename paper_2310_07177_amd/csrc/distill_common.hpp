@@ -12,10 +12,6 @@ namespace osd {
 // Largest finite fp32 magnitude used to stand in for log2(0) = -inf, so that
 // p * log2(p) stays 0 * finite = 0 for logits of -inf.
 constexpr float kLogFloor = -1.0e30f;
-// Added to the mixture before log2 (a normal fp32 number, so that v_log_f32
-// stays finite when both p and q underflow; below the rounding unit of any
-// mixture that matters).
-constexpr float kMixFloor = 1.0e-37f;
 
 template <typename Fmt>
 __device__ inline chunk_t pack_grad(const float (&g)[Fmt::kPerChunk]) {

@@ -171,7 +171,7 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                             c0v[j] = fmaxf(vt, kLogFloor);
                             c1[r][e] = fmaxf(vs, kLogFloor);
                         } else {
-                            c0v[j] = t - s;
+                            c0v[j] = vt - vs;  // log2 of the unnormalised ratio
                             c1[r][e] = KIND == 0 ? vt : vs;
                         }
                     }
@@ -199,20 +199,20 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
         } else {
             // Exponent range exceeded by an element far above the first
             // chunk's maximum: rescale exactly from the cache.  (FKL and RKL
-            // cache one row's exponent; the other is rebuilt from t - s.)
+            // cache one row's exponent; the other is rebuilt from v_t - v_s.)
             float ks_t = kc_t, ks_s = kc_s;
             if (!(S_t < 1.0e300)) {
                 ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float {
                     if constexpr (KIND == 2) return lc.load(r, e / 4)[e % 4];
                     else if constexpr (KIND == 0) return c1[r][e];
-                    else return c1[r][e] + (kc_s - kc_t) + lc.load(r, e / 4)[e % 4] * c2;
+                    else return c1[r][e] + lc.load(r, e / 4)[e % 4];
                 });
             }
             if (!(S_s < 1.0e300)) {
                 ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float {
                     if constexpr (KIND == 2) return c1[r][e];
                     else if constexpr (KIND == 1) return c1[r][e];
-                    else return c1[r][e] + (kc_t - kc_s) - lc.load(r, e / 4)[e % 4] * c2;
+                    else return c1[r][e] - lc.load(r, e / 4)[e % 4];
                 });
             }
             float Kt = ks_t, Ks = ks_s;
@@ -223,7 +223,10 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             // difference is needed in fp64 (from the ratio of the sums).
             const double dTd = double(Kt - Ks) + (St == Ss ? 0.0 : log2_pos(St / Ss));
             const float ct = float(double(Kt - kc_t) + log2_pos(St)), cs = float(double(Ks - kc_s) + log2_pos(Ss));
-            const float dT = float(dTd);  // log2 p - log2 q = (t - s) c2 - dT
+            // FKL/RKL: log2(p/q) = (v_t - v_s) - dTk, from the same rounded
+            // exponents as the sums (so the normalisers and the log-ratios
+            // agree: rows with p ~ q keep their small divergence accurate).
+            const float dTk = float(dTd - double(kc_t - kc_s));
 
             // ---- loss pass (from the cache) ----
             float acc0 = 0.0f, acc1 = 0.0f;
@@ -239,17 +242,23 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                         const int e = 4 * g + j;
                         if constexpr (KIND == 2) {
                             const float lp = c0v[j] - ct, lq = c1[r][e] - cs;
+                            // log2 m = lp + L, L = log2(beta + (1 - beta) 2^(lq - lp)): the
+                            // mixture's log relative to p, a number near 0 when p ~ q, so the
+                            // rounding of log2 m does not bias every term of a small divergence.
+                            // The ratio is clamped to 2^+-126; both limits stay exact enough
+                            // (the vanishing side carries no weight).
+                            const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                            const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
                             const float p = exp2_fast(lp), q = exp2_fast(lq);
-                            const float lm = log2_fast(__builtin_fmaf(beta, p, __builtin_fmaf(omb, q, kMixFloor)));
-                            const float x = lq - lm;
-                            a0 = __builtin_fmaf(p, lp - lm, a0);
+                            const float x = d - L;  // log2(q/m)
+                            a0 = __builtin_fmaf(p, -L, a0);
                             a1 = __builtin_fmaf(q, x, a1);
                             c0v[j] = x;
                             c1[r][e] = q;
                         } else {
                             // log2(p/q), clamped so that a zero probability
                             // times an infinite log-ratio stays 0.
-                            const float lr = fmaxf(fminf(__builtin_fmaf(c0v[j], c2, -dT), -kLogFloor), kLogFloor);
+                            const float lr = fmaxf(fminf(c0v[j] - dTk, -kLogFloor), kLogFloor);
                             if constexpr (KIND == 0) {
                                 const float lp = c1[r][e] - ct;
                                 const float p = exp2_fast(lp);

@@ -237,6 +237,18 @@ def test_distill_llama_vocab_on_rejected_rows(osd, sigma):
                   B=x["B"], K=K, tstride=(K + 1) * x["V"], sstride=K * x["V"])
 
 
+@pytest.mark.parametrize("kind", ["fkl", "rkl", "jsd"])
+def test_distill_llama_vocab_small_divergence_all_rows(osd, kind):
+    """sigma = 0.25 (D ~ 0.01-0.02 nats per row, peaked rows) on every row:
+    the divergence is a small difference of large terms, so the log-ratios
+    and the normalisers must be formed from the same rounded exponents."""
+    x = synth.config_llama_vocab(0.25, 0)
+    K = x["K"]
+    check_distill(osd, x["target"], x["draft"], kind, 0.5, 1.0, np.ones((x["B"], K), np.uint8),
+                  f"llama {kind} sigma=0.25 all rows", B=x["B"], K=K, tstride=(K + 1) * x["V"],
+                  sstride=K * x["V"])
+
+
 @pytest.mark.parametrize("kind", ["rkl", "jsd"])
 def test_distill_t5_vocab_full_batch(osd, kind):
     x = synth.config_t5_vocab(0)
