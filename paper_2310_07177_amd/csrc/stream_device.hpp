@@ -84,18 +84,6 @@ __device__ inline float first_chunk_shift(const chunk_t& c, float c2) {
     return (k > -3.0e38f && k < 3.0e38f) ? k : 0.0f;
 }
 
-// ---------------------------------------------------------------------------
-// Wave64 reductions and scans on DPP (data-parallel primitives: operand lane
-// permutations inside the vector ALU).  Lane shuffles compile to LDS permute
-// round trips; these do not.  Steps: row_shr 1, 2, 4, 8 form inclusive
-// prefixes inside each row of 16 lanes, then row_bcast 15 and 31 carry the row
-// totals into the later rows.  Lanes whose source is outside the row (or a
-// disabled row) take the identity.  The order of operations is fixed, so
-// results are reproducible.  The total ends in lane 63; readlane broadcasts it.
-// ---------------------------------------------------------------------------
-enum : int { kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
-             kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143 };
-
 // The thread index through an opaque copy: lane and wave numbers derived from
 // it are recomputed where they are used instead of being kept alive (or
 // spilled) across a long loop.
@@ -103,74 +91,6 @@ __device__ inline int opaque_tid() {
     int t = threadIdx.x;
     asm volatile("" : "+v"(t));
     return t;
-}
-
-template <int CTRL, int ROWS>
-__device__ inline uint32_t dpp(uint32_t identity, uint32_t v) {
-    return uint32_t(__builtin_amdgcn_update_dpp(int(identity), int(v), CTRL, ROWS, 0xF, false));
-}
-__device__ inline uint32_t readlane_u32(uint32_t v, int lane) {
-    return uint32_t(__builtin_amdgcn_readlane(int(v), lane));
-}
-__device__ inline float readlane_f32(float v, int lane) {
-    return __uint_as_float(readlane_u32(__float_as_uint(v), lane));
-}
-__device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
-    return uint64_t(readlane_u32(uint32_t(v), lane)) | (uint64_t(readlane_u32(uint32_t(v >> 32), lane)) << 32);
-}
-__device__ inline double readlane_f64(double v, int lane) {
-    return __builtin_bit_cast(double, readlane_u64(__builtin_bit_cast(uint64_t, v), lane));
-}
-
-// Floats as unsigned keys in the same order (no NaN): a float maximum over
-// lanes becomes an unsigned one, which the DPP move folds into (identity 0)
-// and which needs no NaN quieting of each operand.
-__device__ inline uint32_t float_key(float f) {
-    const uint32_t b = __float_as_uint(f);
-    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-__device__ inline float key_float(uint32_t k) {
-    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
-template <int CTRL, int ROWS>
-__device__ inline uint32_t dpp_umax_step(uint32_t k) {
-    const uint32_t o = dpp<CTRL, ROWS>(0u, k);
-    return k > o ? k : o;
-}
-// A 32-bit lane permutation for a sum (identity 0).  Every row enabled
-// (the row shifts): lanes whose source is outside the row read 0 through
-// the bound control, and no register has to be preset to the identity.
-template <int CTRL, int ROWS>
-__device__ inline uint32_t dpp_sum_src(uint32_t v) {
-    if constexpr (ROWS == 0xF)
-        return uint32_t(__builtin_amdgcn_mov_dpp(int(v), CTRL, 0xF, 0xF, true));
-    else
-        return dpp<CTRL, ROWS>(0u, v);
-}
-template <int CTRL, int ROWS>
-__device__ inline double dpp_add_step(double v) {
-    const uint64_t b = __builtin_bit_cast(uint64_t, v);
-    const uint64_t o = uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(b))) |
-                       (uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(b >> 32))) << 32);
-    return v + __builtin_bit_cast(double, o);
-}
-template <int CTRL, int ROWS>
-__device__ inline uint64_t dpp_add_step(uint64_t v) {
-    const uint64_t o = uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(v))) |
-                       (uint64_t(dpp_sum_src<CTRL, ROWS>(uint32_t(v >> 32))) << 32);
-    return v + o;
-}
-
-// Inclusive scans over the wave (lane 63 holds the total).
-template <typename T>
-__device__ inline T wave_scan_add(T v) {
-    v = dpp_add_step<kDppRowShr1, 0xF>(v);
-    v = dpp_add_step<kDppRowShr2, 0xF>(v);
-    v = dpp_add_step<kDppRowShr4, 0xF>(v);
-    v = dpp_add_step<kDppRowShr8, 0xF>(v);
-    v = dpp_add_step<kDppRowBcast15, 0xA>(v);
-    v = dpp_add_step<kDppRowBcast31, 0xC>(v);
-    return v;
 }
 
 // Wave totals, uniform.  (The maximum of values without NaN.)
