@@ -11,10 +11,14 @@ osd_distill_loss_grad) is timed too and reported beside it.
 
 Inputs are synthetic and seeded; R copies of the batch rotate through the
 timed loop so that consecutive launches never find their inputs in the 256 MB
-Infinity Cache.  The timed steps are captured once into a HIP graph and
+Infinity Cache.  The timed steps are captured once into HIP graphs and
 replayed, so that host launch overhead does not pace the GPU (the library
 allocates nothing and clears its own workspace, so its calls capture as they
-are).  Each entry point is also timed alone the same way (HIP events on the
+are).  Independent steps are kept in flight on --streams streams (default 2,
+steps alternating, each call with its own workspace), as a serving loop with
+more than one batch would: one call's last workgroups then overlap the next
+call's first loads.  The same steps one after another on one stream are
+timed too and reported beside it.  Each entry point is also timed alone the same way (HIP events on the
 stream the kernels run on) to report its achieved HBM bandwidth against the
 8 TB/s peak.  The CPU baseline is the fp64 oracle on the host.
 
@@ -46,6 +50,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--kernel-iters", type=int, default=400)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--streams", type=int, default=2,
+                   help="independent steps in flight: consecutive steps alternate between this many "
+                        "streams, each call with its own workspace")
     p.add_argument("--only", default=None,
                    help="profiling aid: run only the named loops, comma-separated "
                         "(verify,greedy,jsd,rkl,fused,sample_prop,sample_mix,copy)")
@@ -206,6 +213,18 @@ def main():
                    P(s["ua"]), P(s["ur"]), ctypes.c_float(T_VERIFY), P(s["acc"]), P(s["toks"]),
                    P(s["rmask"]), P(s["mask"]), binding.OSD_JSD, ctypes.c_float(BETA), P(s["loss"]),
                    P(s["rows"]), P(s["grad"]), P(fws), fws.numel(), hs) for s in sets]
+    # Steps in flight on several streams: stream j runs steps j, j+S, ...,
+    # each call with its own workspace (the library's contract for calls that
+    # may overlap).  A kernel's last workgroups and the next kernel's first
+    # loads then overlap across streams.
+    nstr = max(1, args.streams)
+    streams = [stream] + [torch.cuda.Stream(dev) for _ in range(nstr - 1)]
+    for st in streams[1:]:
+        st.wait_stream(torch.cuda.current_stream(dev))
+    ws_s = [fws] + [torch.zeros_like(fws) for _ in range(nstr - 1)]
+    torch.cuda.synchronize()
+    fused_args_s = [[a[:-3] + (P(ws_s[j]), ws_s[j].numel(), ctypes.c_void_p(streams[j].cuda_stream))
+                     for a in fused_args] for j in range(nstr)]
     fv, fd, ff = L.osd_verify, L.osd_distill_loss_grad, L.osd_verify_distill
 
     # Token sampling: the draft proposals of one step (draft row 0 of every
@@ -297,14 +316,45 @@ def main():
                               "launches": args.warmup + args.kernel_iters}), flush=True)
         return
 
-    with torch.cuda.stream(stream):
-        for r in range(args.warmup):
-            step(r)
+    for r in range(args.warmup):
+        with torch.cuda.stream(streams[r % nstr]):
+            call(ff, fused_args_s[r % nstr][r % R])
     torch.cuda.synchronize()
-    print(f"# warmup done: {args.warmup} steps, R={R} rotating input sets", file=sys.stderr, flush=True)
-    # Exactly K steps, captured once and replayed between events.
-    ms_step = time_graph(capture(step, args.steps), args.steps)
-    print(f"# timed {args.steps} steps: {ms_step * 1e3:.2f} us/step", file=sys.stderr, flush=True)
+    print(f"# warmup done: {args.warmup} steps, R={R} rotating input sets, {nstr} stream(s)",
+          file=sys.stderr, flush=True)
+    # Exactly K steps, captured once (stream j: steps j, j+S, ...) and
+    # replayed between events on the stream that joins them.
+    graphs = []
+    for j in range(nstr):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=streams[j]):
+            for r in range(j, args.steps, nstr):
+                call(ff, fused_args_s[j][r % R])
+        graphs.append(g)
+    main = torch.cuda.current_stream(dev)
+
+    def replay_all():
+        for st in streams:
+            st.wait_stream(main)
+        for g, st in zip(graphs, streams):
+            with torch.cuda.stream(st):
+                g.replay()
+        for st in streams:
+            main.wait_stream(st)
+
+    replay_all()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(main)
+    replay_all()
+    e1.record(main)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    print(f"# timed {args.steps} steps on {nstr} stream(s): {ms_step * 1e3:.2f} us/step",
+          file=sys.stderr, flush=True)
+    ms_one = time_graph(capture(step, args.steps), args.steps) if nstr > 1 else ms_step
+    print(f"# the same steps one after another on one stream: {ms_one * 1e3:.2f} us/step",
+          file=sys.stderr, flush=True)
 
     ms_sep = time_loop(step_separate, args.steps)
     print(f"# the same step as osd_verify + osd_distill_loss_grad: {ms_sep * 1e3:.2f} us/step",
@@ -355,6 +405,8 @@ def main():
         "kernels": kernels,
         "step_GBps": round(kernels["verify_distill"]["algorithmic_bytes"] / (ms_step * 1e-3) / 1e9, 1),
         "separate_calls_ms_per_step": round(ms_sep, 6),
+        "streams": nstr,
+        "single_stream_ms_per_step": round(ms_one, 6),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
