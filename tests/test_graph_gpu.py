@@ -149,3 +149,60 @@ def test_graph_replays_match_eager_fused():
             step(b)
         torch.cuda.synchronize()
     assert int(ws.count_nonzero()) == 0
+
+
+def test_concurrent_calls_on_two_streams():
+    """Fused calls on two streams at once, each with its own workspace (the
+    way bench.py keeps two steps in flight): every output equals that of the
+    same call made alone, and both workspaces end zeroed."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    dev = torch.device("cuda:0")
+    L = binding.lib()
+    B, K, V = 64, 8, 32128
+    sets = []
+    for seed in (7, 8, 9, 10):
+        x = synth.verify_inputs(B, K, V, "bf16", T=0.7, seed=seed, target_std=2.5, draft_scale=0.7,
+                                draft_noise=1.5)
+        s = {k: _dev(x[k], dev) for k in ("target", "draft", "u_accept", "u_resample")}
+        s["tokens"] = _dev(x["tokens"].astype(np.int32), dev)
+        s["acc"] = torch.empty(B, dtype=torch.int32, device=dev)
+        s["toks"] = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+        s["rmask"] = torch.empty(B, K, dtype=torch.uint8, device=dev)
+        s["loss"] = torch.empty(2, dtype=torch.float32, device=dev)
+        s["rows"] = torch.empty(B, K, dtype=torch.float32, device=dev)
+        s["grad"] = torch.empty(B, K, V, dtype=torch.bfloat16, device=dev)
+        sets.append(s)
+    streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+    wss = [torch.zeros(L.osd_verify_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+           for _ in streams]
+    torch.cuda.synchronize()
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    keys = ("acc", "toks", "rmask", "loss", "rows", "grad")
+
+    def call(s, j):
+        st = L.osd_verify_distill(P(s["target"]), P(s["draft"]), binding.OSD_BF16, B, K, V, P(s["tokens"]),
+                                  None, P(s["u_accept"]), P(s["u_resample"]), ctypes.c_float(0.7), P(s["acc"]),
+                                  P(s["toks"]), P(s["rmask"]), None, binding.OSD_JSD, ctypes.c_float(0.5),
+                                  P(s["loss"]), P(s["rows"]), P(s["grad"]), P(wss[j]), wss[j].numel(),
+                                  ctypes.c_void_p(streams[j].cuda_stream))
+        assert st == 0
+
+    alone = []
+    for s in sets:
+        call(s, 0)
+        torch.cuda.synchronize()
+        alone.append([s[k].clone() for k in keys])
+    for rep in range(3):
+        for s in sets:
+            for k in keys:
+                s[k].zero_()
+        torch.cuda.synchronize()
+        for i, s in enumerate(sets):  # sets 0, 2 on stream 0; 1, 3 on stream 1
+            call(s, i % 2)
+        torch.cuda.synchronize()
+        for i, s in enumerate(sets):
+            for k, want in zip(keys, alone[i]):
+                assert torch.equal(s[k], want), f"rep {rep} set {i} {k}"
+    assert all(int(w.count_nonzero()) == 0 for w in wss)
