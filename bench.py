@@ -55,7 +55,7 @@ def parse():
                         "streams, each call with its own workspace")
     p.add_argument("--only", default=None,
                    help="profiling aid: run only the named loops, comma-separated "
-                        "(verify,greedy,jsd,rkl,fused,sample_prop,sample_mix,copy)")
+                        "(verify,greedy,jsd,rkl,fused,sample_prop,sample_mix,shard_stats,shard_step,copy)")
     return p.parse_args()
 
 
@@ -94,6 +94,22 @@ def sample_bytes(N, V, rows, elem=2):
 # = teacher + N(0, 1), beta = 0.5, T = 1.  0.5 GB per call, beyond the
 # Infinity Cache, so one input set suffices.
 MIX_N, MIX_V, MIX_BETA, MIX_T = 4096, 32000, 0.5, 1.0
+
+# Vocabulary-sharded verification, one rank's share of a tensor-parallel LM
+# head: the large-vocabulary serving step (B = 256 sequences, k_b ~ U{1..8},
+# V = 128256 bf16, target ~ N(0, 3^2), draft = target + N(0, 1), T = 0.8)
+# split over 8 ranks of 16032 columns each.  All 8 ranks' slices stay
+# resident (1.1 GB) and consecutive timed steps take consecutive ranks, so no
+# step finds its slice in the Infinity Cache.
+SH_B, SH_K, SH_V, SH_G, SH_T = 256, 8, 128256, 8, 0.8
+
+
+def shard_stats_bytes(klen, Vs, elem=2):
+    """Algorithmic bytes of one rank's osd_shard_verify_stats call: target
+    slice rows 0..k_b and draft slice rows 0..k_b-1 read once, the proposals
+    read, one 40-byte record written per row pair."""
+    rows = int((2 * klen + 1).sum())
+    return rows * Vs * elem + 4 * int(klen.sum()) + 4 * len(klen) + 40 * int((klen + 1).sum())
 
 
 def kernel_source_hash():
@@ -247,6 +263,44 @@ def main():
                 ctypes.c_float(MIX_BETA), P(mix_u), P(mix_out), hs)
     torch.cuda.synchronize()
 
+    # Sharded verification: the whole rows are generated on the device, cut
+    # into the 8 ranks' contiguous slices, and freed; proposals are drawn
+    # from softmax(draft / T) by Gumbel-max.
+    sh_gen = torch.Generator(device=dev)
+    sh_gen.manual_seed(16 * 5 + synth.SEED_LOGITS)
+    sh_klen_np = synth.rng(16 * 5 + synth.SEED_AUX).integers(1, SH_K + 1, size=SH_B).astype(np.int32)
+    Vs = SH_V // SH_G
+    sh_t = [None] * SH_G
+    sh_d = [None] * SH_G
+    full_t = torch.randn(SH_B, SH_K + 1, SH_V, generator=sh_gen, device=dev) * 3.0
+    full_d = full_t[:, :SH_K] + torch.randn(SH_B, SH_K, SH_V, generator=sh_gen, device=dev)
+    gum = -torch.log(-torch.log(torch.rand(SH_B, SH_K, SH_V, generator=sh_gen, device=dev).clamp_min(1e-30)))
+    full_d = full_d.to(torch.bfloat16)
+    sh_tokens = torch.argmax(full_d.float() / SH_T + gum, dim=-1).to(torch.int32).contiguous()
+    del gum
+    full_t = full_t.to(torch.bfloat16)
+    for g in range(SH_G):
+        sh_t[g] = full_t[:, :, g * Vs:(g + 1) * Vs].contiguous()
+        sh_d[g] = full_d[:, :, g * Vs:(g + 1) * Vs].contiguous()
+    del full_t, full_d
+    sh_klen = t_(sh_klen_np)
+    sh_ua = torch.rand(SH_B, SH_K, generator=sh_gen, device=dev)
+    sh_ur = torch.rand(SH_B, generator=sh_gen, device=dev)
+    sh_stats = torch.zeros(SH_G, SH_B, SH_K + 1, binding.SHARD_ROW_STATS_BYTES, dtype=torch.uint8, device=dev)
+    sh_mass = torch.zeros(SH_G, SH_B, binding.SHARD_MASS_BYTES, dtype=torch.uint8, device=dev)
+    sh_acc = torch.empty(SH_B, dtype=torch.int32, device=dev)
+    sh_toks = torch.empty(SH_B, SH_K + 1, dtype=torch.int32, device=dev)
+    sh_rm = torch.empty(SH_B, SH_K, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    f1, f2, f3 = L.osd_shard_verify_stats, L.osd_shard_verify_mass, L.osd_shard_verify_draw
+    cT = ctypes.c_float(SH_T)
+    sh1 = [(P(sh_t[g]), P(sh_d[g]), binding.OSD_BF16, SH_B, SH_K, Vs, g * Vs, SH_V, P(sh_tokens), P(sh_klen), cT,
+            P(sh_stats[g]), hs) for g in range(SH_G)]
+    sh2 = [(P(sh_t[g]), P(sh_d[g]), binding.OSD_BF16, SH_B, SH_K, Vs, SH_G, P(sh_tokens), P(sh_klen), P(sh_ua),
+            cT, P(sh_stats), P(sh_mass[g]), hs) for g in range(SH_G)]
+    sh3 = [(P(sh_t[g]), P(sh_d[g]), binding.OSD_BF16, SH_B, SH_K, Vs, g * Vs, SH_G, g, P(sh_tokens), P(sh_klen),
+            P(sh_ur), cT, P(sh_mass), P(sh_acc), P(sh_toks), P(sh_rm), hs) for g in range(SH_G)]
+
     def call(f, a):
         st = f(*a)
         if st != 0:
@@ -258,6 +312,23 @@ def main():
     def step_separate(r):
         call(fv, verify_args[r % R])
         call(fd, jsd_args[r % R])
+
+    # Every rank's phases once, untimed, so that the records each phase
+    # reads are the exchanged ones (the all-gathers are the shared arrays).
+    with torch.cuda.stream(stream):
+        for g in range(SH_G):
+            call(f1, sh1[g])
+        for g in range(SH_G):
+            call(f2, sh2[g])
+    torch.cuda.synchronize()
+
+    def shard_step(r):
+        """One rank's share of a sharded verification step (rank r mod 8):
+        its three phases; the exchanges between them are not run."""
+        g = r % SH_G
+        call(f1, sh1[g])
+        call(f2, sh2[g])
+        call(f3, sh3[g])
 
     def capture(fn, iters):
         """A HIP graph of fn(0..iters-1) on the side stream."""
@@ -296,7 +367,9 @@ def main():
                  "jsd": lambda r: call(fd, jsd_args[r % R]),
                  "rkl": lambda r: call(fd, rkl_args[r % R]),
                  "sample_prop": lambda r: call(fs, prop_args[r % R]),
-                 "sample_mix": lambda r: call(fs, mix_args)}
+                 "sample_mix": lambda r: call(fs, mix_args),
+                 "shard_stats": lambda r: call(f1, sh1[r % SH_G]),
+                 "shard_step": shard_step}
         for name in args.only.split(","):
             if name == "copy":
                 src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -378,6 +451,23 @@ def main():
         print(f"# {name}: {ms * 1e3:.2f} us/launch, {gbs:.0f} GB/s ({100 * gbs / PEAK_HBM_GBS:.1f}% of peak)",
               file=sys.stderr, flush=True)
 
+    ms_sh1 = time_loop(lambda r: call(f1, sh1[r % SH_G]), args.kernel_iters)
+    ms_shs = time_loop(shard_step, args.kernel_iters)
+    sh_bytes = shard_stats_bytes(sh_klen_np, Vs)
+    sh_gbs = sh_bytes / (ms_sh1 * 1e-3) / 1e9
+    sh_pos = int(sh_klen_np.sum())
+    kernels["shard_stats"] = {"us_per_launch": round(ms_sh1 * 1e3, 3), "algorithmic_bytes": sh_bytes,
+                              "achieved_GBps": round(sh_gbs, 1), "frac_of_peak": round(sh_gbs / PEAK_HBM_GBS, 4)}
+    sharded = {"workload": f"large-vocab ragged verify, one rank of {SH_G}: B={SH_B}, k_b~U{{1..{SH_K}}} "
+                           f"(sum {sh_pos}), V={SH_V} bf16 over {SH_G} slices of {Vs}, T={SH_T}",
+               "us_per_rank_step": round(ms_shs * 1e3, 3),
+               "positions_per_s": round(sh_pos / (ms_shs * 1e-3), 1),
+               "exchanges": "not run (one GPU): 3 per step, records of "
+                            f"{SH_G * SH_B * (SH_K + 1) * 40} + {SH_G * SH_B * 48} + {SH_B * (SH_K + 1) * 4} B"}
+    print(f"# shard_stats: {ms_sh1 * 1e3:.2f} us/launch, {sh_gbs:.0f} GB/s ({100 * sh_gbs / PEAK_HBM_GBS:.1f}% "
+          f"of peak); one rank's 3-phase step: {ms_shs * 1e3:.2f} us, {sh_pos / (ms_shs * 1e-3) / 1e6:.2f} M "
+          "positions/s", file=sys.stderr, flush=True)
+
     # The step is one kernel.
     dom = "verify_distill"
     kd = kernels[dom]
@@ -407,6 +497,7 @@ def main():
         "separate_calls_ms_per_step": round(ms_sep, 6),
         "streams": nstr,
         "single_stream_ms_per_step": round(ms_one, 6),
+        "sharded_verify": sharded,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()

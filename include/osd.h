@@ -3,7 +3,7 @@
  * path of online speculative decoding (Liu et al., "Online Speculative
  * Decoding", ICML 2024, arXiv:2310.07177).
  *
- * Two operations:
+ * Two operations (and their fused, sampling and vocabulary-sharded forms):
  *   osd_verify             speculative-sampling verification of k proposed
  *                          tokens against the target (Appendix A.1, Eq. 5;
  *                          Algorithm 1, the verification step);
@@ -216,6 +216,101 @@ int osd_sample(const void* p_logits, int64_t p_row_stride,
                const void* q_logits, int64_t q_row_stride,
                int dtype, int N, int V, float temperature, float beta,
                const float* u, int32_t* out_tokens, void* stream);
+
+/*
+ * Vocabulary-sharded verification.  When the target and draft LM heads are
+ * split by vocabulary over G ranks (tensor parallelism), rank g holds columns
+ * [v_begin_g, v_begin_g + V_g) of every logit row, and no rank sees a whole
+ * row.  The verification of osd_verify (Appendix A.1, Eq. 5) then runs in
+ * three phases with one exchange after each:
+ *
+ *   1. osd_shard_verify_stats   each rank reduces its slice of every row to an
+ *                               osd_shard_row_stats record;
+ *      -> all-gather of the records over the G ranks, in rank order
+ *         (stats_all [G, B, K+1]);
+ *   2. osd_shard_verify_mass    every rank merges the G records of each row
+ *                               (identically, in rank order), takes the
+ *                               acceptance tests, finds the first rejection a_b,
+ *                               and sums the extra draw's mass over its own
+ *                               slice of row a_b into an osd_shard_mass record;
+ *      -> all-gather of those records (mass_all [G, B]);
+ *   3. osd_shard_verify_draw    every rank finds which slice holds the point
+ *                               u * Z of the whole row's CDF; that rank draws
+ *                               the token from its slice.  Every rank writes
+ *                               the same accepted_len and reject_mask and an
+ *                               out_tokens row whose extra token is -1 except
+ *                               on the drawing rank;
+ *      -> all-reduce MAX of out_tokens gives every rank the result.
+ *
+ * The result is osd_verify's on the whole rows: masses are summed in exact
+ * fixed point, so how the vocabulary is split changes no decision beyond the
+ * fp32 rounding that osd_verify documents.  The slices must partition
+ * [0, V) in rank order (v_begin_0 = 0, v_begin_{g+1} = v_begin_g + V_g).
+ * Greedy verification (T == 0) needs phases 1-3 too; its phase 2 finds the
+ * extra token itself (the argmax) and phase 3 draws nothing.
+ *
+ * Shard logits are row-major [B, K+1, V_g] (target) and [B, K, V_g] (draft),
+ * each row contiguous.  Arguments shared with osd_verify (draft_tokens as
+ * global ids, draft_len, u_accept, u_resample, temperature, the outputs) have
+ * its meaning.  Records are 8-byte aligned device arrays owned by the caller;
+ * rows past k_b are neither read nor written.  No workspace.  Errors:
+ * OSD_ERR_INVALID_ARG for a bad dtype, sizes <= 0, K > OSD_MAX_K, G outside
+ * 1..OSD_MAX_SHARDS, shard outside [0, G), a slice outside [0, V), T < 0 or
+ * not finite, a needed NULL pointer or a misaligned record array;
+ * OSD_ERR_UNSUPPORTED for V_g > osd_max_vocab(dtype); OSD_ERR_DEVICE for a
+ * failed launch.  Nothing is enqueued on an error.
+ */
+#define OSD_MAX_SHARDS 64
+
+/* One rank's reduction of its slice of one logit row pair (40 bytes). */
+typedef struct {
+    double s_target;  /* T > 0: sum over the slice of 2^(t_j log2(e)/T - k_target) */
+    double s_draft;   /* T > 0: the same for the draft row (proposal rows only)   */
+    float k_target;   /* T > 0: whole-number shift >= max_j t_j log2(e)/T, -inf if
+                         the slice has no finite logit; T == 0: max_j t_j      */
+    float k_draft;    /* T > 0: the draft row's shift                           */
+    float t_y, d_y;   /* T > 0: target and draft logits of the proposal y_i when
+                         this slice holds it                                   */
+    int32_t argmax;   /* T == 0: global id of the slice's largest target logit
+                         (lowest id on ties), -1 if the slice has none           */
+    int32_t flags;    /* bit 0: the slice holds y_i; bit 1: y_i lies outside [0, V) */
+} osd_shard_row_stats;
+
+/* One rank's part of a sequence's extra draw (48 bytes). */
+typedef struct {
+    uint64_t z;        /* mass of max(0, p - q) (of p at the bonus row) over the
+                          slice, 2^-44 fixed point in units of the target row's
+                          sum of exponentials                                  */
+    uint64_t z_p;      /* mass of p over the slice, same units (used should the
+                          whole row's residual mass round to 0)                 */
+    double s_target, s_draft;  /* merged sums of row a_b (whole row)           */
+    float k_target, k_draft;   /* their shifts                                 */
+    int32_t accepted;  /* a_b, or -1 for an invalid sequence                   */
+    int32_t token;     /* T == 0: the extra token (global id); else -1         */
+} osd_shard_mass;
+
+int osd_shard_verify_stats(const void* target_shard, const void* draft_shard, int dtype,
+                           int B, int K, int V_shard, int v_begin, int V,
+                           const int32_t* draft_tokens, const int32_t* draft_len,
+                           float temperature,
+                           osd_shard_row_stats* stats, /* out [B, K+1] */
+                           void* stream);
+
+int osd_shard_verify_mass(const void* target_shard, const void* draft_shard, int dtype,
+                          int B, int K, int V_shard, int G,
+                          const int32_t* draft_tokens, const int32_t* draft_len,
+                          const float* u_accept, float temperature,
+                          const osd_shard_row_stats* stats_all, /* [G, B, K+1] */
+                          osd_shard_mass* mass,                 /* out [B]      */
+                          void* stream);
+
+int osd_shard_verify_draw(const void* target_shard, const void* draft_shard, int dtype,
+                          int B, int K, int V_shard, int v_begin, int G, int shard,
+                          const int32_t* draft_tokens, const int32_t* draft_len,
+                          const float* u_resample, float temperature,
+                          const osd_shard_mass* mass_all,       /* [G, B] */
+                          int32_t* accepted_len, int32_t* out_tokens,
+                          uint8_t* reject_mask, void* stream);
 
 #ifdef __cplusplus
 }

@@ -18,11 +18,17 @@ OSD_OK, OSD_ERR_INVALID_ARG, OSD_ERR_UNSUPPORTED, OSD_ERR_DEVICE, OSD_ERR_WORKSP
 OSD_F32, OSD_BF16 = 0, 1
 OSD_FKL, OSD_RKL, OSD_JSD = 0, 1, 2
 OSD_MAX_K = 16
+OSD_MAX_SHARDS = 64
+# Byte sizes of the sharded verification's records (osd_shard_row_stats,
+# osd_shard_mass in include/osd.h); the binding keeps them as uint8 tensors.
+SHARD_ROW_STATS_BYTES = 40
+SHARD_MASS_BYTES = 48
 KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
 EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify",
            "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
-           "osd_verify_distill", "osd_sample")
+           "osd_verify_distill", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
+           "osd_shard_verify_draw")
 
 _lib = None
 _lock = threading.Lock()
@@ -66,6 +72,13 @@ def lib():
                                              vp, i32, f32, vp, vp, vp, vp, sz, vp]
             L.osd_sample.restype = i32
             L.osd_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f32, vp, vp, vp]
+            L.osd_shard_verify_stats.restype = i32
+            L.osd_shard_verify_stats.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, f32, vp, vp]
+            L.osd_shard_verify_mass.restype = i32
+            L.osd_shard_verify_mass.argtypes = [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp]
+            L.osd_shard_verify_draw.restype = i32
+            L.osd_shard_verify_draw.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, f32,
+                                                vp, vp, vp, vp, vp]
             _lib = L
     return _lib
 
@@ -266,3 +279,81 @@ def osd_sample(p_logits, q_logits, temperature, beta, u=None, out=None):
     if st != OSD_OK:
         raise OsdError("osd_sample", st)
     return out
+
+
+def _shard_args(target_shard, draft_shard, draft_tokens, draft_len, temperature, *more):
+    torch = _torch()
+    _check_cuda(target_shard, draft_shard, draft_tokens, draft_len, *more)
+    for t in (target_shard, draft_shard, draft_tokens, draft_len) + more:
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if draft_tokens.dtype != torch.int32 or (draft_len is not None and draft_len.dtype != torch.int32):
+        raise TypeError("draft_tokens and draft_len must be int32")
+    if temperature != 0 and draft_shard is not None and draft_shard.dtype != target_shard.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    B, K1, Vs = target_shard.shape
+    return B, K1 - 1, Vs
+
+
+def osd_shard_verify_stats(target_shard, draft_shard, draft_tokens, temperature, v_begin, V, draft_len=None,
+                           out=None):
+    """Phase 1 of vocabulary-sharded verification on this rank's slice
+    (target_shard [B, K+1, V_g], draft_shard [B, K, V_g], columns
+    v_begin .. v_begin+V_g-1 of a V-token vocabulary).  Returns the
+    osd_shard_row_stats records as a uint8 tensor [B, K+1, 40]."""
+    torch = _torch()
+    B, K, Vs = _shard_args(target_shard, draft_shard, draft_tokens, draft_len, temperature)
+    if out is None:
+        out = torch.empty(B, K + 1, SHARD_ROW_STATS_BYTES, dtype=torch.uint8, device=target_shard.device)
+    st = lib().osd_shard_verify_stats(_ptr(target_shard), _ptr(draft_shard), _dtype_code(target_shard), B, K, Vs,
+                                      int(v_begin), int(V), _ptr(draft_tokens), _ptr(draft_len),
+                                      float(temperature), _ptr(out), _stream_handle(target_shard.device))
+    if st != OSD_OK:
+        raise OsdError("osd_shard_verify_stats", st)
+    return out
+
+
+def osd_shard_verify_mass(target_shard, draft_shard, draft_tokens, u_accept, temperature, stats_all,
+                          draft_len=None, out=None):
+    """Phase 2: stats_all [G, B, K+1, 40] holds the records of every rank in
+    rank order (the all-gather of phase 1).  Returns this rank's
+    osd_shard_mass records as a uint8 tensor [B, 48]."""
+    torch = _torch()
+    B, K, Vs = _shard_args(target_shard, draft_shard, draft_tokens, draft_len, temperature, u_accept, stats_all)
+    G = stats_all.shape[0]
+    if tuple(stats_all.shape) != (G, B, K + 1, SHARD_ROW_STATS_BYTES) or stats_all.dtype != torch.uint8:
+        raise ValueError("stats_all must be a uint8 tensor [G, B, K+1, 40]")
+    if out is None:
+        out = torch.empty(B, SHARD_MASS_BYTES, dtype=torch.uint8, device=target_shard.device)
+    st = lib().osd_shard_verify_mass(_ptr(target_shard), _ptr(draft_shard), _dtype_code(target_shard), B, K, Vs,
+                                     G, _ptr(draft_tokens), _ptr(draft_len), _ptr(u_accept), float(temperature),
+                                     _ptr(stats_all), _ptr(out), _stream_handle(target_shard.device))
+    if st != OSD_OK:
+        raise OsdError("osd_shard_verify_mass", st)
+    return out
+
+
+def osd_shard_verify_draw(target_shard, draft_shard, draft_tokens, u_resample, temperature, v_begin, shard,
+                          mass_all, draft_len=None, out=None):
+    """Phase 3: mass_all [G, B, 48] holds every rank's phase-2 records in rank
+    order.  Returns (accepted_len [B], out_tokens [B, K+1], reject_mask
+    [B, K]); out_tokens carries the extra token only on the rank that drew
+    it (-1 on the others), so an all-reduce MAX over the ranks completes it."""
+    torch = _torch()
+    B, K, Vs = _shard_args(target_shard, draft_shard, draft_tokens, draft_len, temperature, u_resample, mass_all)
+    G = mass_all.shape[0]
+    if tuple(mass_all.shape) != (G, B, SHARD_MASS_BYTES) or mass_all.dtype != torch.uint8:
+        raise ValueError("mass_all must be a uint8 tensor [G, B, 48]")
+    dev = target_shard.device
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, K + 1, dtype=torch.int32, device=dev),
+               torch.empty(B, K, dtype=torch.uint8, device=dev))
+    acc, toks, rmask = out
+    st = lib().osd_shard_verify_draw(_ptr(target_shard), _ptr(draft_shard), _dtype_code(target_shard), B, K, Vs,
+                                     int(v_begin), G, int(shard), _ptr(draft_tokens), _ptr(draft_len),
+                                     _ptr(u_resample), float(temperature), _ptr(mass_all), _ptr(acc), _ptr(toks),
+                                     _ptr(rmask), _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_shard_verify_draw", st)
+    return acc, toks, rmask

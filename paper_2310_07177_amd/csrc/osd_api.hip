@@ -325,3 +325,107 @@ int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits,
 }
 
 }  // extern "C"
+
+namespace {
+
+// Vocabulary-sharded verification: the checks every phase shares.  The whole
+// row's fixed-point mass stays below 2^63 for V <= 2^19.
+constexpr int kMaxShardedVocab = 1 << 19;
+
+int shard_common(const void* target, int dtype, int B, int K, int V_shard, float temperature,
+                 const int32_t* draft_tokens) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || K <= 0 || V_shard <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
+    if (!sizes_ok(B, K, V_shard, dtype)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    if (!target || !draft_tokens) return OSD_ERR_INVALID_ARG;
+    return OSD_OK;
+}
+
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
+
+osd::ShardLaunch shard_launch(int phase, const void* target, const void* draft, int dtype, int B, int K,
+                              int V_shard, float temperature, const int32_t* tokens, const int32_t* draft_len,
+                              void* stream) {
+    osd::ShardLaunch L = {};
+    L.phase = phase;
+    L.target = target;
+    L.draft = temperature == 0.0f ? nullptr : draft;
+    L.dtype = dtype;
+    L.B = B;
+    L.K = K;
+    L.Vs = V_shard;
+    L.tokens = tokens;
+    L.draft_len = draft_len;
+    L.temperature = temperature;
+    L.vec = (int64_t(V_shard) * elem_bytes(dtype)) % 16 == 0 && aligned16(target) &&
+            (L.draft == nullptr || aligned16(L.draft));
+    L.stream = static_cast<hipStream_t>(stream);
+    return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+int osd_shard_verify_stats(const void* target_shard, const void* draft_shard, int dtype, int B, int K,
+                           int V_shard, int v_begin, int V, const int32_t* draft_tokens,
+                           const int32_t* draft_len, float temperature, osd_shard_row_stats* stats,
+                           void* stream) {
+    const int st = shard_common(target_shard, dtype, B, K, V_shard, temperature, draft_tokens);
+    if (st != OSD_OK) return st;
+    if (V <= 0 || v_begin < 0 || int64_t(v_begin) + V_shard > V) return OSD_ERR_INVALID_ARG;
+    if (V > kMaxShardedVocab) return OSD_ERR_UNSUPPORTED;
+    if (temperature > 0.0f && !draft_shard) return OSD_ERR_INVALID_ARG;
+    if (!stats || !aligned8(stats)) return OSD_ERR_INVALID_ARG;
+    osd::ShardLaunch L = shard_launch(1, target_shard, draft_shard, dtype, B, K, V_shard, temperature,
+                                      draft_tokens, draft_len, stream);
+    L.v_begin = v_begin;
+    L.V = V;
+    L.stats = stats;
+    return osd::launch_verify_shard(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+int osd_shard_verify_mass(const void* target_shard, const void* draft_shard, int dtype, int B, int K,
+                          int V_shard, int G, const int32_t* draft_tokens, const int32_t* draft_len,
+                          const float* u_accept, float temperature, const osd_shard_row_stats* stats_all,
+                          osd_shard_mass* mass, void* stream) {
+    const int st = shard_common(target_shard, dtype, B, K, V_shard, temperature, draft_tokens);
+    if (st != OSD_OK) return st;
+    if (G < 1 || G > OSD_MAX_SHARDS) return OSD_ERR_INVALID_ARG;
+    if (temperature > 0.0f && (!draft_shard || !u_accept)) return OSD_ERR_INVALID_ARG;
+    if (!stats_all || !mass || !aligned8(stats_all) || !aligned8(mass)) return OSD_ERR_INVALID_ARG;
+    osd::ShardLaunch L = shard_launch(2, target_shard, draft_shard, dtype, B, K, V_shard, temperature,
+                                      draft_tokens, draft_len, stream);
+    L.G = G;
+    L.u_accept = u_accept;
+    L.stats_in = stats_all;
+    L.mass = mass;
+    return osd::launch_verify_shard(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+int osd_shard_verify_draw(const void* target_shard, const void* draft_shard, int dtype, int B, int K,
+                          int V_shard, int v_begin, int G, int shard, const int32_t* draft_tokens,
+                          const int32_t* draft_len, const float* u_resample, float temperature,
+                          const osd_shard_mass* mass_all, int32_t* accepted_len, int32_t* out_tokens,
+                          uint8_t* reject_mask, void* stream) {
+    const int st = shard_common(target_shard, dtype, B, K, V_shard, temperature, draft_tokens);
+    if (st != OSD_OK) return st;
+    if (G < 1 || G > OSD_MAX_SHARDS || shard < 0 || shard >= G) return OSD_ERR_INVALID_ARG;
+    if (v_begin < 0 || int64_t(v_begin) + V_shard > kMaxShardedVocab) return OSD_ERR_INVALID_ARG;
+    if (temperature > 0.0f && (!draft_shard || !u_resample)) return OSD_ERR_INVALID_ARG;
+    if (!mass_all || !aligned8(mass_all) || !accepted_len || !out_tokens) return OSD_ERR_INVALID_ARG;
+    osd::ShardLaunch L = shard_launch(3, target_shard, draft_shard, dtype, B, K, V_shard, temperature,
+                                      draft_tokens, draft_len, stream);
+    L.v_begin = v_begin;
+    L.G = G;
+    L.shard = shard;
+    L.u_resample = u_resample;
+    L.mass_in = mass_all;
+    L.accepted_len = accepted_len;
+    L.out_tokens = out_tokens;
+    L.reject_mask = reject_mask;
+    return osd::launch_verify_shard(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "osd.h"
+
 namespace osd {
 
 // Kernel tile shape chosen from V: W threads per workgroup, CPT 16-byte chunks
@@ -143,5 +145,30 @@ hipError_t launch_sample(const SampleLaunch& L);
 // base are 16-byte multiples and whose V fits one of the streaming tiles.
 bool pick_stream_tile(int V, int per_chunk, RowTile* t);
 hipError_t launch_distill_stream(const DistillLaunch& L);
+
+// Vocabulary-sharded verification, one phase per call (1 stats, 2 mass,
+// 3 draw).  Records are the public osd_shard_row_stats / osd_shard_mass.
+struct ShardLaunch {
+    int phase;
+    const void* target;  // this rank's slice [B, K+1, Vs]
+    const void* draft;   // [B, K, Vs]
+    int dtype;
+    int B, K, Vs, v_begin, V, G, shard;
+    const int32_t* tokens;
+    const int32_t* draft_len;
+    const float* u_accept;
+    const float* u_resample;
+    float temperature;
+    osd_shard_row_stats* stats;          // phase 1 out [B, K+1]
+    const osd_shard_row_stats* stats_in;  // phase 2 in [G, B, K+1]
+    osd_shard_mass* mass;                 // phase 2 out [B]
+    const osd_shard_mass* mass_in;        // phase 3 in [G, B]
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    uint8_t* reject_mask;
+    bool vec;
+    hipStream_t stream;
+};
+hipError_t launch_verify_shard(const ShardLaunch& L);
 
 }  // namespace osd

@@ -21,7 +21,10 @@ struct DrawShared {
 // Inverse-CDF draw over a register-resident row pair.  mass(t, d, e) returns
 // the non-negative fp32 mass of element e of the chunks t, d (0 for padding).
 // Returns the drawn token on exactly one thread and -1 on every other thread;
-// *z_zero is set (uniformly) when the total mass is zero.
+// *z_zero is set (uniformly) when the total mass is zero.  The point drawn is
+// floor(u * Z) in fixed point, or, when c_given >= 0, c_given itself (a point
+// already chosen in a larger CDF of which this row is one part); either is
+// clamped to Z - 1.
 //
 // Token order is (round n, wave w, lane, element e).  Chunk masses are summed
 // left to right in fp32 and converted exactly to fixed point, so every partial
@@ -32,7 +35,7 @@ struct DrawShared {
 template <int SH, int W, int CPT, int EPC, typename MassFn>
 __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CPT], MassFn mass,
                                 float u, unsigned long long* s_tot, DrawShared* s_draw,
-                                chunk_t* s_stage, bool* z_zero) {
+                                chunk_t* s_stage, bool* z_zero, long long c_given = -1) {
     constexpr int NW = W / kWave;
     constexpr int CELLS = CPT * NW;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
@@ -53,7 +56,8 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
         z = wave_sum(z);
         if (lane == 0) s_draw->cell_round = -1;
         if (z > 0) {
-            uint64_t c = static_cast<uint64_t>(double(u) * double(z));
+            uint64_t c = c_given >= 0 ? static_cast<uint64_t>(c_given)
+                                      : static_cast<uint64_t>(double(u) * double(z));
             if (c >= z) c = z - 1;
             uint64_t carry = 0;
             for (int base = 0; base < CELLS; base += kWave) {

@@ -163,3 +163,72 @@ def test_binding_sample_fails_loudly_without_gpu_tensors():
     import torch
     with pytest.raises(ValueError):
         osd.osd_sample(torch.zeros(2, 8), None, 1.0, 1.0, torch.zeros(2))
+
+
+# Vocabulary-sharded verification (three phases, one call per rank each).
+FAKE_MISALIGNED = ctypes.c_void_p(0x1004)
+
+
+def shard_stats(**kw):
+    a = dict(t=FAKE, d=FAKE, dtype=1, B=4, K=3, Vs=64, v0=64, V=256, y=FAKE, kl=None, T=0.8, out=FAKE,
+             stream=None)
+    a.update(kw)
+    return osd.lib().osd_shard_verify_stats(a["t"], a["d"], a["dtype"], a["B"], a["K"], a["Vs"], a["v0"], a["V"],
+                                            a["y"], a["kl"], a["T"], a["out"], a["stream"])
+
+
+def shard_mass(**kw):
+    a = dict(t=FAKE, d=FAKE, dtype=1, B=4, K=3, Vs=64, G=4, y=FAKE, kl=None, u=FAKE, T=0.8, stats=FAKE,
+             out=FAKE, stream=None)
+    a.update(kw)
+    return osd.lib().osd_shard_verify_mass(a["t"], a["d"], a["dtype"], a["B"], a["K"], a["Vs"], a["G"], a["y"],
+                                           a["kl"], a["u"], a["T"], a["stats"], a["out"], a["stream"])
+
+
+def shard_draw(**kw):
+    a = dict(t=FAKE, d=FAKE, dtype=1, B=4, K=3, Vs=64, v0=64, G=4, g=1, y=FAKE, kl=None, u=FAKE, T=0.8,
+             mass=FAKE, acc=FAKE, toks=FAKE, rmask=None, stream=None)
+    a.update(kw)
+    return osd.lib().osd_shard_verify_draw(a["t"], a["d"], a["dtype"], a["B"], a["K"], a["Vs"], a["v0"], a["G"],
+                                           a["g"], a["y"], a["kl"], a["u"], a["T"], a["mass"], a["acc"],
+                                           a["toks"], a["rmask"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), -1), (dict(K=0), -1), (dict(K=17), -1), (dict(Vs=0), -1), (dict(dtype=5), -1),
+    (dict(Vs=(1 << 17) + 8, V=1 << 19, v0=0), -2), (dict(V=(1 << 19) + 64), -2),
+    (dict(v0=-1), -1), (dict(v0=200), -1), (dict(V=0), -1),
+    (dict(T=-1.0), -1), (dict(T=float("nan")), -1), (dict(T=float("inf")), -1),
+    (dict(t=None), -1), (dict(d=None), -1), (dict(y=None), -1), (dict(out=None), -1),
+    (dict(out=FAKE_MISALIGNED), -1),  # records must be 8-byte aligned
+])
+def test_shard_stats_rejects_bad_arguments(kw, status):
+    assert shard_stats(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), -1), (dict(K=17), -1), (dict(Vs=(1 << 17) + 8), -2),
+    (dict(G=0), -1), (dict(G=65), -1), (dict(T=-0.5), -1),
+    (dict(t=None), -1), (dict(d=None), -1), (dict(u=None), -1), (dict(stats=None), -1), (dict(out=None), -1),
+    (dict(stats=FAKE_MISALIGNED), -1), (dict(out=FAKE_MISALIGNED), -1),
+])
+def test_shard_mass_rejects_bad_arguments(kw, status):
+    assert shard_mass(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), -1), (dict(K=17), -1), (dict(Vs=(1 << 17) + 8), -2),
+    (dict(G=0), -1), (dict(G=65), -1), (dict(g=-1), -1), (dict(g=4), -1), (dict(v0=-3), -1),
+    (dict(v0=(1 << 19) - 32), -1), (dict(T=float("nan")), -1),
+    (dict(t=None), -1), (dict(d=None), -1), (dict(u=None), -1), (dict(mass=None), -1), (dict(acc=None), -1),
+    (dict(toks=None), -1), (dict(mass=FAKE_MISALIGNED), -1),
+])
+def test_shard_draw_rejects_bad_arguments(kw, status):
+    assert shard_draw(**kw) == status
+
+
+def test_binding_shard_fails_loudly_without_gpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        osd.osd_shard_verify_stats(torch.zeros(2, 3, 8), torch.zeros(2, 2, 8), torch.zeros(2, 2, dtype=torch.int32),
+                                   1.0, 0, 8)
