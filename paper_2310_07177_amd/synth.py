@@ -195,3 +195,53 @@ def config_large_vocab(seed=0, B=256, K=8, V=128256):
                       draft_noise=1.0, ragged=True)
     x.update(kind="fkl", beta=0.5, tau=0.8, mask=None)
     return x
+
+
+def config_large_vocab_device(seed=0, B=256, K=8, V=128256, device="cuda"):
+    """The large-vocabulary workload at its full size, drawn on the GPU with
+    torch's seeded generator (the host generator takes minutes at 0.6 G
+    logits): target ~ N(0, 3^2), draft = target + N(0, 1), both float32
+    normals rounded once to bf16; k_b ~ U{1..8}; proposals by Gumbel-max on
+    the stored draft logits at T = 0.8; float32 uniforms in [0, 1).  Returns
+    device tensors (target and draft bf16, tokens and draft_len int32,
+    uniforms float32) plus the scalar settings; slices of them, copied to the
+    host, are the oracle's inputs."""
+    import torch
+    T = 0.8
+    g = torch.Generator(device=device)
+    g.manual_seed(seed * 16 + SEED_LOGITS)
+    t = torch.randn(B, K + 1, V, generator=g, device=device) * 3.0
+    d = (t[:, :K] + torch.randn(B, K, V, generator=g, device=device)).to(torch.bfloat16)
+    t = t.to(torch.bfloat16)
+    gt = torch.Generator(device=device)
+    gt.manual_seed(seed * 16 + SEED_TOKENS)
+    tokens = torch.empty(B, K, dtype=torch.int32, device=device)
+    for b0 in range(0, B, 32):  # bounded temporaries
+        u = torch.rand(min(32, B - b0), K, V, generator=gt, device=device).clamp_min_(1e-30)
+        gum = -torch.log(-torch.log(u))
+        tokens[b0:b0 + 32] = torch.argmax(d[b0:b0 + 32].float() / T + gum, dim=-1).to(torch.int32)
+    gu = torch.Generator(device=device)
+    gu.manual_seed(seed * 16 + SEED_UNIFORM)
+    u_acc = torch.rand(B, K, generator=gu, device=device)
+    u_res = torch.rand(B, generator=gu, device=device)
+    ga = torch.Generator(device=device)
+    ga.manual_seed(seed * 16 + SEED_AUX)
+    draft_len = torch.randint(1, K + 1, (B,), generator=ga, device=device, dtype=torch.int32)
+    return dict(target=t, draft=d, tokens=tokens, u_accept=u_acc, u_resample=u_res, draft_len=draft_len,
+                T=T, B=B, K=K, V=V, dtype="bf16", kind="fkl", beta=0.5, tau=T)
+
+
+def to_host_sample(x, idx):
+    """Host copies (numpy, bf16 as uint16 bit patterns) of the sequences idx
+    of a device workload, in the layout the oracle takes."""
+    import torch
+    ii = torch.as_tensor(np.asarray(idx), device=x["target"].device)
+
+    def h(t):
+        s = t.index_select(0, ii).contiguous().cpu()
+        if s.dtype == torch.bfloat16:
+            return s.view(torch.int16).numpy().view(np.uint16)
+        return s.numpy()
+    return dict(target=h(x["target"]), draft=h(x["draft"]), tokens=h(x["tokens"]), u_accept=h(x["u_accept"]),
+                u_resample=h(x["u_resample"]), draft_len=h(x["draft_len"]), T=x["T"], B=len(idx), K=x["K"],
+                V=x["V"], dtype=x["dtype"])
