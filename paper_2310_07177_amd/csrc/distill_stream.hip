@@ -168,8 +168,11 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                         st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
                         ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
                         if constexpr (KIND == 2) {
+                            // One floor suffices: with lp finite, a draft
+                            // exponent of -inf clamps lq - lp to -126 and
+                            // gives q = 0, so its terms vanish.
                             c0v[j] = fmaxf(vt, kLogFloor);
-                            c1[r][e] = fmaxf(vs, kLogFloor);
+                            c1[r][e] = vs;
                         } else {
                             c0v[j] = vt - vs;  // log2 of the unnormalised ratio
                             c1[r][e] = KIND == 0 ? vt : vs;

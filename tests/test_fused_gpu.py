@@ -201,3 +201,17 @@ def test_fused_high_acceptance_bonus_rows(osd):
                             loss_atol=1e-6)
     want = np.array([rej.get(b, 8) for b in range(64)])
     assert np.array_equal(acc, want)
+
+
+@pytest.mark.parametrize("side", ["draft", "target"])
+def test_fused_jsd_one_sided_neg_inf(osd, side):
+    """-inf logits in the draft rows only (q = 0 where p > 0) or in the target
+    rows only, with JSD distillation of every row: verification and the
+    divergence agree with the oracle."""
+    x = synth.verify_inputs(6, 4, 6000, "bf16", T=1.0, seed=31, target_std=2.0, draft_noise=1.0)
+    g = np.random.default_rng(37)
+    holes = g.random(x[side].shape) < 0.25
+    x[side][holes] = 0xFF80
+    x["tokens"] = synth.gumbel_max_tokens(synth.rng(8), x["draft"], 1.0)
+    mask = np.ones((6, 4), np.uint8)
+    check_fused(osd, x, "jsd", 0.5, mask, f"fused one-sided -inf ({side})")

@@ -360,3 +360,23 @@ def test_distill_neg_inf_entries(osd, kind, dtype):
     _, _, grad = check_distill(osd, tt, ss, kind, 0.5, 0.9, mask, f"-inf {kind} {dtype}")
     gg = synth.bf16_to_f32(grad) if dtype == "bf16" else grad
     assert np.all(gg[holes] == 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("side", ["student", "teacher"])
+def test_distill_jsd_one_sided_neg_inf(osd, side, dtype):
+    """-inf logits on one side only (q = 0 where p > 0, or the reverse): JSD
+    stays finite (its mixture keeps both logs finite) and the oracle's terms
+    with a zero probability vanish; the kernel must agree."""
+    g = np.random.default_rng(23 if side == "student" else 29)
+    B, K, V = 3, 4, 5000
+    t = g.normal(0, 2, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    holes = g.random((B, K, V)) < 0.25
+    (s if side == "student" else t)[holes] = -np.inf
+    mask = np.ones((B, K), np.uint8)
+    tt, ss = (synth.to_bf16(t), synth.to_bf16(s)) if dtype == "bf16" else (t, s)
+    _, _, grad = check_distill(osd, tt, ss, "jsd", 0.5, 0.9, mask, f"one-sided -inf ({side}) {dtype}")
+    if side == "student":
+        gg = synth.bf16_to_f32(grad) if dtype == "bf16" else grad
+        assert np.all(gg[holes] == 0)  # q = 0 there
