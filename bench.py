@@ -20,7 +20,9 @@ more than one batch would: one call's last workgroups then overlap the next
 call's first loads.  The same steps one after another on one stream are
 timed too and reported beside it.  Each entry point is also timed alone the same way (HIP events on the
 stream the kernels run on) to report its achieved HBM bandwidth against the
-8 TB/s peak.  The CPU baseline is the fp64 oracle on the host.
+8 TB/s peak.  One rank's share of the vocabulary-sharded verification
+(B = 256, V = 128256 over 8 ranks) is timed as well and reported under
+"sharded_verify".  The CPU baseline is the fp64 oracle on the host.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -153,9 +155,18 @@ def cpu_baseline():
         el = time.perf_counter() - t0
         if el > 10.0 or reps >= 60:
             break
+    model = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": reps * B * K / el, "unit": "positions/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} full batch(es) of B=64 k=8 V=32128 bf16 (verify T=0.7 + JSD "
-                      f"beta=0.5 tau=0.7 with gradient), {el:.1f} s single-threaded fp64"}
+                      f"beta=0.5 tau=0.7 with gradient), {el:.1f} s single-threaded fp64 on one core "
+                      f"of {os.cpu_count()} ({model})"}
 
 
 def main():
@@ -338,17 +349,22 @@ def main():
                 fn(r)
         return g
 
-    def time_graph(g, iters):
-        """Replay g once untimed, then once between events; ms per iteration."""
+    def time_graph(g, iters, reps=5):
+        """Replay g once untimed, then `reps` times between events; the median
+        ms per iteration."""
         with torch.cuda.stream(stream):
             g.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            g.replay()
-            e1.record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters
+        times = []
+        for _ in range(reps):
+            with torch.cuda.stream(stream):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / iters)
+        return sorted(times)[len(times) // 2]
 
     def time_loop(fn, iters):
         with torch.cuda.stream(stream):
@@ -417,14 +433,18 @@ def main():
 
     replay_all()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(main)
-    replay_all()
-    e1.record(main)
-    torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
-    print(f"# timed {args.steps} steps on {nstr} stream(s): {ms_step * 1e3:.2f} us/step",
-          file=sys.stderr, flush=True)
+    # Exactly K steps between the events, five times; the median is reported.
+    step_times = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main)
+        replay_all()
+        e1.record(main)
+        torch.cuda.synchronize()
+        step_times.append(e0.elapsed_time(e1) / args.steps)
+    ms_step = sorted(step_times)[2]
+    print(f"# timed {args.steps} steps on {nstr} stream(s), 5 repetitions: median {ms_step * 1e3:.2f} us/step "
+          f"(range {min(step_times) * 1e3:.2f}-{max(step_times) * 1e3:.2f})", file=sys.stderr, flush=True)
     ms_one = time_graph(capture(step, args.steps), args.steps) if nstr > 1 else ms_step
     print(f"# the same steps one after another on one stream: {ms_one * 1e3:.2f} us/step",
           file=sys.stderr, flush=True)
