@@ -206,3 +206,61 @@ def test_concurrent_calls_on_two_streams():
             for k, want in zip(keys, alone[i]):
                 assert torch.equal(s[k], want), f"rep {rep} set {i} {k}"
     assert all(int(w.count_nonzero()) == 0 for w in wss)
+
+
+def test_graph_replays_match_eager_sharded():
+    """The three phases of the vocabulary-sharded verification for 4 ranks
+    (12 calls, the exchanges being the shared record arrays) captured once
+    and replayed; each replay equals the eager result."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    dev = torch.device("cuda:0")
+    L = binding.lib()
+    B, K, V, G = 16, 5, 8192, 4
+    Vs = V // G
+    x = synth.verify_inputs(B, K, V, "bf16", T=0.8, seed=7, target_std=2.5, draft_noise=1.0, ragged=True)
+    t, d = _dev(x["target"], dev), _dev(x["draft"], dev)
+    tg = [t[:, :, g * Vs:(g + 1) * Vs].contiguous() for g in range(G)]
+    dg = [d[:, :, g * Vs:(g + 1) * Vs].contiguous() for g in range(G)]
+    y, kl = _dev(x["tokens"].astype(np.int32), dev), _dev(x["draft_len"], dev)
+    ua, ur = _dev(x["u_accept"], dev), _dev(x["u_resample"], dev)
+    stats = torch.zeros(G, B, K + 1, binding.SHARD_ROW_STATS_BYTES, dtype=torch.uint8, device=dev)
+    mass = torch.zeros(G, B, binding.SHARD_MASS_BYTES, dtype=torch.uint8, device=dev)
+    acc = torch.empty(G, B, dtype=torch.int32, device=dev)
+    toks = torch.empty(G, B, K + 1, dtype=torch.int32, device=dev)
+    rm = torch.empty(G, B, K, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.Stream(dev)
+    stream.wait_stream(torch.cuda.current_stream(dev))
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    torch.cuda.synchronize()
+    P = lambda a: ctypes.c_void_p(a.data_ptr())
+    cT = ctypes.c_float(x["T"])
+
+    def step():
+        for g in range(G):
+            assert L.osd_shard_verify_stats(P(tg[g]), P(dg[g]), binding.OSD_BF16, B, K, Vs, g * Vs, V, P(y), P(kl),
+                                            cT, P(stats[g]), hs) == 0
+        for g in range(G):
+            assert L.osd_shard_verify_mass(P(tg[g]), P(dg[g]), binding.OSD_BF16, B, K, Vs, G, P(y), P(kl), P(ua),
+                                           cT, P(stats), P(mass[g]), hs) == 0
+        for g in range(G):
+            assert L.osd_shard_verify_draw(P(tg[g]), P(dg[g]), binding.OSD_BF16, B, K, Vs, g * Vs, G, g, P(y), P(kl),
+                                           P(ur), cT, P(mass), P(acc[g]), P(toks[g]), P(rm[g]), hs) == 0
+
+    with torch.cuda.stream(stream):
+        step()
+    torch.cuda.synchronize()
+    eager = [a.clone() for a in (stats, mass, acc, toks, rm)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        step()
+    for rep in range(3):
+        for a in (stats, mass, acc, toks, rm):
+            a.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            g.replay()
+        torch.cuda.synchronize()
+        for e, o in zip(eager, (stats, mass, acc, toks, rm)):
+            assert torch.equal(e, o), f"replay {rep}"
