@@ -42,6 +42,9 @@ struct BF16 {
     __device__ static inline float load_one(const void* row, int j) {
         return __uint_as_float(uint32_t(static_cast<const uint16_t*>(row)[j]) << 16);
     }
+    // The bits of element j, and their value (a load kept apart from its use).
+    __device__ static inline uint32_t load_raw(const void* row, int j) { return static_cast<const uint16_t*>(row)[j]; }
+    __device__ static inline float from_raw(uint32_t r) { return __uint_as_float(r << 16); }
     __device__ static inline chunk_t load_scalar(const void* row, int64_t first, int V) {
         const uint16_t* p = static_cast<const uint16_t*>(row);
         uint16_t v[8];
@@ -66,6 +69,8 @@ struct F32 {
     __device__ static inline float load_one(const void* row, int j) {
         return static_cast<const float*>(row)[j];
     }
+    __device__ static inline uint32_t load_raw(const void* row, int j) { return static_cast<const uint32_t*>(row)[j]; }
+    __device__ static inline float from_raw(uint32_t r) { return __uint_as_float(r); }
     __device__ static inline chunk_t load_scalar(const void* row, int64_t first, int V) {
         const float* p = static_cast<const float*>(row);
         uint32_t v[4];
@@ -87,21 +92,68 @@ __device__ inline chunk_t pad_chunk() {
 
 // Load the CPT chunks of one row owned by this thread.  VEC: the row is
 // 16-byte aligned and V is a multiple of the chunk size.
+// VEC loads are issued without branches (a chunk past the row reloads the
+// row's last chunk and is replaced by padding): with every load in one basic
+// block the compiler waits for exactly the chunk a sweep consumes next, so
+// the statistics fold in as the loads land instead of after the last one.
 template <typename Fmt, int W, int CPT, bool VEC>
 __device__ inline void load_row(chunk_t (&c)[CPT], const void* row, int V) {
     const int nchunks = (V + Fmt::kPerChunk - 1) / Fmt::kPerChunk;
 #pragma unroll
     for (int n = 0; n < CPT; ++n) {
         const int ch = n * W + static_cast<int>(threadIdx.x);
-        if (ch < nchunks) {
-            if constexpr (VEC)
-                c[n] = __builtin_nontemporal_load(static_cast<const chunk_t*>(row) + ch);
-            else
-                c[n] = Fmt::load_scalar(row, int64_t(ch) * Fmt::kPerChunk, V);
+        if constexpr (VEC) {
+            const bool in = ch < nchunks;
+            const chunk_t v = __builtin_nontemporal_load(static_cast<const chunk_t*>(row) + (in ? ch : nchunks - 1));
+            const chunk_t pad = pad_chunk<Fmt>();
+            c[n] = chunk_t{in ? v.x : pad.x, in ? v.y : pad.y, in ? v.z : pad.z, in ? v.w : pad.w};
         } else {
-            c[n] = pad_chunk<Fmt>();
+            c[n] = ch < nchunks ? Fmt::load_scalar(row, int64_t(ch) * Fmt::kPerChunk, V) : pad_chunk<Fmt>();
         }
     }
+}
+
+// The loads of load_row<VEC> without the padding: a chunk past the row
+// re-reads the row's last chunk and stays as loaded.  Consumers apply the
+// padding where they use a chunk (row_stats_tail, pad_row_tail), so no
+// instruction right after the loads needs their data and each sweep waits
+// only for the chunk it takes next.
+template <int W, int CPT>
+__device__ inline void load_row_clamped(chunk_t (&c)[CPT], const void* row, int nchunks) {
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const int ch = n * W + static_cast<int>(threadIdx.x);
+        c[n] = __builtin_nontemporal_load(static_cast<const chunk_t*>(row) + (ch < nchunks ? ch : nchunks - 1));
+    }
+}
+
+// Two rows loaded as load_row_clamped loads each, chunk by chunk in turn
+// (a0, b0, a1, b1, ...), the order in which row_stats2_tail takes them.
+template <int W, int CPT>
+__device__ inline void load_rows_interleaved(chunk_t (&a)[CPT], chunk_t (&b)[CPT], const void* ra, const void* rb,
+                                             int nchunks) {
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const int ch = n * W + static_cast<int>(threadIdx.x);
+        const int cl = ch < nchunks ? ch : nchunks - 1;
+        a[n] = __builtin_nontemporal_load(static_cast<const chunk_t*>(ra) + cl);
+        b[n] = __builtin_nontemporal_load(static_cast<const chunk_t*>(rb) + cl);
+    }
+}
+
+// Chunk n of this thread, or padding if it lies past the row.
+template <typename Fmt, int W>
+__device__ inline chunk_t chunk_or_pad(const chunk_t& c, int n, int nchunks) {
+    const bool in = n * W + static_cast<int>(threadIdx.x) < nchunks;
+    const chunk_t pad = pad_chunk<Fmt>();
+    return chunk_t{in ? c.x : pad.x, in ? c.y : pad.y, in ? c.z : pad.z, in ? c.w : pad.w};
+}
+
+// Replace the chunks of load_row_clamped that lie past the row by padding.
+template <typename Fmt, int W, int CPT>
+__device__ inline void pad_row_tail(chunk_t (&c)[CPT], int nchunks) {
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) c[n] = chunk_or_pad<Fmt, W>(c[n], n, nchunks);
 }
 
 // Make register-resident chunks opaque to the optimiser at the start of a
@@ -270,6 +322,63 @@ __device__ inline void row_stats(const chunk_t (&c)[CPT], float c2, float& K, fl
             for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
         S = S + e8[0];
         __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
+    }
+}
+
+// row_stats over chunks from load_row_clamped: each chunk is padded as the
+// sweep takes it (after its load has landed).
+template <typename Fmt, int W, int CPT>
+__device__ inline void row_stats_tail(const chunk_t (&c)[CPT], int nchunks, float c2, float& K, float& S) {
+    constexpr int EPC = Fmt::kPerChunk;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+        const chunk_t x = chunk_or_pad<Fmt, W>(c[n], n, nchunks);
+        const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(x) * c2));
+        S = rescale(S, K, kn);
+        K = kn;
+        const float kx = fmaxf(K, -3.0e38f);  // see row_stats
+        float e8[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(x, e), c2, -kx));
+#pragma unroll
+        for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+            for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+        S = S + e8[0];
+        __builtin_amdgcn_sched_barrier(0);  // one chunk in flight: bounded VGPRs
+    }
+}
+
+// Two rows from load_rows_interleaved swept together: chunk n of both rows
+// in iteration n, in the order the loads were issued, each row folded exactly
+// as row_stats_tail folds it.  With second == false only the first row is
+// folded (its partner's loads are ignored).
+template <typename Fmt, int W, int CPT>
+__device__ inline void row_stats2_tail(const chunk_t (&a)[CPT], const chunk_t (&b)[CPT], int nchunks, float c2,
+                                       bool second, float& Ka, float& Sa, float& Kb, float& Sb) {
+    constexpr int EPC = Fmt::kPerChunk;
+#pragma unroll
+    for (int n = 0; n < CPT; ++n) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            if (r == 1 && !second) continue;
+            const chunk_t x = chunk_or_pad<Fmt, W>(r == 0 ? a[n] : b[n], n, nchunks);
+            float& K = r == 0 ? Ka : Kb;
+            float& S = r == 0 ? Sa : Sb;
+            const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(x) * c2));
+            S = rescale(S, K, kn);
+            K = kn;
+            const float kx = fmaxf(K, -3.0e38f);  // see row_stats
+            float e8[EPC];
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(x, e), c2, -kx));
+#pragma unroll
+            for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+                for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+            S = S + e8[0];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one chunk pair in flight: bounded VGPRs
     }
 }
 

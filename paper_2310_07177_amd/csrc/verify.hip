@@ -201,8 +201,29 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(V
 
     const char* trow = static_cast<const char*>(a.target) +
                        (int64_t(b) * (K + 1) + i) * int64_t(V) * Fmt::kBytes;
+    // A bonus row has no draft row: its draft loads re-read the target row
+    // (ignored), so that every workgroup issues the same loads without a
+    // branch and the compiler can wait for each chunk exactly.
+    const char* drow = GREEDY || bonus
+                           ? trow
+                           : static_cast<const char*>(a.draft) + (int64_t(b) * K + i) * int64_t(V) * Fmt::kBytes;
+    // The logits of the proposal itself, for the acceptance test, requested
+    // before the rows and converted only after the statistics: loads complete
+    // in issue order, so a value used early that was loaded after the rows
+    // would make the sweeps wait for the whole row pair.
+    uint32_t ty_raw = 0u, dy_raw = 0u;
+    if constexpr (!GREEDY) {
+        ty_raw = Fmt::load_raw(trow, bonus ? 0 : y);
+        dy_raw = Fmt::load_raw(drow, bonus ? 0 : y);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // Sampling with 16-byte rows: the rows are loaded without padding and the
+    // statistics pad each chunk as they take it, so they fold in as the
+    // loads land; the register copy is padded afterwards for the draw.
+    constexpr bool kFold = VEC && !GREEDY;
+    const int nchunks = (V + EPC - 1) / EPC;
     chunk_t tv[CPT];
-    load_row<Fmt, W, CPT, VEC>(tv, trow, V);
+    if constexpr (!kFold) load_row<Fmt, W, CPT, VEC>(tv, trow, V);
 
     if constexpr (GREEDY) {
         // Target argmax, lowest index on ties: within a thread indices grow
@@ -247,22 +268,23 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(V
         const float c2 = a.c2;
         // The draft row is read only for proposal rows.
         chunk_t dv[CPT];
-        const char* drow = static_cast<const char*>(a.draft) +
-                           (int64_t(b) * K + i) * int64_t(V) * Fmt::kBytes;
-        if (!bonus) load_row<Fmt, W, CPT, VEC>(dv, drow, V);
-        // The logits of the proposal itself, for the acceptance test.
-        float ty = 0.0f, dy = 0.0f;
-        if (!bonus) {
-            ty = Fmt::load_one(trow, y);
-            dy = Fmt::load_one(drow, y);
-        }
+        if constexpr (kFold)
+            load_rows_interleaved<W, CPT>(tv, dv, trow, drow, nchunks);
+        else
+            load_row<Fmt, W, CPT, VEC>(dv, drow, V);
 
         // Row statistics (K, S), folded in chunk by chunk as the loads land.
         float Kt = kNegInf, Kd = kNegInf;
         {
             float st = 0.0f, sd = 0.0f;
-            row_stats<Fmt, CPT>(tv, c2, Kt, st);
-            if (!bonus) row_stats<Fmt, CPT>(dv, c2, Kd, sd);
+            if constexpr (kFold) {
+                row_stats2_tail<Fmt, W, CPT>(tv, dv, nchunks, c2, !bonus, Kt, st, Kd, sd);
+                pad_row_tail<Fmt, W, CPT>(tv, nchunks);
+                pad_row_tail<Fmt, W, CPT>(dv, nchunks);
+            } else {
+                row_stats<Fmt, CPT>(tv, c2, Kt, st);
+                if (!bonus) row_stats<Fmt, CPT>(dv, c2, Kd, sd);
+            }
             double dt = st, dd = sd;
             wave_merge_stats(Kt, dt);
             wave_merge_stats(Kd, dd);
@@ -301,6 +323,8 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(V
                 // Acceptance test: p(y)/q(y) = 2^e * S_d / S_t with
                 // e = (t_y c2 - K_t) - (d_y c2 - K_d) in fp64; 2^e is split
                 // into an exact power of two and 2^frac (v_exp_f32, 1 ulp).
+                asm volatile("" : "+v"(ty_raw), "+v"(dy_raw));  // converted here, not at the load
+                const float ty = Fmt::from_raw(ty_raw), dy = Fmt::from_raw(dy_raw);
                 const double e = (double(ty) * a.c2d - double(Kt)) - (double(dy) * a.c2d - double(Kd));
                 double ratio;
                 if (!(e > -2000.0)) {
