@@ -53,8 +53,19 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void sample_kernel(S
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const int n = blockIdx.x;
     chunk_t tv[CPT], dv[CPT];
-    load_row<Fmt, W, CPT, VEC>(tv, a.p + int64_t(n) * a.p_stride, a.V);
-    if constexpr (MIX) load_row<Fmt, W, CPT, VEC>(dv, a.q + int64_t(n) * a.q_stride, a.V);
+    // Sampling from 16-byte rows: loads without padding (a row pair
+    // interleaved chunk by chunk), so that the statistics fold in as they
+    // land; the register copy is padded afterwards for the draw.
+    constexpr bool kFold = VEC && MODE != kModeGreedy;
+    const int nchunks = (a.V + EPC - 1) / EPC;
+    if constexpr (kFold && MIX) {
+        load_rows_interleaved<W, CPT>(tv, dv, a.p + int64_t(n) * a.p_stride, a.q + int64_t(n) * a.q_stride, nchunks);
+    } else if constexpr (kFold) {
+        load_row_clamped<W, CPT>(tv, a.p + int64_t(n) * a.p_stride, nchunks);
+    } else {
+        load_row<Fmt, W, CPT, VEC>(tv, a.p + int64_t(n) * a.p_stride, a.V);
+        if constexpr (MIX) load_row<Fmt, W, CPT, VEC>(dv, a.q + int64_t(n) * a.q_stride, a.V);
+    }
 
     if constexpr (MODE == kModeGreedy) {
         // Argmax, lowest index on ties: within a thread indices grow with
@@ -93,8 +104,17 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void sample_kernel(S
         float Kp = kNegInf, Kq = kNegInf;
         {
             float sp = 0.0f, sq = 0.0f;
-            row_stats<Fmt, CPT>(tv, c2, Kp, sp);
-            if constexpr (MIX) row_stats<Fmt, CPT>(dv, c2, Kq, sq);
+            if constexpr (kFold && MIX) {
+                row_stats2_tail<Fmt, W, CPT>(tv, dv, nchunks, c2, true, Kp, sp, Kq, sq);
+                pad_row_tail<Fmt, W, CPT>(tv, nchunks);
+                pad_row_tail<Fmt, W, CPT>(dv, nchunks);
+            } else if constexpr (kFold) {
+                row_stats_tail<Fmt, W, CPT>(tv, nchunks, c2, Kp, sp);
+                pad_row_tail<Fmt, W, CPT>(tv, nchunks);
+            } else {
+                row_stats<Fmt, CPT>(tv, c2, Kp, sp);
+                if constexpr (MIX) row_stats<Fmt, CPT>(dv, c2, Kq, sq);
+            }
             double dp = sp, dq = sq;
             wave_merge_stats(Kp, dp);
             if constexpr (MIX) wave_merge_stats(Kq, dq);
