@@ -232,3 +232,40 @@ def test_shard_deterministic_and_reusable(osd):
     b = run_sharded(osd, x, even_bounds(32128, 8))
     for u, v in zip(a, b):
         assert np.array_equal(u, v)
+
+
+def test_shard_gap_in_slices_invalidates_the_sequence(osd):
+    """Slices that do not cover the vocabulary (a caller's mistake the host
+    cannot see): a sequence is invalid (-1) when the test reaches a proposal
+    that no rank holds; sequences whose tested proposals all lie inside the
+    slices are still verified exactly like the whole rows (the oracle), as
+    long as the residual draw does not need the missing columns.  Nothing
+    faults."""
+    import torch
+    B, K, V = 16, 3, 3000
+    x = synth.verify_inputs(B, K, V, "f32", T=1.0, seed=51, target_std=2.0, draft_noise=1.0)
+    # the gap [1000, 1100) holds no probability in either row, so the draws
+    # of the whole rows and of the covered slices coincide
+    x["target"][:, :, 1000:1100] = -np.inf
+    x["draft"][:, :, 1000:1100] = -np.inf
+    x["tokens"] = synth.gumbel_max_tokens(synth.rng(9), x["draft"], 1.0)
+    x["tokens"][:4, 0] = 1050  # proposals inside the gap (p = q = 0 there)
+    slices = [(0, 1000), (1100, 3000)]
+    t, d = to_device(x["target"]), to_device(x["draft"])
+    y = to_device(x["tokens"].astype(np.int32))
+    ua, ur = to_device(x["u_accept"]), to_device(x["u_resample"])
+    tg = [t[:, :, a:e].contiguous() for a, e in slices]
+    dg = [d[:, :, a:e].contiguous() for a, e in slices]
+    G = len(slices)
+    st = torch.stack([osd.osd_shard_verify_stats(tg[g], dg[g], y, 1.0, slices[g][0], V) for g in range(G)])
+    ms = torch.stack([osd.osd_shard_verify_mass(tg[g], dg[g], y, ua, 1.0, st) for g in range(G)])
+    outs = [osd.osd_shard_verify_draw(tg[g], dg[g], y, ur, 1.0, slices[g][0], g, ms) for g in range(G)]
+    toks = torch.stack([o[1] for o in outs]).amax(0).cpu().numpy()
+    acc = outs[0][0].cpu().numpy()
+    torch.cuda.synchronize()
+    assert acc[:4].tolist() == [-1] * 4 and (toks[:4] == -1).all()
+    r = oracle_verify(x)
+    ok = np.arange(B) >= 4
+    n, ex = compare_verify({k: (v[ok] if isinstance(v, np.ndarray) else v) for k, v in r.items()},
+                           acc[ok], toks[ok], outs[0][2].cpu().numpy()[ok], "gap in slices")
+    print(f"[gap in slices] compared {n}, excluded {ex}", flush=True)
