@@ -38,7 +38,9 @@ namespace {
 static_assert(sizeof(osd_shard_row_stats) == 40, "record layout");
 static_assert(sizeof(osd_shard_mass) == 48, "record layout");
 
-constexpr int kFixedShift = 44;  // as the whole-row verification: row totals < 2^17 units
+// 2^-44 fixed point, as the whole-row verification: an element's mass is at
+// most 1 unit, so a whole row of V <= 2^19 tokens totals below 2^63.
+constexpr int kFixedShift = 44;
 constexpr int kRecWords = sizeof(osd_shard_row_stats) / 4;
 
 enum : int32_t { kHoldsY = 1, kBadToken = 2 };
