@@ -232,3 +232,22 @@ def test_binding_shard_fails_loudly_without_gpu_tensors():
     with pytest.raises(ValueError):
         osd.osd_shard_verify_stats(torch.zeros(2, 3, 8), torch.zeros(2, 2, 8), torch.zeros(2, 2, dtype=torch.int32),
                                    1.0, 0, 8)
+
+
+def test_shard_record_layout_matches_header(tmp_path):
+    """The record sizes and field offsets the binding and the tests assume are
+    the ones a C compiler gives the structs declared in include/osd.h."""
+    import subprocess
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "osd.h"\n'
+        "int main(void) {\n"
+        '  printf("%zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(osd_shard_row_stats), sizeof(osd_shard_mass),\n'
+        "         offsetof(osd_shard_row_stats, k_target), offsetof(osd_shard_row_stats, argmax),\n"
+        "         offsetof(osd_shard_row_stats, flags), offsetof(osd_shard_mass, s_target),\n"
+        "         offsetof(osd_shard_mass, accepted), offsetof(osd_shard_mass, token));\n"
+        "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()]
+    assert got == [binding.SHARD_ROW_STATS_BYTES, binding.SHARD_MASS_BYTES, 16, 32, 36, 16, 40, 44]
