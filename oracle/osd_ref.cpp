@@ -86,8 +86,12 @@ bool temperature_softmax(const std::vector<double>& z, double T,
  * the smallest j whose running sum C_j exceeds c = u * Z, walking ascending
  * token ids.  If rounding leaves c at or beyond the last running sum, the
  * last token with r_j > 0 is taken.  *margin receives
- * min(C_j - c, c - C_{j-1}), the distance in probability mass from c to the
- * nearer edge of the chosen interval.
+ * min(C_j - c, c - C_{j-1}), the distance from c to the nearer edge of the
+ * chosen interval in absolute probability mass (r_j = max(0, p_j - q_j) or
+ * p_j, so Z <= 1), NOT divided by Z: a kernel that forms these masses in
+ * fp32 errs by an amount of order 1e-7 in absolute mass whatever Z is, so
+ * the absolute distance is the one that says whether such a kernel can land
+ * on the other side of an edge.
  */
 int inverse_cdf(const std::vector<double>& r, double Z, float u,
                 double* margin) {
@@ -353,23 +357,34 @@ extern "C" int osd_ref_distill_loss_grad(const void* teacher,
             } else if (ok) {
                 /* Eq. 3: JSD[beta] = beta KL(p || m) + (1-beta) KL(q || m) with
                  * m = beta p + (1-beta) q (beta weights the teacher).
-                 * d/ds_j = (1-beta) q_j (log q_j - log m_j - KL(q || m)) / tau. */
+                 * d/ds_j = (1-beta) q_j (log q_j - log m_j - KL(q || m)) / tau.
+                 * A term whose weight is 0 is left out rather than multiplied
+                 * by 0: at beta = 1 KL(q || m) = KL(q || p) may be infinite,
+                 * at beta = 0 KL(p || m) = KL(p || q) may be, and 0 * inf is
+                 * not the 0 the printed formula means.  With that reading
+                 * JSD is identically 0 at both ends (m equals the one
+                 * distribution left in the sum). */
+                const double wp = beta, wq = 1.0 - beta;
                 std::vector<double> logM((size_t)V);
                 for (int j = 0; j < V; ++j)
                     logM[(size_t)j] =
-                        std::log(beta * P[(size_t)j] + (1.0 - beta) * Q[(size_t)j]);
+                        std::log(wp * P[(size_t)j] + wq * Q[(size_t)j]);
                 double kl_pm = 0.0, kl_qm = 0.0;
-                for (int j = 0; j < V; ++j)
-                    if (P[(size_t)j] > 0.0)
-                        kl_pm += P[(size_t)j] * (logP[(size_t)j] - logM[(size_t)j]);
-                for (int j = 0; j < V; ++j)
-                    if (Q[(size_t)j] > 0.0)
-                        kl_qm += Q[(size_t)j] * (logQ[(size_t)j] - logM[(size_t)j]);
-                D = beta * kl_pm + (1.0 - beta) * kl_qm;
+                if (wp > 0.0)
+                    for (int j = 0; j < V; ++j)
+                        if (P[(size_t)j] > 0.0)
+                            kl_pm += P[(size_t)j] * (logP[(size_t)j] - logM[(size_t)j]);
+                if (wq > 0.0)
+                    for (int j = 0; j < V; ++j)
+                        if (Q[(size_t)j] > 0.0)
+                            kl_qm += Q[(size_t)j] * (logQ[(size_t)j] - logM[(size_t)j]);
+                D = 0.0;
+                if (wp > 0.0) D += wp * kl_pm;
+                if (wq > 0.0) D += wq * kl_qm;
                 if (g)
                     for (int j = 0; j < V; ++j)
-                        g[j] = Q[(size_t)j] > 0.0
-                                   ? (1.0 - beta) * Q[(size_t)j] *
+                        g[j] = (wq > 0.0 && Q[(size_t)j] > 0.0)
+                                   ? wq * Q[(size_t)j] *
                                          (logQ[(size_t)j] - logM[(size_t)j] - kl_qm) /
                                          tau
                                    : 0.0;
@@ -472,10 +487,6 @@ extern "C" void osd_ref_round_bf16(const double* x, uint16_t* out, int64_t n) {
         std::memcpy(&bits, &f, sizeof bits);
         out[i] = (uint16_t)(bits >> 16);
     }
-}
-
-extern "C" void osd_ref_round_f32(const double* x, float* out, int64_t n) {
-    for (int64_t i = 0; i < n; ++i) out[i] = (float)x[i];
 }
 
 extern "C" void osd_ref_bf16_midpoint_flags(const double* x, uint8_t* flag,

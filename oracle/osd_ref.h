@@ -45,9 +45,10 @@ enum { OSD_REF_FKL = 0, OSD_REF_RKL = 1, OSD_REF_JSD = 2 };
  * reject_mask   out [B, K]   nullable; 1 at i == a_b when a_b < k_b
  * margin_accept out [B, K]   nullable; |u - p(y)/q(y)| for every acceptance
  *                            test actually evaluated, NaN elsewhere
- * margin_cdf    out [B]      nullable; distance, in probability mass, from
- *                            u*Z to the nearer edge of the chosen token's CDF
- *                            interval (NaN for greedy and invalid rows)
+ * margin_cdf    out [B]      nullable; distance, in absolute probability
+ *                            mass (not divided by Z), from u*Z to the nearer
+ *                            edge of the chosen token's CDF interval (NaN for
+ *                            greedy and invalid rows)
  * z_fallback    out [B]      nullable; 1 where a rejection met Z == 0 and the
  *                            sample fell back to p
  */
@@ -107,9 +108,6 @@ int osd_ref_sample(const void* p, int64_t p_stride, const void* q, int64_t q_str
 /* Round fp64 values to bf16 bit patterns, round-to-nearest-even, directly
  * (no intermediate fp32 rounding). */
 void osd_ref_round_bf16(const double* x, uint16_t* out, int64_t n);
-
-/* Round fp64 values to fp32, round-to-nearest-even. */
-void osd_ref_round_f32(const double* x, float* out, int64_t n);
 
 /* flag[i] = 1 where x[i] lies within rel*|x[i]| of a bf16 rounding midpoint,
  * i.e. where a correctly computed fp32 value could legitimately round to

@@ -40,8 +40,6 @@ def lib():
         L.osd_ref_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f64, vp, vp, vp]
         L.osd_ref_round_bf16.restype = None
         L.osd_ref_round_bf16.argtypes = [vp, vp, i64]
-        L.osd_ref_round_f32.restype = None
-        L.osd_ref_round_f32.argtypes = [vp, vp, i64]
         L.osd_ref_bf16_midpoint_flags.restype = None
         L.osd_ref_bf16_midpoint_flags.argtypes = [vp, vp, i64, f64]
         _lib = L
@@ -165,13 +163,6 @@ def round_bf16(x):
     x = np.ascontiguousarray(x, np.float64)
     out = np.empty(x.shape, np.uint16)
     lib().osd_ref_round_bf16(_ptr(x), _ptr(out), x.size)
-    return out
-
-
-def round_f32(x):
-    x = np.ascontiguousarray(x, np.float64)
-    out = np.empty(x.shape, np.float32)
-    lib().osd_ref_round_f32(_ptr(x), _ptr(out), x.size)
     return out
 
 

@@ -91,6 +91,34 @@ def test_jsd_bounds_and_disjoint_supports(beta):
     assert math.isclose(out["row_loss"][0, 0], hb, rel_tol=1e-13)
 
 
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+def test_jsd_is_identically_zero_at_the_endpoints(beta):
+    """Eq. 3 at beta = 1 is KL(p || p) (+ 0 x KL(q || p)), at beta = 0 it is
+    0 x KL(p || q) + KL(q || q): zero, with a zero gradient, whatever p and
+    q are -- also for disjoint supports, where the weight-0 KL is infinite
+    and must be left out rather than multiplied by 0."""
+    t, s = _rows(11, 2, 3, 40, scale=3.0, noise=2.0)
+    out = ref.distill(t, s, "jsd", beta=beta, tau=0.8)
+    assert np.all(np.isfinite(out["row_loss"])) and np.all(np.abs(out["row_loss"]) <= 1e-14)
+    assert np.all(np.isfinite(out["grad"])) and np.all(np.abs(out["grad"]) <= 1e-14)
+    V = 6
+    td = np.full((1, 2, V), -np.inf)
+    sd = np.full((1, 2, V), -np.inf)
+    td[0, :, :3] = [0.0, 1.0, 2.0]
+    sd[0, :, 2:] = [0.5, -1.0, 0.0, 3.0]      # overlapping support (token 2)
+    sd[0, 1, 2] = -np.inf                     # row 1: disjoint supports
+    out = ref.distill(td, sd, "jsd", beta=beta)
+    assert np.all(np.isfinite(out["row_loss"])) and np.all(np.abs(out["row_loss"]) <= 1e-14)
+    assert np.all(np.isfinite(out["grad"])) and np.all(np.abs(out["grad"]) <= 1e-14)
+    assert out["loss_sum"] == 0.0 or abs(out["loss_sum"]) <= 1e-14
+    # just inside the endpoints the divergence is small and positive, bounded
+    # by H(beta') (disjoint supports reach the bound)
+    bp = 1e-6 if beta == 0.0 else 1 - 1e-6
+    hb = -bp * math.log(bp) - (1 - bp) * math.log(1 - bp)
+    near = ref.distill(td, sd, "jsd", beta=bp)["row_loss"][0]
+    assert 0 < near[0] < hb and math.isclose(near[1], hb, rel_tol=1e-9)
+
+
 @pytest.mark.parametrize("tau", [1.0, 0.5])
 def test_bernoulli_closed_forms(tau):
     """V = 2: the softmax is a logistic sigmoid and KL is the textbook

@@ -42,6 +42,26 @@ MUTATIONS = {
     "sample_mixture_weights_swapped": ("if (use_p) w += beta * P[(size_t)j];",
                                        "if (use_p) w += (1.0 - beta) * P[(size_t)j];"),
     "sample_temperature_ignored": ("const double temp = (double)temperature;", "const double temp = 1.0;"),
+    "jsd_endpoint_zero_times_inf": ("""                if (wp > 0.0)
+                    for (int j = 0; j < V; ++j)
+                        if (P[(size_t)j] > 0.0)
+                            kl_pm += P[(size_t)j] * (logP[(size_t)j] - logM[(size_t)j]);
+                if (wq > 0.0)
+                    for (int j = 0; j < V; ++j)
+                        if (Q[(size_t)j] > 0.0)
+                            kl_qm += Q[(size_t)j] * (logQ[(size_t)j] - logM[(size_t)j]);
+                D = 0.0;
+                if (wp > 0.0) D += wp * kl_pm;
+                if (wq > 0.0) D += wq * kl_qm;""",
+                                    """                for (int j = 0; j < V; ++j)
+                    if (P[(size_t)j] > 0.0)
+                        kl_pm += P[(size_t)j] * (logP[(size_t)j] - logM[(size_t)j]);
+                for (int j = 0; j < V; ++j)
+                    if (Q[(size_t)j] > 0.0)
+                        kl_qm += Q[(size_t)j] * (logQ[(size_t)j] - logM[(size_t)j]);
+                D = wp * kl_pm + wq * kl_qm;"""),
+    "jsd_endpoint_grad_weight_ignored": ("g[j] = (wq > 0.0 && Q[(size_t)j] > 0.0)", "g[j] = (Q[(size_t)j] > 0.0)"),
+    "cdf_margin_divided_by_z": ("*margin = a < b ? a : b;", "*margin = (a < b ? a : b) / Z;"),
     "sample_row_stride_ignored": ("temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), temp, Q, logQ)",
                                   "temperature_softmax(load_row(q, dtype, (int64_t)n * V, V), temp, Q, logQ)"),
 }

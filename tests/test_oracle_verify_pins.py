@@ -247,6 +247,24 @@ def test_acceptance_threshold_is_probability_ratio():
     assert abs(out["margin_cdf"][0] - 0.0) < 1e-12  # u_res = 0 sits on the lower edge
 
 
+def test_residual_margin_is_absolute_mass():
+    """After a rejection the residual max(0, p - q) has total Z < 1, and the
+    recorded CDF margin is the distance from u*Z to the nearer edge of the
+    drawn token's interval in probability mass, not divided by Z.  Hand
+    case: p = (0.5, 0.1, 0.4), q = (0.3, 0.5, 0.2), proposal 1 (ratio 0.2)
+    rejected; r = (0.2, 0, 0.2), Z = 0.4."""
+    t = np.log(np.array([[[0.5, 0.1, 0.4], [1 / 3, 1 / 3, 1 / 3]]]))
+    d = np.log(np.array([[[0.3, 0.5, 0.2]]]))
+    y = np.array([[1]], np.int32)
+    for u, tok, lo, hi in [(0.3, 0, 0.0, 0.2), (0.55, 2, 0.2, 0.4), (0.125, 0, 0.0, 0.2)]:
+        uf = float(np.float32(u))
+        out = ref.verify(t, d, y, np.array([[0.9]], np.float32), np.array([uf], np.float32), 1.0)
+        assert out["accepted_len"][0] == 0 and out["reject_mask"][0, 0] == 1
+        assert out["out_tokens"][0].tolist() == [tok, -1]
+        c = uf * 0.4
+        assert abs(out["margin_cdf"][0] - min(hi - c, c - lo)) < 1e-12, (u, out["margin_cdf"][0])
+
+
 def test_greedy_is_argmax_chain():
     """T = 0: accept while the proposal equals the target argmax (numpy's
     argmax, which also breaks ties towards the lowest index)."""
