@@ -246,6 +246,7 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
         // rounding of the (much larger) constants themselves.
         const float dk = float(ktd - ksd);
         const float beta = a.beta, omb = 1.0f - a.beta;
+        const bool q_only = a.beta == 0.0f;  // JSD at beta = 0: m = q, log2(q/m) = 0
         const float ln2 = float(kLn2);
 
         // Divergence terms, in log2 units.
@@ -280,7 +281,7 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
                     const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
                     const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
                     c0 = __builtin_fmaf(p, -L, c0);
-                    c1 = __builtin_fmaf(q, d - L, c1);
+                    c1 = __builtin_fmaf(q, q_only ? 0.0f : d - L, c1);  // log2(q/m); m = q at beta = 0
                 }
                 if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);  // 4 elements in flight
             }
@@ -335,7 +336,7 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
                         } else {
                             // log2(q/m), as in the loss pass
                             const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
-                            lr = d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                            lr = q_only ? 0.0f : d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
                         }
                         g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
                     }

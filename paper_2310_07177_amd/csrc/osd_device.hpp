@@ -417,6 +417,10 @@ __device__ inline void wave_merge_stats(float& K, Acc& S) {
 // to floor(x * 2^SH); the conversion is exact for x >= 2^(23-SH) (the
 // mantissa is shifted, not rounded).  Integer sums of such values are
 // associative, so every reduction order partitions a CDF identically.
+// Values outside the domain never shift by 64 or more: negatives and
+// subnormals give 0, and anything at or above 2^(63-SH) -- infinities and
+// NaN included -- saturates at 2^39 * (2^24 - 1) < 2^63.  (Callers reject
+// rows whose sums are not finite before they draw, so none reaches a draw.)
 // ---------------------------------------------------------------------------
 template <int SH>
 __device__ inline uint64_t mass_to_fixed(float x) {
@@ -424,11 +428,16 @@ __device__ inline uint64_t mass_to_fixed(float x) {
     const int e = int((b >> 23) & 0xFF) - 127;
     if (e < -126 || (b >> 31)) return 0;  // zero, subnormal or negative
     const uint64_t m = uint64_t((b & 0x7FFFFFu) | 0x800000u);
-    const int sh = e + SH - 23;  // x * 2^SH = m * 2^(e - 23 + SH)
+    int sh = e + SH - 23;  // x * 2^SH = m * 2^(e - 23 + SH)
+    if (sh > 39) sh = 39;  // beyond the domain: saturate below 2^63
     if (sh >= 0) return m << sh;
     if (sh <= -64) return 0;
     return m >> (-sh);
 }
+
+// A row's sum of exponentials that a draw or a test can use: positive and
+// finite (a NaN logit makes it NaN, an overflow makes it infinite).
+__device__ inline bool usable_sum(double s) { return s > 0.0 && s < 1.0e300; }
 
 // Two fp32 values to a packed pair of bf16, round to nearest even, with the
 // native v_cvt_pk_bf16_f32 of gfx950.

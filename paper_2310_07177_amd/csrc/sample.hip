@@ -139,7 +139,8 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void sample_kernel(S
             Sp += rescale(s_sum[0][w], s_max[0][w], Kp);
             if constexpr (MIX) Sq += rescale(s_sum[1][w], s_max[1][w], Kq);
         }
-        const bool bad = !(Kp > kNegInf && Kp < -kNegInf) || (MIX && !(Kq > kNegInf && Kq < -kNegInf));
+        const bool bad = !(Kp > kNegInf && Kp < -kNegInf) || !usable_sum(Sp) ||
+                         (MIX && (!(Kq > kNegInf && Kq < -kNegInf) || !usable_sum(Sq)));
         if (bad) {
             if (tid == 0) a.out[n] = -1;
             return;

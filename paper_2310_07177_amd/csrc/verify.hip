@@ -309,8 +309,10 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(V
             St += rescale(s_sum[0][w], s_max[0][w], Kt);
             Sd += rescale(s_sum[1][w], s_max[1][w], Kd);
         }
-        const bool bad = !(Kt > kNegInf && Kt < -kNegInf) ||
-                         (!bonus && !(Kd > kNegInf && Kd < -kNegInf));
+        // A row without finite logits, or with a NaN logit (its sum is NaN),
+        // cannot be tested or drawn from.
+        const bool bad = !(Kt > kNegInf && Kt < -kNegInf) || !usable_sum(St) ||
+                         (!bonus && (!(Kd > kNegInf && Kd < -kNegInf) || !usable_sum(Sd)));
         if (bad) {
             if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadRow, 0));
             return;

@@ -394,6 +394,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     const float c2 = a.c2;
     const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
     const float beta = a.beta, omb = 1.0f - a.beta;
+    // JSD at beta = 0: the mixture is q itself, and every log2(q/m) is 0.
+    const bool q_only = a.beta == 0.0f;
 
     chunk_t rt[CPT], rs[CPT];
     float c1[CPT][EPC];
@@ -531,16 +533,15 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         // (the first term starts the sums: 0 + x would cost an add)
                         st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
                         ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
-                        if constexpr (KIND == 2) {
-                            // One floor suffices: with lp finite, a draft
-                            // exponent of -inf clamps lq - lp to -126 and
-                            // gives q = 0, so its terms vanish.
-                            c0v[j] = fmaxf(vt, kLogFloor);
-                            c1[r][e] = vs;
-                        } else {
-                            c0v[j] = vt - vs;  // log2 of the unnormalised ratio
-                            c1[r][e] = KIND == 0 ? vt : vs;
-                        }
+                        // Both exponents, for every kind: each side's
+                        // probability is rebuilt from its own exponent, so
+                        // a -inf logit on either side alone gives that side
+                        // 0 and the other its true value.  One floor
+                        // suffices: with the target's exponent finite, a
+                        // draft exponent of -inf still gives q = 0, and two
+                        // -inf exponents give a finite difference.
+                        c0v[j] = fmaxf(vt, kLogFloor);
+                        c1[r][e] = vs;
                     }
                     lc.store(r, g, f32x4_t{c0v[0], c0v[1], c0v[2], c0v[3]});
                 }
@@ -580,19 +581,11 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             // Exponent range exceeded by an element far above the first
             // chunk's maximum: rescale exactly from the cache.
             float ks_t = kc_t, ks_s = kc_s;
-            if (!(S_t < 1.0e300)) {
-                ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float {
-                    if constexpr (KIND == 2) return lc.load(r, e / 4)[e % 4];
-                    else if constexpr (KIND == 0) return c1[r][e];
-                    else return c1[r][e] + lc.load(r, e / 4)[e % 4];
-                });
+            if (S_t >= 1.0e300) {  // (a NaN sum stays NaN: it marks a NaN logit)
+                ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float { return lc.load(r, e / 4)[e % 4]; });
             }
-            if (!(S_s < 1.0e300)) {
-                ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float {
-                    if constexpr (KIND == 2) return c1[r][e];
-                    else if constexpr (KIND == 1) return c1[r][e];
-                    else return c1[r][e] - lc.load(r, e / 4)[e % 4];
-                });
+            if (S_s >= 1.0e300) {
+                ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float { return c1[r][e]; });
             }
             float Kt = ks_t, Ks = ks_s;
             double St = S_t, Ss = S_s;
@@ -642,20 +635,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     // Element masses from the cache; the sums and the walk
                     // evaluate exactly this formula on the same values.
                     auto formula = [&](float c0, float cc1, bool residual) -> float {
-                        float lp, lq;
-                        if constexpr (KIND == 2) {
-                            lp = c0 - ct;
-                            lq = cc1 - cs;
-                        } else {
-                            const float lr = fmaxf(fminf(c0 - dTk, -kLogFloor), kLogFloor);
-                            if constexpr (KIND == 0) {
-                                lp = cc1 - ct;
-                                lq = lp - lr;
-                            } else {
-                                lq = cc1 - cs;
-                                lp = lq + lr;
-                            }
-                        }
+                        const float lp = c0 - ct, lq = cc1 - cs;
                         const float p = exp2_fast(lp);
                         if (!residual) return p;
                         return fmaxf(p - exp2_fast(lq), 0.0f);
@@ -713,21 +693,21 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                                 const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
                                 const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
                                 const float p = exp2_fast(lp), q = exp2_fast(lq);
-                                const float x = d - L;  // log2(q/m)
+                                const float x = q_only ? 0.0f : d - L;  // log2(q/m); m = q at beta = 0
                                 a0 = __builtin_fmaf(p, -L, a0);
                                 a1 = __builtin_fmaf(q, x, a1);
                                 c0v[j] = x;
                                 c1[r][e] = q;
                             } else {
-                                // log2(p/q), clamped so that a zero probability
+                                // log2(p/q) from the difference of the two
+                                // exponents, clamped so that a zero probability
                                 // times an infinite log-ratio stays 0.
-                                const float lr = fmaxf(fminf(c0v[j] - dTk, -kLogFloor), kLogFloor);
+                                const float lr = fmaxf(fminf((c0v[j] - c1[r][e]) - dTk, -kLogFloor), kLogFloor);
                                 if constexpr (KIND == 0) {
-                                    const float lp = c1[r][e] - ct;
-                                    const float p = exp2_fast(lp);
+                                    const float p = exp2_fast(c0v[j] - ct);
                                     a0 = __builtin_fmaf(p, lr, a0);
                                     c0v[j] = p;
-                                    c1[r][e] = lp - lr;
+                                    c1[r][e] = c1[r][e] - cs;  // log2 q
                                 } else {
                                     const float q = exp2_fast(c1[r][e] - cs);
                                     a0 = __builtin_fmaf(q, lr, a0);

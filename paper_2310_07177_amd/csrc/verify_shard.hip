@@ -293,8 +293,9 @@ __global__ __launch_bounds__(W, 4) void shard_mass_kernel(MassArgs a) {
                     sd = mine ? rec(i).s_draft : 0.0;
                     wave_merge_stats(kd, sd);
                 }
-                if (!finite_shift(kt) || (!bonus_row && !finite_shift(kd))) {
-                    bad = true;  // a row the test reaches has no finite logit
+                if (!finite_shift(kt) || !usable_sum(st) ||
+                    (!bonus_row && (!finite_shift(kd) || !usable_sum(sd)))) {
+                    bad = true;  // a row the test reaches has no finite logit (or a NaN)
                     break;
                 }
                 d.kt = kt;

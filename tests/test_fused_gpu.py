@@ -215,3 +215,49 @@ def test_fused_jsd_one_sided_neg_inf(osd, side):
     x["tokens"] = synth.gumbel_max_tokens(synth.rng(8), x["draft"], 1.0)
     mask = np.ones((6, 4), np.uint8)
     check_fused(osd, x, "jsd", 0.5, mask, f"fused one-sided -inf ({side})")
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+def test_fused_jsd_endpoints_are_zero(osd, beta):
+    """JSD at beta in {0, 1} is identically 0 (the term of weight 0 is left
+    out): zero losses and gradient rows, while verification is unaffected."""
+    x = synth.verify_inputs(8, 4, 8192, "bf16", T=0.9, seed=43, target_std=2.5, draft_noise=1.5)
+    holes = np.random.default_rng(3).random(x["draft"].shape) < 0.2
+    x["draft"][holes] = 0xFF80
+    x["tokens"] = synth.gumbel_max_tokens(synth.rng(9), x["draft"], 0.9)
+    mask = np.ones((8, 4), np.uint8)
+    _, _, loss = check_fused(osd, x, "jsd", beta, mask, f"fused jsd beta={beta}")
+    acc, toks, rmask, loss, rows, g = run_fused(osd, x, "jsd", beta, mask)
+    assert loss.tolist() == [0.0, 0.0] and not rows.any()
+    assert np.all(synth.bf16_to_f32(g) == 0.0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind,side", [("fkl", "target"), ("rkl", "draft")])
+def test_fused_kl_one_sided_neg_inf(osd, kind, side, dtype):
+    """-inf logits on the side that keeps the divergence finite (FKL: target
+    holes, p = 0 < q; RKL: draft holes, q = 0 < p): the gradient at a hole is
+    q/tau (FKL) or 0 (RKL), and the draws use each side's own probability."""
+    V = 8192 if dtype == "bf16" else 4100
+    x = synth.verify_inputs(6, 4, V, dtype, T=1.0, seed=47, target_std=2.0, draft_noise=1.0)
+    holes = np.random.default_rng(53).random(x[side].shape) < 0.25
+    x[side][holes] = 0xFF80 if dtype == "bf16" else -np.inf
+    x["tokens"] = synth.gumbel_max_tokens(synth.rng(10), x["draft"], 1.0)
+    check_fused(osd, x, kind, 0.5, np.ones((6, 4), np.uint8), f"fused {kind} one-sided -inf ({side}) {dtype}")
+
+
+def test_fused_nan_logits_give_invalid_rows(osd):
+    """A NaN logit in a target or draft row that the test reaches invalidates
+    the sequence, as in osd_verify."""
+    x = synth.verify_inputs(8, 4, 8192, "bf16", T=1.0, seed=59, draft_noise=0.5)
+    x["target"][0, 0, 100] = np.uint16(0x7FC0)
+    x["draft"][1, 0, 7] = np.uint16(0x7FC0)
+    mask = np.ones((8, 4), np.uint8)
+    mask[:2] = 0                          # a NaN row has no finite divergence
+    acc, toks, rmask, loss, rows, g = run_fused(osd, x, "fkl", 0.5, mask)
+    assert acc[0] == -1 and acc[1] == -1 and (toks[:2] == -1).all() and not rmask[:2].any()
+    rv = ref.verify(x["target"], x["draft"], x["tokens"], x["u_accept"], x["u_resample"], x["T"])
+    keep = np.arange(8) >= 2
+    rr = {k: (v[keep] if isinstance(v, np.ndarray) and v.shape[:1] == (8,) else v) for k, v in rv.items()}
+    compare_verify(rr, acc[keep], toks[keep], rmask[keep], "fused nan rows")
+    assert np.isfinite(loss).all()

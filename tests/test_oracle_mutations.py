@@ -26,8 +26,8 @@ MUTATIONS = {
                                       "                    a = i;\n                    rejected = true;"),
     "rkl_grad_missing_kl_term": ("(logQ[(size_t)j] - logP[(size_t)j] - D) /",
                                  "(logQ[(size_t)j] - logP[(size_t)j]) /"),
-    "jsd_mixture_swapped": ("std::log(beta * P[(size_t)j] + (1.0 - beta) * Q[(size_t)j]);",
-                            "std::log(beta * Q[(size_t)j] + (1.0 - beta) * P[(size_t)j]);"),
+    "jsd_mixture_swapped": ("std::log(wp * P[(size_t)j] + wq * Q[(size_t)j]);",
+                            "std::log(wp * Q[(size_t)j] + wq * P[(size_t)j]);"),
     "fkl_grad_missing_tau": ("g[j] = (Q[(size_t)j] - P[(size_t)j]) / tau;",
                              "g[j] = (Q[(size_t)j] - P[(size_t)j]);"),
     "fkl_sign_flipped": ("D += P[(size_t)j] * (logP[(size_t)j] - logQ[(size_t)j]);",

@@ -380,3 +380,76 @@ def test_distill_jsd_one_sided_neg_inf(osd, side, dtype):
     if side == "student":
         gg = synth.bf16_to_f32(grad) if dtype == "bf16" else grad
         assert np.all(gg[holes] == 0)  # q = 0 there
+
+
+@pytest.mark.parametrize("V", [4096, 5000])
+@pytest.mark.parametrize("beta", [0.0, 1.0])
+def test_distill_jsd_endpoints_are_zero(osd, beta, V):
+    """Eq. 3 at beta in {0, 1}: m is q (beta = 0) or p (beta = 1) and the term
+    whose weight is 0 is left out, so JSD and its gradient are exactly 0,
+    also where one side has -inf logits (disjoint supports).  V = 4096 takes
+    the streaming kernel, V = 5000 (rows not a multiple of 16 bytes) the
+    row-resident one."""
+    g = np.random.default_rng(int(beta * 10) + V)
+    B, K = 3, 4
+    t = g.normal(0, 2.5, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1.5, (B, K, V))).astype(np.float32)
+    t[g.random((B, K, V)) < 0.3] = -np.inf
+    s[g.random((B, K, V)) < 0.3] = -np.inf
+    s[0, 0, :V // 2] = -np.inf            # row (0, 0): supports disjoint
+    t[0, 0, V // 2:] = -np.inf
+    mask = np.ones((B, K), np.uint8)
+    mask[2, 1] = 0
+    loss, rows, grad = check_distill(osd, synth.to_bf16(t), synth.to_bf16(s), "jsd", beta, 0.9, mask,
+                                     f"jsd beta={beta} V={V}")
+    assert loss.tolist() == [0.0, 0.0] and not rows.any()
+    assert np.all(synth.bf16_to_f32(grad) == 0.0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("V", [4096, 5000])
+@pytest.mark.parametrize("kind,side", [("fkl", "teacher"), ("rkl", "student"), ("fkl", "student")])
+def test_distill_kl_one_sided_neg_inf(osd, kind, side, V, dtype):
+    """-inf logits on one side only.  FKL with teacher holes (p = 0 < q) and
+    RKL with student holes (q = 0 < p) stay finite and their gradients are
+    q/tau and 0 there; FKL with student holes is infinite, but its gradient
+    (q - p)/tau = -p/tau at a hole is finite and is compared."""
+    g = np.random.default_rng(V + {"fkl": 0, "rkl": 1}[kind] * 10 + (side == "student") * 100)
+    B, K = 3, 4
+    t = g.normal(0, 2, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    holes = g.random((B, K, V)) < 0.25
+    (s if side == "student" else t)[holes] = -np.inf
+    mask = np.ones((B, K), np.uint8)
+    tt, ss = (synth.to_bf16(t), synth.to_bf16(s)) if dtype == "bf16" else (t, s)
+    label = f"one-sided -inf {kind} ({side}) V={V} {dtype}"
+    if (kind, side) != ("fkl", "student"):
+        check_distill(osd, tt, ss, kind, 0.5, 0.9, mask, label)
+        return
+    _, rows, grad = run_distill(osd, tt, ss, kind, 0.5, 0.9, mask)
+    r = ref.distill(tt, ss, kind, beta=0.5, tau=0.9, mask=mask)
+    assert np.all(np.isinf(r["row_loss"])) and np.all(rows > 1e20), rows
+    if dtype == "bf16":
+        compare_grad_bf16(grad, r["grad"], label)
+    else:
+        compare_grad_f32(grad, r["grad"], label)
+
+
+def test_verify_nan_logits_give_invalid_rows(osd):
+    """A NaN logit in a row the test reaches makes its sequence invalid (-1),
+    in the target row or in the draft row; a NaN in a row the test never
+    reaches changes nothing.  Other sequences match the oracle."""
+    x = synth.verify_inputs(8, 4, 4096, "bf16", T=1.0, seed=41, draft_noise=0.5)
+    nan = np.uint16(0x7FC0)
+    x["target"][0, 0, 100] = nan          # reached: invalid
+    x["draft"][1, 0, 7] = nan             # reached: invalid
+    x["u_accept"][2, 0] = np.float32(0.999)
+    x["target"][2, 1, 5] = nan            # position 0 rejects (u ~ 1 unless p/q > 1): check below
+    acc, toks, rmask = run_verify(osd, x)
+    assert acc[0] == -1 and acc[1] == -1 and (toks[:2] == -1).all() and not rmask[:2].any()
+    r = oracle_verify(x)
+    keep = np.arange(8) >= 2
+    rr = {k: (v[keep] if isinstance(v, np.ndarray) and v.shape[:1] == (8,) else v) for k, v in r.items()}
+    compare_verify(rr, acc[keep], toks[keep], rmask[keep], "nan rows")
+    if r["accepted_len"][2] == 0:
+        assert acc[2] == 0  # the NaN row 1 was never reached
