@@ -28,8 +28,12 @@
  *   - Workspaces: the caller allocates `*_workspace_bytes(...)` bytes of
  *     device memory and fills them with zeros ONCE before first use; every
  *     call leaves its workspace zeroed again when its kernels finish.  Calls
- *     that may run concurrently need distinct workspaces.
- *   - Thread-safe: the library holds no mutable global state.
+ *     that may run concurrently need distinct workspaces.  (A workspace that
+ *     is not zero -- fresh from an uninitialised allocation, or shared by
+ *     calls in flight on two streams -- is not detected: the outputs are then
+ *     wrong, with no status to say so.)
+ *   - Thread-safe: apart from osd_verify_noalloc's per-GPU scratch array
+ *     (see there), the library holds no mutable global state.
  */
 #ifndef OSD_H
 #define OSD_H
@@ -46,7 +50,8 @@ typedef enum {
     OSD_ERR_INVALID_ARG = -1,
     OSD_ERR_UNSUPPORTED = -2,
     OSD_ERR_DEVICE = -3,
-    OSD_ERR_WORKSPACE = -4
+    OSD_ERR_WORKSPACE = -4,
+    OSD_ERR_SCRATCH = -5
 } osd_status;
 
 typedef enum { OSD_F32 = 0, OSD_BF16 = 1 } osd_dtype;
@@ -107,6 +112,30 @@ int osd_verify(const void* target_logits, const void* draft_logits, int dtype,
                int32_t* accepted_len, int32_t* out_tokens,
                uint8_t* reject_mask,
                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * osd_verify_noalloc -- osd_verify for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same arguments without the workspace, and the same
+ * results.  Its scratch is a device array the library holds, one per GPU, of
+ * OSD_VERIFY_NOALLOC_SCRATCH_BYTES bytes, kept until the process ends; the
+ * call itself allocates nothing.  Calls with
+ * osd_verify_workspace_bytes(B, K) > OSD_VERIFY_NOALLOC_SCRATCH_BYTES
+ * (about B * (K + 1) > 10000 rows) return OSD_ERR_SCRATCH and enqueue
+ * nothing.  Every call on one GPU shares that GPU's array: each call clears
+ * the part it needs on its own stream first, and calls that may overlap on
+ * one GPU (concurrent streams, other host threads) race and must not be made
+ * -- give those osd_verify with separate workspaces.  Other errors as
+ * osd_verify.
+ */
+#define OSD_VERIFY_NOALLOC_SCRATCH_BYTES (4u << 20)
+int osd_verify_noalloc(const void* target_logits, const void* draft_logits, int dtype,
+                       int B, int K, int V,
+                       const int32_t* draft_tokens, const int32_t* draft_len,
+                       const float* u_accept, const float* u_resample,
+                       float temperature,
+                       int32_t* accepted_len, int32_t* out_tokens,
+                       uint8_t* reject_mask, void* stream);
 
 /* Workspace needed by osd_distill_loss_grad for B*K rows. */
 size_t osd_distill_workspace_bytes(int B, int K);

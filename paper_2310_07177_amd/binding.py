@@ -14,7 +14,8 @@ import threading
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libosd.so")
 
-OSD_OK, OSD_ERR_INVALID_ARG, OSD_ERR_UNSUPPORTED, OSD_ERR_DEVICE, OSD_ERR_WORKSPACE = 0, -1, -2, -3, -4
+OSD_OK, OSD_ERR_INVALID_ARG, OSD_ERR_UNSUPPORTED, OSD_ERR_DEVICE, OSD_ERR_WORKSPACE, OSD_ERR_SCRATCH = 0, -1, -2, -3, -4, -5
+OSD_VERIFY_NOALLOC_SCRATCH_BYTES = 4 << 20
 OSD_F32, OSD_BF16 = 0, 1
 OSD_FKL, OSD_RKL, OSD_JSD = 0, 1, 2
 OSD_MAX_K = 16
@@ -25,7 +26,7 @@ SHARD_ROW_STATS_BYTES = 40
 SHARD_MASS_BYTES = 48
 KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
-EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify",
+EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify", "osd_verify_noalloc",
            "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
            "osd_verify_distill", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
            "osd_shard_verify_draw")
@@ -60,6 +61,8 @@ def lib():
             L.osd_verify.restype = i32
             L.osd_verify.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32,
                                      vp, vp, vp, vp, sz, vp]
+            L.osd_verify_noalloc.restype = i32
+            L.osd_verify_noalloc.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp]
             L.osd_distill_workspace_bytes.restype = sz
             L.osd_distill_workspace_bytes.argtypes = [i32, i32]
             L.osd_distill_loss_grad.restype = i32
@@ -165,6 +168,35 @@ def osd_verify(target_logits, draft_logits, draft_tokens, u_accept, u_resample, 
                       ws.numel(), _stream_handle(dev))
     if st != OSD_OK:
         raise OsdError("osd_verify", st)
+    return acc, toks, rmask
+
+
+def osd_verify_noalloc(target_logits, draft_logits, draft_tokens, u_accept, u_resample, temperature,
+                       draft_len=None, out=None):
+    """osd_verify through the allocation-free entry point: no workspace, the
+    library's per-GPU scratch array instead (calls that overlap on one GPU
+    race).  Arguments and results as osd_verify; the outputs must be given
+    (`out`) by a caller that cannot allocate."""
+    torch = _torch()
+    B, K1, V = target_logits.shape
+    K = K1 - 1
+    _check_cuda(target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len)
+    dev = target_logits.device
+    for t in (target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if draft_tokens.dtype != torch.int32 or (draft_len is not None and draft_len.dtype != torch.int32):
+        raise TypeError("draft_tokens and draft_len must be int32")
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, K + 1, dtype=torch.int32, device=dev),
+               torch.empty(B, K, dtype=torch.uint8, device=dev))
+    acc, toks, rmask = out
+    st = lib().osd_verify_noalloc(_ptr(target_logits), _ptr(draft_logits), _dtype_code(target_logits), B, K, V,
+                                  _ptr(draft_tokens), _ptr(draft_len), _ptr(u_accept), _ptr(u_resample),
+                                  float(temperature), _ptr(acc), _ptr(toks), _ptr(rmask), _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_verify_noalloc", st)
     return acc, toks, rmask
 
 

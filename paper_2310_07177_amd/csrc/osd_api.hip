@@ -1,7 +1,10 @@
 // osd_api.hip -- the C ABI of libosd (declared in include/osd.h): argument
 // validation, workspace carving and kernel dispatch.  No allocation, no
-// synchronisation, no global mutable state.
+// synchronisation; the only global state is the allocation-free entry
+// point's scratch array and its per-device address (end of this file).
 #include <math.h>
+
+#include <mutex>
 
 #include "osd.h"
 #include "osd_internal.hpp"
@@ -106,6 +109,9 @@ const char* osd_status_string(int status) {
         case OSD_ERR_UNSUPPORTED: return "OSD_ERR_UNSUPPORTED: the vocabulary size or dtype is not supported";
         case OSD_ERR_DEVICE: return "OSD_ERR_DEVICE: the HIP runtime failed to launch a kernel";
         case OSD_ERR_WORKSPACE: return "OSD_ERR_WORKSPACE: the workspace is NULL or smaller than required";
+        case OSD_ERR_SCRATCH:
+            return "OSD_ERR_SCRATCH: the call needs more scratch than the allocation-free entry point holds "
+                   "(osd_verify_workspace_bytes(B, K) > OSD_VERIFY_NOALLOC_SCRATCH_BYTES)";
         default: return "unknown osd status";
     }
 }
@@ -429,3 +435,78 @@ int osd_shard_verify_draw(const void* target_shard, const void* draft_shard, int
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free verification.  The scratch of osd_verify (arrival counters,
+// per-row records, greedy argmax partials) lives in a device array that the
+// library holds for the life of the process, one copy per GPU.  In host code
+// `scratch` names a host-side stand-in, not device memory: its device address
+// on each GPU comes from hipGetSymbolAddress, taken once per device with that
+// device current, and only that address is handed to kernels.
+// ---------------------------------------------------------------------------
+namespace {
+
+static __device__ __align__(256) unsigned char scratch[OSD_VERIFY_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Zero n 32-bit words (a kernel rather than a memset: it may be captured
+// into a graph).
+__global__ void clear_words(uint32_t* p, int n) {
+    for (int i = int(blockIdx.x * blockDim.x + threadIdx.x); i < n; i += int(gridDim.x * blockDim.x)) p[i] = 0u;
+}
+
+// The device address of `scratch` on device dev (nullptr on failure).
+void* scratch_on(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::call_once(g_scratch_once[dev], [dev] {
+        int cur = -1;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+        void* ptr = nullptr;
+        if (e == hipSuccess) e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+        g_scratch_err[dev] = e;
+        g_scratch_ptr[dev] = e == hipSuccess ? ptr : nullptr;
+    });
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" int osd_verify_noalloc(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
+                                  int V, const int32_t* draft_tokens, const int32_t* draft_len,
+                                  const float* u_accept, const float* u_resample, float temperature,
+                                  int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+                                  void* stream) {
+    // Argument checks first (nothing is enqueued on an error), then the size.
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || K <= 0 || V <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
+    if (!sizes_ok(B, K, V, dtype)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    if (!target_logits || !draft_tokens || !accepted_len || !out_tokens) return OSD_ERR_INVALID_ARG;
+    if (temperature > 0.0f && (!draft_logits || !u_accept || !u_resample)) return OSD_ERR_INVALID_ARG;
+    const VerifyWs ws = verify_layout(B, K);
+    if (ws.total > size_t(OSD_VERIFY_NOALLOC_SCRATCH_BYTES)) return OSD_ERR_SCRATCH;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int dev = 0;
+    if (s == nullptr || hipStreamGetDevice(s, &dev) != hipSuccess) {
+        if (hipGetDevice(&dev) != hipSuccess) return OSD_ERR_DEVICE;
+    }
+    void* ptr = scratch_on(dev);
+    if (!ptr) return OSD_ERR_DEVICE;
+    // The counters and records must start at zero.  osd_verify's kernels
+    // leave them zero, but the array keeps whatever the previous call on this
+    // GPU left, so they are cleared here on the call's own stream.  (The
+    // greedy partials are written before they are read.)
+    const int words = int(ws.stats / 4);
+    const int threads = 256, blocks = (words + threads - 1) / threads < 1024 ? (words + threads - 1) / threads : 1024;
+    hipLaunchKernelGGL(clear_words, dim3(blocks), dim3(threads), 0, s, static_cast<uint32_t*>(ptr), words);
+    if (hipGetLastError() != hipSuccess) return OSD_ERR_DEVICE;
+    return osd_verify(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept, u_resample,
+                      temperature, accepted_len, out_tokens, reject_mask, ptr, ws.total, stream);
+}

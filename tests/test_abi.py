@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_limits():
     L = osd.lib()
-    for s in (0, -1, -2, -3, -4):
+    for s in (0, -1, -2, -3, -4, -5):
         assert L.osd_status_string(s).startswith(b"OSD_")
     assert L.osd_max_vocab(binding.OSD_BF16) >= 128256
     assert L.osd_max_vocab(binding.OSD_F32) >= 32768
@@ -251,3 +251,18 @@ def test_shard_record_layout_matches_header(tmp_path):
     subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
     got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()]
     assert got == [binding.SHARD_ROW_STATS_BYTES, binding.SHARD_MASS_BYTES, 16, 32, 36, 16, 40, 44]
+
+
+def test_verify_noalloc_rejects_before_touching_the_gpu():
+    """The allocation-free verification checks its arguments, then its size
+    against the library's scratch, before any HIP call."""
+    L = osd.lib()
+    args = lambda B, K, **kw: (kw.get("t", FAKE), FAKE, 1, B, K, 64, FAKE, None, FAKE, FAKE,
+                               kw.get("T", 1.0), FAKE, FAKE, None, None)
+    assert L.osd_verify_noalloc(*args(2, 3, t=None)) == -1
+    assert L.osd_verify_noalloc(*args(2, 17)) == -1
+    assert L.osd_verify_noalloc(*args(2, 3, T=float("nan"))) == -1
+    big = 4096  # 4096 x 9 rows need more than OSD_VERIFY_NOALLOC_SCRATCH_BYTES
+    assert L.osd_verify_workspace_bytes(big, 8) > binding.OSD_VERIFY_NOALLOC_SCRATCH_BYTES
+    assert L.osd_verify_noalloc(*args(big, 8)) == binding.OSD_ERR_SCRATCH
+    assert L.osd_verify_workspace_bytes(1024, 8) <= binding.OSD_VERIFY_NOALLOC_SCRATCH_BYTES
