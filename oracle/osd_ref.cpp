@@ -404,6 +404,188 @@ extern "C" int osd_ref_distill_loss_grad(const void* teacher,
 }
 
 /*
+ * Multi-candidate (tree) verification.  The paper applies online updates to
+ * Medusa, which proposes several candidate tokens per position arranged in a
+ * tree, and states no verification rule for it (Section 5, "OSD and
+ * Medusa", Table 4).  The rule used here keeps the exactness that the
+ * paper's verification has (the emitted tokens follow the target): the
+ * children of a node are candidates drawn independently from the draft
+ * distribution q at that node, and they are tested one after another by the
+ * same accept/resample step as Appendix A.1, where after each rejection the
+ * distribution the next candidate is tested against becomes the residual
+ * norm(max(0, p - q)) of Eq. 5.  The first accepted candidate is emitted and
+ * the walk continues at its node; when every child of a node is rejected,
+ * one token is drawn from the last residual, and at a node without children
+ * one token is drawn from p (the bonus token).  At T == 0 the first child
+ * whose token is the target argmax is accepted, and the argmax is emitted
+ * where the walk stops.
+ */
+extern "C" int osd_ref_verify_tree(const void* target, const void* draft, int dtype,
+                                   int B, int N, int V,
+                                   const int32_t* parent, const int32_t* node_tokens,
+                                   const float* u_accept, const float* u_resample,
+                                   float temperature, int32_t* accepted_len,
+                                   int32_t* out_tokens, int32_t* path_nodes,
+                                   double* margin_accept, double* margin_cdf,
+                                   int32_t* z_fallback) {
+    if (!target || !parent || !node_tokens || !accepted_len || !out_tokens) return -1;
+    if (B <= 0 || N <= 0 || V <= 0) return -1;
+    if (dtype != OSD_REF_F32 && dtype != OSD_REF_BF16 && dtype != OSD_REF_F64)
+        return -1;
+    if (!(temperature >= 0.0f) || std::isinf(temperature)) return -1;
+    const bool greedy = temperature == 0.0f;
+    if (!greedy && (!draft || !u_accept || !u_resample)) return -1;
+    const double T = (double)temperature;
+    const int64_t stride = (int64_t)N * V;
+
+    for (int b = 0; b < B; ++b) {
+        int32_t* out = out_tokens + (size_t)b * N;
+        int32_t* pn = path_nodes ? path_nodes + (size_t)b * N : nullptr;
+        for (int n = 0; n < N; ++n) {
+            out[n] = -1;
+            if (pn) pn[n] = -1;
+            if (margin_accept) margin_accept[(size_t)b * N + n] = kNaN;
+        }
+        if (margin_cdf) margin_cdf[b] = kNaN;
+        if (z_fallback) z_fallback[b] = 0;
+        accepted_len[b] = -1;
+
+        /* The tree: node 0 is the root (the accepted context); every other
+         * node names an earlier node as its parent and carries a token. */
+        const int32_t* par = parent + (size_t)b * N;
+        const int32_t* tok = node_tokens + (size_t)b * N;
+        bool ok = true;
+        for (int n = 1; n < N; ++n)
+            if (par[n] < 0 || par[n] >= n || tok[n] < 0 || tok[n] >= V) ok = false;
+        if (!ok) continue;
+
+        std::vector<int> path;
+        int extra = -1;
+        int v = 0;
+        for (;;) {
+            std::vector<int> kids;
+            for (int n = v + 1; n < N; ++n)
+                if (par[n] == v) kids.push_back(n);
+            std::vector<double> t = load_row(target, dtype, b * stride + (int64_t)v * V, V);
+            if (greedy) {
+                const int g = row_argmax(t);
+                if (g < 0) {
+                    ok = false;
+                    break;
+                }
+                int next = -1;
+                for (int c : kids)
+                    if (tok[c] == g) {
+                        next = c;
+                        break;
+                    }
+                if (next < 0) {
+                    extra = g;
+                    break;
+                }
+                path.push_back(next);
+                v = next;
+                continue;
+            }
+            std::vector<double> P, logP;
+            if (!temperature_softmax(t, T, P, logP)) {
+                ok = false;
+                break;
+            }
+            if (kids.empty()) {
+                /* no candidate below this node: the bonus token from p */
+                double Z = 0.0;
+                for (int j = 0; j < V; ++j) Z += P[(size_t)j];
+                double m = 0.0;
+                extra = inverse_cdf(P, Z, u_resample[b], &m);
+                if (margin_cdf) margin_cdf[b] = m;
+                if (extra < 0) ok = false;
+                break;
+            }
+            std::vector<double> Q, logQ;
+            std::vector<double> d = load_row(draft, dtype, b * stride + (int64_t)v * V, V);
+            if (!temperature_softmax(d, T, Q, logQ)) {
+                ok = false;
+                break;
+            }
+            /* Candidates in order; R is the distribution the next one is
+             * tested against: p, then after each rejection the normalised
+             * residual max(0, R - q). */
+            std::vector<double> R = P;
+            /* the last rejection's residual max(0, R - q) before it is
+             * normalised, and its total: the extra token is drawn from it,
+             * so that its CDF margin is in the same units as Eq. 5's single
+             * residual (one candidate per node gives exactly that draw) */
+            std::vector<double> last_r;
+            double last_Z = 0.0;
+            int next = -1;
+            for (int c : kids) {
+                const double rc = R[(size_t)tok[c]], qc = Q[(size_t)tok[c]];
+                double ratio;
+                if (qc > 0.0)
+                    ratio = rc / qc;
+                else
+                    ratio = rc > 0.0 ? kInf : 0.0;
+                const float u = u_accept[(size_t)b * N + c];
+                if (margin_accept) margin_accept[(size_t)b * N + c] = std::fabs((double)u - ratio);
+                if ((double)u < ratio) {
+                    next = c;
+                    break;
+                }
+                std::vector<double> r((size_t)V);
+                double Z = 0.0;
+                for (int j = 0; j < V; ++j) {
+                    const double diff = R[(size_t)j] - Q[(size_t)j];
+                    r[(size_t)j] = diff > 0.0 ? diff : 0.0;
+                }
+                for (int j = 0; j < V; ++j) Z += r[(size_t)j];
+                if (!(Z > 0.0)) {
+                    /* impossible in exact arithmetic (a rejection needs
+                     * R(y) < q(y)); under rounding R is kept */
+                    if (z_fallback) z_fallback[b] = 1;
+                    last_r.clear();
+                    continue;
+                }
+                last_r = r;
+                last_Z = Z;
+                for (int j = 0; j < V; ++j) R[(size_t)j] = r[(size_t)j] / Z;
+            }
+            if (next >= 0) {
+                path.push_back(next);
+                v = next;
+                continue;
+            }
+            /* every candidate rejected: one token from the last residual */
+            if (last_r.empty()) {
+                last_r = R;
+                last_Z = 0.0;
+                for (int j = 0; j < V; ++j) last_Z += R[(size_t)j];
+            }
+            double m = 0.0;
+            extra = inverse_cdf(last_r, last_Z, u_resample[b], &m);
+            if (margin_cdf) margin_cdf[b] = m;
+            if (extra < 0) ok = false;
+            break;
+        }
+        if (!ok) {
+            for (int n = 0; n < N; ++n) {
+                out[n] = -1;
+                if (pn) pn[n] = -1;
+            }
+            if (margin_cdf) margin_cdf[b] = kNaN;
+            continue;
+        }
+        accepted_len[b] = (int32_t)path.size();
+        for (size_t i = 0; i < path.size(); ++i) {
+            out[i] = tok[path[i]];
+            if (pn) pn[i] = path[i];
+        }
+        out[path.size()] = extra;
+    }
+    return 0;
+}
+
+/*
  * Token sampling: the draft's proposals y ~ q (Algorithm 1) and the mixed
  * sampling y ~ beta p + (1 - beta) q of Section 4.1.  Per row n the
  * distribution is pi = beta softmax(p_n / T) + (1 - beta) softmax(q_n / T)

@@ -84,6 +84,39 @@ int osd_ref_distill_loss_grad(const void* teacher, int64_t teacher_batch_stride,
                               double* grad);
 
 /*
+ * Multi-candidate (tree) verification (Section 5, "OSD and Medusa": several
+ * candidates per position; the rule is the recursive form of Appendix A.1's
+ * test, see osd_ref.cpp).
+ *
+ * target       [B, N, V]  row n: target logits after the prefix ending at
+ *                         node n (it scores node n's children; at a node
+ *                         without children it is the bonus distribution)
+ * draft        [B, N, V]  row n: draft logits node n's children were drawn
+ *                         from (i.i.d.); unused at T == 0 and at leaves
+ * parent       [B, N]     parent node of each node; node 0 is the root
+ *                         (its entry is ignored); 0 <= parent[n] < n
+ * node_tokens  [B, N]     the candidate token of each node (node 0 ignored)
+ * u_accept     [B, N]     the uniform that tests node n; u_resample [B]
+ * accepted_len out [B]    number of accepted candidates (path length), -1
+ *                         for an invalid tree or a reached row without a
+ *                         finite logit
+ * out_tokens   out [B, N] the accepted candidates' tokens, the extra token,
+ *                         then -1
+ * path_nodes   out [B, N] nullable: the accepted nodes, then -1
+ * margin_accept out [B, N] nullable: |u - ratio| of every tested candidate
+ * margin_cdf   out [B]    nullable: the extra draw's CDF margin (absolute)
+ * z_fallback   out [B]    nullable: 1 where a residual had no mass
+ */
+int osd_ref_verify_tree(const void* target, const void* draft, int dtype,
+                        int B, int N, int V,
+                        const int32_t* parent, const int32_t* node_tokens,
+                        const float* u_accept, const float* u_resample,
+                        float temperature, int32_t* accepted_len,
+                        int32_t* out_tokens, int32_t* path_nodes,
+                        double* margin_accept, double* margin_cdf,
+                        int32_t* z_fallback);
+
+/*
  * Token sampling: the draft's proposals y ~ q (Algorithm 1) and mixed
  * sampling y ~ beta p + (1 - beta) q (Section 4.1).
  *

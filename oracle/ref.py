@@ -36,6 +36,8 @@ def lib():
         L.osd_ref_distill_loss_grad.restype = i32
         L.osd_ref_distill_loss_grad.argtypes = [vp, i64, vp, i64, i32, i32, i32,
                                                 i32, vp, i32, f64, f64, vp, vp, vp]
+        L.osd_ref_verify_tree.restype = i32
+        L.osd_ref_verify_tree.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp, vp, vp]
         L.osd_ref_sample.restype = i32
         L.osd_ref_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f64, vp, vp, vp]
         L.osd_ref_round_bf16.restype = None
@@ -128,6 +130,36 @@ def distill(teacher, student, kind, beta=0.5, tau=1.0, mask=None, grad=True,
     if rc != 0:
         raise ValueError(f"osd_ref_distill_loss_grad rejected its arguments (rc={rc})")
     return dict(loss_mean=loss[0], loss_sum=loss[1], row_loss=rows, grad=g)
+
+
+def verify_tree(target, draft, parent, node_tokens, u_accept, u_resample, temperature):
+    """Oracle multi-candidate (tree) verification.  target, draft [B, N, V]
+    (draft may be None when temperature == 0), parent and node_tokens [B, N]
+    int32, u_accept [B, N], u_resample [B].  Returns a dict: accepted_len [B],
+    out_tokens [B, N], path_nodes [B, N], margin_accept [B, N], margin_cdf [B],
+    z_fallback [B]."""
+    target = _c(target)
+    B, N, V = target.shape
+    draft = _c(draft)
+    if draft is not None:
+        assert draft.shape == (B, N, V) and draft.dtype == target.dtype
+    par = _c(parent, np.int32)
+    tok = _c(node_tokens, np.int32)
+    assert par.shape == (B, N) and tok.shape == (B, N)
+    ua = _c(u_accept, np.float32)
+    ur = _c(u_resample, np.float32)
+    acc = np.empty(B, np.int32)
+    out = np.empty((B, N), np.int32)
+    pn = np.empty((B, N), np.int32)
+    ma = np.empty((B, N), np.float64)
+    mc = np.empty(B, np.float64)
+    zf = np.empty(B, np.int32)
+    rc = lib().osd_ref_verify_tree(_ptr(target), _ptr(draft), _dtype_code(target), B, N, V, _ptr(par), _ptr(tok),
+                                   _ptr(ua), _ptr(ur), float(temperature), _ptr(acc), _ptr(out), _ptr(pn),
+                                   _ptr(ma), _ptr(mc), _ptr(zf))
+    if rc != 0:
+        raise ValueError(f"osd_ref_verify_tree rejected its arguments (rc={rc})")
+    return dict(accepted_len=acc, out_tokens=out, path_nodes=pn, margin_accept=ma, margin_cdf=mc, z_fallback=zf)
 
 
 def sample(p, q, temperature, beta, u=None):

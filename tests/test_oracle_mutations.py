@@ -62,6 +62,11 @@ MUTATIONS = {
                 D = wp * kl_pm + wq * kl_qm;"""),
     "jsd_endpoint_grad_weight_ignored": ("g[j] = (wq > 0.0 && Q[(size_t)j] > 0.0)", "g[j] = (Q[(size_t)j] > 0.0)"),
     "cdf_margin_divided_by_z": ("*margin = a < b ? a : b;", "*margin = (a < b ? a : b) / Z;"),
+    "tree_residual_not_updated": ("for (int j = 0; j < V; ++j) R[(size_t)j] = r[(size_t)j] / Z;", "(void)0;"),
+    "tree_tested_against_p": ("const double rc = R[(size_t)tok[c]], qc", "const double rc = P[(size_t)tok[c]], qc"),
+    "tree_extra_from_p": ("extra = inverse_cdf(last_r, last_Z, u_resample[b], &m);",
+                          "extra = inverse_cdf(P, 1.0, u_resample[b], &m);"),
+    "tree_children_last_first": ("if (par[n] == v) kids.push_back(n);", "if (par[n] == v) kids.insert(kids.begin(), n);"),
     "sample_row_stride_ignored": ("temperature_softmax(load_row(q, dtype, (int64_t)n * q_stride, V), temp, Q, logQ)",
                                   "temperature_softmax(load_row(q, dtype, (int64_t)n * V, V), temp, Q, logQ)"),
 }
@@ -82,6 +87,7 @@ def test_pins_catch_planted_mistake(name, tmp_path):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_verify_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_distill_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_sample_pins.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_sample_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_tree_pins.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"
