@@ -32,8 +32,10 @@ MUTATIONS = {
                              "g[j] = (Q[(size_t)j] - P[(size_t)j]);"),
     "fkl_sign_flipped": ("D += P[(size_t)j] * (logP[(size_t)j] - logQ[(size_t)j]);",
                          "D += P[(size_t)j] * (logQ[(size_t)j] - logP[(size_t)j]);"),
-    "verify_temperature_ignored": ("const double T = (double)temperature;",
-                                   "const double T = 1.0;"),
+    "verify_temperature_ignored": ("const double T = (double)temperature;\n    const int64_t tstride",
+                                   "const double T = 1.0;\n    const int64_t tstride"),
+    "tree_temperature_ignored": ("const double T = (double)temperature;\n    const int64_t stride",
+                                 "const double T = 1.0;\n    const int64_t stride"),
     "distill_temperature_ignored": ("bool ok = temperature_softmax(t, tau, P, logP) &&\n                      temperature_softmax(s, tau, Q, logQ);",
                                     "bool ok = temperature_softmax(t, 1.0, P, logP) &&\n                      temperature_softmax(s, 1.0, Q, logQ);"),
     "argmax_last_on_ties": ("if (z[j] > bv) {", "if (z[j] >= bv) {"),
