@@ -211,6 +211,87 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * osd_verify_distill_rejected -- osd_verify_distill whose distilled rows are
+ * the verification's own outcome: the row pair at each sequence's first
+ * rejection a_b (the error index at which Algorithm 1 records the target for
+ * distillation; Fig. 1: the positions where the draft proposed a wrong
+ * token), and no other.  The results are those of
+ *   osd_verify(target, draft, ..., temperature, ..., reject_mask, ...) then
+ *   osd_distill_loss_grad(target, (K+1)*V, draft, K*V, dtype, B, K, V,
+ *                         reject_mask, kind, beta, temperature, ...):
+ * loss_out = {sum of D over the distilled rows / their number (0 if none),
+ * that sum}; row_loss_out and grad_out hold zeros on every other row.  The
+ * rejected row pair is read once: the workgroup that finds a sequence's
+ * first rejection draws the correction and distils the row from what it
+ * already holds.  (A workgroup that cannot learn in time whether an earlier
+ * position rejected distils its row anyway; if it was not the first, the
+ * call's last workgroup zeroes that row again.)
+ *
+ * Arguments as in osd_verify_distill, without distill_mask; reject_mask is
+ * nullable.  workspace: osd_verify_distill_workspace_bytes(B, K)
+ * zero-initialised bytes (one workspace serves both fused entry points).
+ * Decisions, losses and gradients have osd_verify_distill's accuracy.
+ */
+int osd_verify_distill_rejected(const void* target_logits, const void* draft_logits, int dtype,
+                                int B, int K, int V,
+                                const int32_t* draft_tokens, const int32_t* draft_len,
+                                const float* u_accept, const float* u_resample,
+                                float temperature,
+                                int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+                                int kind, float beta,
+                                float* loss_out, float* row_loss_out, void* grad_out,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * osd_verify_tree -- multi-candidate (tree) verification.  The paper applies
+ * its online updates to Medusa, which proposes several candidate tokens per
+ * position arranged in a tree (Section 5, "OSD and Medusa", Table 4), and
+ * states no verification rule for it; this call takes the rule that keeps
+ * Appendix A.1's exactness (the emitted tokens follow the target): the
+ * children of a node are candidates drawn independently from the draft
+ * distribution q at that node and are tested in ascending node order,
+ * candidate c accepted when u_c < R(y_c) / q(y_c), with R = p for the first
+ * and, after each rejection, R <- norm(max(0, R - q)) (Eq. 5's residual).
+ * The walk continues at the first accepted child; where every child is
+ * rejected one token is drawn from the last residual max(0, R - q), and at a
+ * node without children one token is drawn from p (the bonus token).  The
+ * draws are the inverse CDF of osd_verify.  T == 0: the first child whose
+ * token is the target argmax (lowest index on ties) is accepted and the
+ * argmax is emitted where the walk stops.  A chain (one child per node) is
+ * osd_verify.
+ *
+ * target_logits [B, N, V]  row n: target logits after the prefix ending at
+ *                          node n (it scores node n's children; at a node
+ *                          without children it is the bonus distribution)
+ * draft_logits  [B, N, V]  row n: draft logits node n's children were drawn
+ *                          from; not read at leaves; may be NULL at T == 0
+ * parent        [B, N] int32  node 0 is the root (the accepted context; its
+ *                          entry is ignored); 0 <= parent[n] < n for n >= 1
+ * node_tokens   [B, N] int32  the candidate token of node n (node 0 ignored)
+ * u_accept      [B, N] fp32  u_accept[b, n] tests node n; NULL iff T == 0
+ * u_resample    [B] fp32    the extra token's uniform; NULL iff T == 0
+ * accepted_len  out [B] int32  number of accepted candidates, or -1 for an
+ *                          invalid tree (a parent or token out of range) or
+ *                          a reached row without finite logits
+ * out_tokens    out [B, N] int32  accepted tokens, the extra token, then -1
+ * path_nodes    out [B, N] int32, nullable: the accepted nodes, then -1
+ * workspace     osd_verify_tree_workspace_bytes(B, N) zero-initialised bytes
+ *
+ * N <= OSD_MAX_TREE_NODES; V up to 32768 (bf16) or 16384 (fp32), otherwise
+ * OSD_ERR_UNSUPPORTED.  One workgroup per (sequence, node): every node's
+ * rows are read once, whether or not the walk reaches it.
+ */
+#define OSD_MAX_TREE_NODES 64
+size_t osd_verify_tree_workspace_bytes(int B, int N);
+int osd_verify_tree(const void* target_logits, const void* draft_logits, int dtype,
+                    int B, int N, int V,
+                    const int32_t* parent, const int32_t* node_tokens,
+                    const float* u_accept, const float* u_resample,
+                    float temperature,
+                    int32_t* accepted_len, int32_t* out_tokens, int32_t* path_nodes,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * osd_sample -- token sampling: the draft model's proposals y ~ q
  * (Algorithm 1) and the mixed sampling y ~ beta p + (1 - beta) q that
  * Section 4.1 uses to generate distillation data (beta weights the target

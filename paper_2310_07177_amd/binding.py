@@ -20,6 +20,7 @@ OSD_F32, OSD_BF16 = 0, 1
 OSD_FKL, OSD_RKL, OSD_JSD = 0, 1, 2
 OSD_MAX_K = 16
 OSD_MAX_SHARDS = 64
+OSD_MAX_TREE_NODES = 64
 # Byte sizes of the sharded verification's records (osd_shard_row_stats,
 # osd_shard_mass in include/osd.h); the binding keeps them as uint8 tensors.
 SHARD_ROW_STATS_BYTES = 40
@@ -28,7 +29,7 @@ KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
 EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify", "osd_verify_noalloc",
            "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
-           "osd_verify_distill", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
+           "osd_verify_distill", "osd_verify_distill_rejected", "osd_verify_tree_workspace_bytes", "osd_verify_tree", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
            "osd_shard_verify_draw")
 
 _lib = None
@@ -73,6 +74,13 @@ def lib():
             L.osd_verify_distill.restype = i32
             L.osd_verify_distill.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp,
                                              vp, i32, f32, vp, vp, vp, vp, sz, vp]
+            L.osd_verify_distill_rejected.restype = i32
+            L.osd_verify_distill_rejected.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp,
+                                                      vp, i32, f32, vp, vp, vp, vp, sz, vp]
+            L.osd_verify_tree_workspace_bytes.restype = sz
+            L.osd_verify_tree_workspace_bytes.argtypes = [i32, i32]
+            L.osd_verify_tree.restype = i32
+            L.osd_verify_tree.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp, sz, vp]
             L.osd_sample.restype = i32
             L.osd_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f32, vp, vp, vp]
             L.osd_shard_verify_stats.restype = i32
@@ -281,6 +289,71 @@ def osd_verify_distill(target_logits, draft_logits, draft_tokens, u_accept, u_re
     if st != OSD_OK:
         raise OsdError("osd_verify_distill", st)
     return acc, toks, rmask, loss, rows, g
+
+
+def osd_verify_distill_rejected(target_logits, draft_logits, draft_tokens, u_accept, u_resample, temperature,
+                                kind, beta=0.5, draft_len=None, grad=True, row_loss=True):
+    """Verification and distillation of the row at each sequence's first
+    rejection (the error index), in one pass through the C ABI: the results
+    of osd_verify(...) and of osd_distill_loss_grad with mask = reject_mask
+    at tau = temperature.  Returns what osd_verify_distill returns."""
+    torch = _torch()
+    B, K1, V = target_logits.shape
+    K = K1 - 1
+    _check_cuda(target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len)
+    dev = target_logits.device
+    for t in (target_logits, draft_logits, draft_tokens, u_accept, u_resample, draft_len):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if draft_tokens.dtype != torch.int32 or (draft_len is not None and draft_len.dtype != torch.int32):
+        raise TypeError("draft_tokens and draft_len must be int32")
+    if target_logits.dtype != draft_logits.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    kind_code = KINDS[kind] if isinstance(kind, str) else int(kind)
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    toks = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+    rmask = torch.empty(B, K, dtype=torch.uint8, device=dev)
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    rows = torch.empty(B, K, dtype=torch.float32, device=dev) if row_loss else None
+    g = torch.empty(B, K, V, dtype=draft_logits.dtype, device=dev) if grad else None
+    L = lib()
+    ws = workspace("verify_distill", L.osd_verify_distill_workspace_bytes(B, K), dev)
+    st = L.osd_verify_distill_rejected(_ptr(target_logits), _ptr(draft_logits), _dtype_code(target_logits), B, K,
+                                       V, _ptr(draft_tokens), _ptr(draft_len), _ptr(u_accept), _ptr(u_resample),
+                                       float(temperature), _ptr(acc), _ptr(toks), _ptr(rmask), kind_code,
+                                       float(beta), _ptr(loss), _ptr(rows), _ptr(g), _ptr(ws), ws.numel(),
+                                       _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_verify_distill_rejected", st)
+    return acc, toks, rmask, loss, rows, g
+
+
+def osd_verify_tree(target_logits, draft_logits, parent, node_tokens, u_accept, u_resample, temperature):
+    """Multi-candidate (tree) verification through the C ABI.  target_logits,
+    draft_logits [B, N, V] (draft may be None at temperature 0), parent and
+    node_tokens [B, N] int32, u_accept [B, N] and u_resample [B] float32 (None
+    at temperature 0).  Returns (accepted_len [B], out_tokens [B, N],
+    path_nodes [B, N])."""
+    torch = _torch()
+    B, N, V = target_logits.shape
+    _check_cuda(target_logits, draft_logits, parent, node_tokens, u_accept, u_resample)
+    dev = target_logits.device
+    for t in (target_logits, draft_logits, parent, node_tokens, u_accept, u_resample):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+    if parent.dtype != torch.int32 or node_tokens.dtype != torch.int32:
+        raise TypeError("parent and node_tokens must be int32")
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    toks = torch.empty(B, N, dtype=torch.int32, device=dev)
+    nodes = torch.empty(B, N, dtype=torch.int32, device=dev)
+    L = lib()
+    ws = workspace("verify_tree", L.osd_verify_tree_workspace_bytes(B, N), dev)
+    st = L.osd_verify_tree(_ptr(target_logits), _ptr(draft_logits), _dtype_code(target_logits), B, N, V,
+                           _ptr(parent), _ptr(node_tokens), _ptr(u_accept), _ptr(u_resample), float(temperature),
+                           _ptr(acc), _ptr(toks), _ptr(nodes), _ptr(ws), ws.numel(), _stream_handle(dev))
+    if st != OSD_OK:
+        raise OsdError("osd_verify_tree", st)
+    return acc, toks, nodes
 
 
 def osd_sample(p_logits, q_logits, temperature, beta, u=None, out=None):

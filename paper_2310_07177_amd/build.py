@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libosd.so")
 SOURCES = ["osd_api.hip", "verify.hip", "distill.hip", "verify_greedy.hip", "distill_stream.hip", "verify_distill.hip",
-           "sample.hip", "verify_shard.hip"]
+           "sample.hip", "verify_shard.hip", "verify_tree.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -355,12 +355,13 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
 template <typename Fmt, int W, int CPT, bool VEC>
 hipError_t launch_kind(const DistillLaunch& L, const DistillArgs& a) {
     const dim3 grid(unsigned(L.B) * unsigned(L.K)), block(W);
+    hipError_t e;
     switch (L.kind) {
-        case 0: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 0>), grid, block, 0, L.stream, a); break;
-        case 1: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 1>), grid, block, 0, L.stream, a); break;
-        default: hipLaunchKernelGGL((distill_kernel<Fmt, W, CPT, VEC, 2>), grid, block, 0, L.stream, a); break;
+        case 0: e = launch_kernel(&distill_kernel<Fmt, W, CPT, VEC, 0>, grid, block, 0, L.stream, a); break;
+        case 1: e = launch_kernel(&distill_kernel<Fmt, W, CPT, VEC, 1>, grid, block, 0, L.stream, a); break;
+        default: e = launch_kernel(&distill_kernel<Fmt, W, CPT, VEC, 2>, grid, block, 0, L.stream, a); break;
     }
-    return hipGetLastError();
+    return e;
 }
 
 template <typename Fmt, int W, int CPT>

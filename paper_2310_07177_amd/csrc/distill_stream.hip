@@ -342,8 +342,8 @@ hipError_t launch_kind(const DistillLaunch& L, const StreamDistillArgs& a) {
     const int64_t min_grid = (int64_t(a.nrows) + W - 1) / W;
     if (want < min_grid) want = min_grid;
     const unsigned grid = unsigned(want < a.nrows ? want : a.nrows);
-    hipLaunchKernelGGL((distill_stream_kernel<Fmt, W, CPT, KIND>), dim3(grid), dim3(W), 0, L.stream, a);
-    return hipGetLastError();
+    const hipError_t e = launch_kernel(&distill_stream_kernel<Fmt, W, CPT, KIND>, dim3(grid), dim3(W), 0, L.stream, a);
+    return e;
 }
 
 template <typename Fmt, int W, int CPT>

@@ -53,18 +53,22 @@ DistillWs distill_layout(int B, int K) {
     return w;
 }
 
-// The fused entry point: the verify workspace, then the distill workspace
-// (both used as they are by the two-call path), then per-workgroup loss
-// partials of the fused kernel (at most one per item).
+// The fused entry points: the verify workspace, then the distill workspace
+// (both used as they are by the two-call path; the fused kernel keeps its
+// per-position decisions where the greedy partials go), then per-workgroup
+// loss partials of the fused kernel (at most one per item; per-row losses in
+// the error-index mode), then a [B, K] mask for the error-index mode's
+// two-call path when the caller passes no reject_mask.
 struct FusedWs {
-    size_t verify, distill, part, total;
+    size_t verify, distill, part, mask, total;
 };
 FusedWs fused_layout(int B, int K) {
     FusedWs w;
     w.verify = 0;
     w.distill = round_up(verify_layout(B, K).total, kAlign);
     w.part = w.distill + round_up(distill_layout(B, K).total, kAlign);
-    w.total = w.part + round_up(size_t(B) * size_t(K + 1) * 8, kAlign);
+    w.mask = w.part + round_up(size_t(B) * size_t(K + 1) * 8, kAlign);
+    w.total = w.mask + round_up(size_t(B) * size_t(K), kAlign);
     return w;
 }
 
@@ -83,6 +87,17 @@ int device_cus(hipStream_t stream) {
         __atomic_store_n(&cache[dev], n, __ATOMIC_RELAXED);
     }
     return n;
+}
+
+// Zero n 32-bit words (a kernel rather than a memset: it may be captured
+// into a graph).
+__global__ void clear_words(uint32_t* p, int n) {
+    for (int i = int(blockIdx.x * blockDim.x + threadIdx.x); i < n; i += int(gridDim.x * blockDim.x)) p[i] = 0u;
+}
+
+hipError_t launch_clear_words(uint32_t* p, int n, hipStream_t s) {
+    const int threads = 256, want = (n + threads - 1) / threads, blocks = want < 1024 ? (want > 0 ? want : 1) : 1024;
+    return osd::launch_kernel(&clear_words, dim3(blocks), dim3(threads), 0, s, p, n);
 }
 
 bool sizes_ok(int B, int K, int V, int dtype) {
@@ -232,13 +247,18 @@ size_t osd_verify_distill_workspace_bytes(int B, int K) {
     return fused_layout(B, K).total;
 }
 
-int osd_verify_distill(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
-                       int V, const int32_t* draft_tokens, const int32_t* draft_len,
-                       const float* u_accept, const float* u_resample, float temperature,
-                       int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
-                       const uint8_t* distill_mask, int kind, float beta, float* loss_out,
-                       float* row_loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Both fused entry points: erridx = 0 distils the caller's mask, 1 the row
+// at each sequence's first rejection (the error index).
+int verify_distill_impl(const void* target_logits, const void* draft_logits, int dtype, int B, int K, int V,
+                        const int32_t* draft_tokens, const int32_t* draft_len, const float* u_accept,
+                        const float* u_resample, float temperature, int32_t* accepted_len, int32_t* out_tokens,
+                        uint8_t* reject_mask, const uint8_t* distill_mask, int erridx, int kind, float beta,
+                        float* loss_out, float* row_loss_out, void* grad_out, void* workspace,
+                        size_t workspace_bytes, void* stream) {
     if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
     if (B <= 0 || K <= 0 || V <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
     if (!sizes_ok(B, K, V, dtype)) return OSD_ERR_UNSUPPORTED;
@@ -259,13 +279,22 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
     if (!fused) {  // the two calls, each on its own part of the workspace
         const VerifyWs vw = verify_layout(B, K);
         const DistillWs dw = distill_layout(B, K);
+        uint8_t* rmask = reject_mask;
+        if (erridx && !rmask) rmask = reinterpret_cast<uint8_t*>(w + ws.mask);
         int st = osd_verify(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept,
-                            u_resample, temperature, accepted_len, out_tokens, reject_mask, w + ws.verify,
-                            vw.total, stream);
+                            u_resample, temperature, accepted_len, out_tokens, rmask, w + ws.verify, vw.total,
+                            stream);
         if (st != OSD_OK) return st;
-        return osd_distill_loss_grad(target_logits, int64_t(K + 1) * V, draft_logits, int64_t(K) * V, dtype, B,
-                                     K, V, distill_mask, kind, beta, temperature, loss_out, row_loss_out,
-                                     grad_out, w + ws.distill, dw.total, stream);
+        st = osd_distill_loss_grad(target_logits, int64_t(K + 1) * V, draft_logits, int64_t(K) * V, dtype, B, K, V,
+                                   erridx ? rmask : distill_mask, kind, beta, temperature, loss_out, row_loss_out,
+                                   grad_out, w + ws.distill, dw.total, stream);
+        if (st != OSD_OK || rmask == reject_mask) return st;
+        // The mask kept in the workspace: every call leaves its workspace zero.
+        const int words = int((size_t(B) * size_t(K) + 3) / 4);
+        return launch_clear_words(reinterpret_cast<uint32_t*>(rmask), words, static_cast<hipStream_t>(stream)) ==
+                       hipSuccess
+                   ? OSD_OK
+                   : OSD_ERR_DEVICE;
     }
     osd::FusedLaunch L;
     L.target = target_logits;
@@ -279,7 +308,7 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
     L.u_accept = u_accept;
     L.u_resample = u_resample;
     L.temperature = temperature;
-    L.mask = distill_mask;
+    L.mask = erridx ? nullptr : distill_mask;
     L.kind = kind;
     L.beta = beta;
     L.accepted_len = accepted_len;
@@ -288,12 +317,42 @@ int osd_verify_distill(const void* target_logits, const void* draft_logits, int 
     L.loss_out = loss_out;
     L.row_loss_out = row_loss_out;
     L.grad_out = grad_out;
-    L.records = reinterpret_cast<uint32_t*>(w + ws.verify + verify_layout(B, K).records);
+    const VerifyWs vw = verify_layout(B, K);
+    L.records = reinterpret_cast<uint32_t*>(w + ws.verify + vw.records);
+    L.dec = reinterpret_cast<uint32_t*>(w + ws.verify + vw.stats);
+    L.erridx = erridx;
     L.done = reinterpret_cast<uint32_t*>(w + ws.distill + distill_layout(B, K).done);
     L.part_ws = reinterpret_cast<double*>(w + ws.part);
     L.stream = static_cast<hipStream_t>(stream);
     L.cus = device_cus(L.stream);
     return osd::launch_verify_distill(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" {
+
+int osd_verify_distill(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
+                       int V, const int32_t* draft_tokens, const int32_t* draft_len,
+                       const float* u_accept, const float* u_resample, float temperature,
+                       int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask,
+                       const uint8_t* distill_mask, int kind, float beta, float* loss_out,
+                       float* row_loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return verify_distill_impl(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept,
+                               u_resample, temperature, accepted_len, out_tokens, reject_mask, distill_mask, 0,
+                               kind, beta, loss_out, row_loss_out, grad_out, workspace, workspace_bytes, stream);
+}
+
+int osd_verify_distill_rejected(const void* target_logits, const void* draft_logits, int dtype, int B, int K,
+                                int V, const int32_t* draft_tokens, const int32_t* draft_len,
+                                const float* u_accept, const float* u_resample, float temperature,
+                                int32_t* accepted_len, int32_t* out_tokens, uint8_t* reject_mask, int kind,
+                                float beta, float* loss_out, float* row_loss_out, void* grad_out,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+    return verify_distill_impl(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept,
+                               u_resample, temperature, accepted_len, out_tokens, reject_mask, nullptr, 1, kind,
+                               beta, loss_out, row_loss_out, grad_out, workspace, workspace_bytes, stream);
 }
 
 int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits, int64_t q_row_stride,
@@ -453,12 +512,6 @@ std::once_flag g_scratch_once[kMaxDevices];
 void* g_scratch_ptr[kMaxDevices];
 hipError_t g_scratch_err[kMaxDevices];
 
-// Zero n 32-bit words (a kernel rather than a memset: it may be captured
-// into a graph).
-__global__ void clear_words(uint32_t* p, int n) {
-    for (int i = int(blockIdx.x * blockDim.x + threadIdx.x); i < n; i += int(gridDim.x * blockDim.x)) p[i] = 0u;
-}
-
 // The device address of `scratch` on device dev (nullptr on failure).
 void* scratch_on(int dev) {
     if (dev < 0 || dev >= kMaxDevices) return nullptr;
@@ -503,10 +556,75 @@ extern "C" int osd_verify_noalloc(const void* target_logits, const void* draft_l
     // leave them zero, but the array keeps whatever the previous call on this
     // GPU left, so they are cleared here on the call's own stream.  (The
     // greedy partials are written before they are read.)
-    const int words = int(ws.stats / 4);
-    const int threads = 256, blocks = (words + threads - 1) / threads < 1024 ? (words + threads - 1) / threads : 1024;
-    hipLaunchKernelGGL(clear_words, dim3(blocks), dim3(threads), 0, s, static_cast<uint32_t*>(ptr), words);
-    if (hipGetLastError() != hipSuccess) return OSD_ERR_DEVICE;
+    if (launch_clear_words(static_cast<uint32_t*>(ptr), int(ws.stats / 4), s) != hipSuccess) return OSD_ERR_DEVICE;
     return osd_verify(target_logits, draft_logits, dtype, B, K, V, draft_tokens, draft_len, u_accept, u_resample,
                       temperature, accepted_len, out_tokens, reject_mask, ptr, ws.total, stream);
 }
+
+// ---------------------------------------------------------------------------
+// Multi-candidate (tree) verification.
+// ---------------------------------------------------------------------------
+namespace {
+
+struct TreeWs {
+    size_t counters, records, total;
+};
+TreeWs tree_layout(int B, int N) {
+    TreeWs w;
+    w.counters = 0;
+    w.records = round_up(size_t(B) * 4, kAlign);
+    w.total = w.records + round_up(size_t(B) * size_t(N) * 4, kAlign);
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t osd_verify_tree_workspace_bytes(int B, int N) {
+    if (B <= 0 || N <= 0 || N > OSD_MAX_TREE_NODES) return 0;
+    if (int64_t(B) * int64_t(N) > 0x7FFFFFFFll) return 0;
+    return tree_layout(B, N).total;
+}
+
+int osd_verify_tree(const void* target_logits, const void* draft_logits, int dtype, int B, int N, int V,
+                    const int32_t* parent, const int32_t* node_tokens, const float* u_accept,
+                    const float* u_resample, float temperature, int32_t* accepted_len, int32_t* out_tokens,
+                    int32_t* path_nodes, void* workspace, size_t workspace_bytes, void* stream) {
+    if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
+    if (B <= 0 || N <= 0 || V <= 0 || N > OSD_MAX_TREE_NODES) return OSD_ERR_INVALID_ARG;
+    if (int64_t(B) * int64_t(N) > 0x7FFFFFFFll) return OSD_ERR_INVALID_ARG;
+    osd::RowTile t;
+    if (!osd::pick_tree_tile(V, per_chunk(dtype), &t)) return OSD_ERR_UNSUPPORTED;
+    if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
+    const bool greedy = temperature == 0.0f;
+    if (!target_logits || !parent || !node_tokens || !accepted_len || !out_tokens) return OSD_ERR_INVALID_ARG;
+    if (!greedy && (!draft_logits || !u_accept || !u_resample)) return OSD_ERR_INVALID_ARG;
+    const TreeWs ws = tree_layout(B, N);
+    if (!workspace || workspace_bytes < ws.total || (reinterpret_cast<uintptr_t>(workspace) & 15u))
+        return OSD_ERR_WORKSPACE;
+    osd::TreeLaunch L;
+    L.target = target_logits;
+    L.draft = greedy ? nullptr : draft_logits;
+    L.dtype = dtype;
+    L.B = B;
+    L.N = N;
+    L.V = V;
+    L.parent = parent;
+    L.node_tokens = node_tokens;
+    L.u_accept = u_accept;
+    L.u_resample = u_resample;
+    L.temperature = temperature;
+    L.accepted_len = accepted_len;
+    L.out_tokens = out_tokens;
+    L.path_nodes = path_nodes;
+    char* w = static_cast<char*>(workspace);
+    L.counters = reinterpret_cast<uint32_t*>(w + ws.counters);
+    L.records = reinterpret_cast<uint32_t*>(w + ws.records);
+    L.vec = (int64_t(V) * elem_bytes(dtype)) % 16 == 0 && aligned16(target_logits) &&
+            (greedy || aligned16(draft_logits));
+    L.stream = static_cast<hipStream_t>(stream);
+    return osd::launch_verify_tree(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -10,6 +10,21 @@
 
 namespace osd {
 
+template <typename T>
+struct same_type {
+    using type = T;
+};
+
+// Enqueue kernel<<<grid, block, lds, stream>>>(args...) and return the status
+// of this launch alone (hipGetLastError would also report an earlier failure
+// of some other call made by the same thread).
+template <typename... P>
+inline hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                                typename same_type<P>::type... args) {
+    void* ptrs[] = {static_cast<void*>(&args)..., nullptr};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, lds, stream);
+}
+
 // Kernel tile shape chosen from V: W threads per workgroup, CPT 16-byte chunks
 // per thread per row.
 struct RowTile {
@@ -114,12 +129,36 @@ struct FusedLaunch {
     float* row_loss_out;
     void* grad_out;
     uint32_t* records;  // [B*(K+1)]     zero on entry and exit
+    uint32_t* dec;      // [B*(K+1)]     zero on entry and exit
+    int erridx;         // distil each sequence's first rejected row instead of `mask`
     double* part_ws;    // [B*(K+1)]     zero on entry and exit
     uint32_t* done;     // [1]           zero on entry and exit
     int cus;
     hipStream_t stream;
 };
 hipError_t launch_verify_distill(const FusedLaunch& L);
+
+// Multi-candidate (tree) verification: one workgroup per (sequence, node).
+struct TreeLaunch {
+    const void* target;  // [B, N, V]
+    const void* draft;   // [B, N, V]
+    int dtype;
+    int B, N, V;
+    const int32_t* parent;
+    const int32_t* node_tokens;
+    const float* u_accept;
+    const float* u_resample;
+    float temperature;
+    int32_t* accepted_len;
+    int32_t* out_tokens;
+    int32_t* path_nodes;
+    uint32_t* records;   // [B*N] zero on entry and exit
+    uint32_t* counters;  // [B]   zero on entry and exit
+    bool vec;
+    hipStream_t stream;
+};
+bool pick_tree_tile(int V, int per_chunk, RowTile* t);
+hipError_t launch_verify_tree(const TreeLaunch& L);
 
 // Token sampling: one workgroup per row, pi = beta softmax(p/T) +
 // (1 - beta) softmax(q/T) (a row with weight 0 is not read); T == 0 takes

@@ -174,11 +174,12 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void sample_kernel(S
 template <typename Fmt, int W, int CPT, int MODE>
 hipError_t launch_mode(const SampleLaunch& L, const SampleArgs& a) {
     const dim3 grid(unsigned(L.N)), block(W);
+    hipError_t e;
     if (L.vec)
-        hipLaunchKernelGGL((sample_kernel<Fmt, W, CPT, true, MODE>), grid, block, 0, L.stream, a);
+        e = launch_kernel(&sample_kernel<Fmt, W, CPT, true, MODE>, grid, block, 0, L.stream, a);
     else
-        hipLaunchKernelGGL((sample_kernel<Fmt, W, CPT, false, MODE>), grid, block, 0, L.stream, a);
-    return hipGetLastError();
+        e = launch_kernel(&sample_kernel<Fmt, W, CPT, false, MODE>, grid, block, 0, L.stream, a);
+    return e;
 }
 
 template <typename Fmt, int W, int CPT>

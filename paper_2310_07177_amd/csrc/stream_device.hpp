@@ -46,6 +46,12 @@ __device__ inline void store_chunk(rsrc_t r, int n, const chunk_t& c) {
                                            r, off, 0, kStreamAux);
 }
 
+// Chunk c of a row, whoever holds it (byte offset c*16).
+__device__ inline void store_chunk_at(rsrc_t r, int c, const chunk_t& v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) int, v), r, c * 16,
+                                           0, kStreamAux);
+}
+
 // Uniform (scalar-cache) loads of small per-row arguments.  The address must
 // be the same in every lane; the value lands in a scalar register and its
 // wait does not depend on the vector loads in flight.

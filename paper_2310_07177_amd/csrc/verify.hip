@@ -405,18 +405,19 @@ template <typename Fmt, int W, int CPT>
 hipError_t launch_tile(const VerifyLaunch& L, const VerifyArgs& a) {
     const dim3 grid(unsigned(L.B) * unsigned(L.K + 1)), block(W);
     const bool greedy = L.temperature == 0.0f;
+    hipError_t e;
     if (L.vec) {
         if (greedy)
-            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, true, true>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&verify_kernel<Fmt, W, CPT, true, true>, grid, block, 0, L.stream, a);
         else
-            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, true, false>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&verify_kernel<Fmt, W, CPT, true, false>, grid, block, 0, L.stream, a);
     } else {
         if (greedy)
-            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, false, true>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&verify_kernel<Fmt, W, CPT, false, true>, grid, block, 0, L.stream, a);
         else
-            hipLaunchKernelGGL((verify_kernel<Fmt, W, CPT, false, false>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&verify_kernel<Fmt, W, CPT, false, false>, grid, block, 0, L.stream, a);
     }
-    return hipGetLastError();
+    return e;
 }
 
 template <typename Fmt>

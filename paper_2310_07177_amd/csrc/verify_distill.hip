@@ -28,6 +28,8 @@
 // an earlier rejection of their sequence is known.  Each item posts a
 // one-word record; the last workgroup to finish reduces the loss and turns
 // the records of every sequence into the outputs.
+#include <stdlib.h>
+
 #include "osd.h"
 #include "osd_device.hpp"
 #include "osd_internal.hpp"
@@ -46,7 +48,14 @@ enum : uint32_t {
     kRecBadToken = 5,        // proposal outside [0, V)
     kRecBonus = 6,           // bonus token attached
     kRecBonusSkipped = 7,    // an earlier rejection was known
+    kRecRejectSpec = 8,      // rejected, correction attached, drawn before the
+                             // earlier positions' outcomes were known (in the
+                             // error-index mode its row was also distilled)
 };
+// Decision word of a tested position, posted as soon as the acceptance test
+// is taken (before the draw and the distillation), so that a later position
+// of the sequence can learn early whether it holds the first rejection.
+enum : uint32_t { kDecAccept = 1, kDecStop = 2 };
 __device__ inline uint32_t make_rec(uint32_t state, uint32_t tok) { return (state << 28) | (tok & 0x0FFFFFFFu); }
 
 // Masses are probabilities (at most 1 per element); chunk sums become exact
@@ -55,6 +64,13 @@ constexpr int kFixedShift = 40;
 // Items per workgroup (their arguments are staged in LDS) and the outcomes a
 // workgroup remembers.
 constexpr int kMaxItems = 256;
+// Looks at the earlier positions' decisions before a rejecting workgroup
+// draws without knowing whether it holds the first rejection.  Each look is
+// one device-coherent round trip plus a short sleep; the bound keeps every
+// wait finite whatever the dispatch order.  (The environment variable
+// OSD_FUSED_POLLS overrides it, for tests: 0 makes every such workgroup draw
+// without looking.)
+constexpr int kMaxPolls = 32;
 
 struct FusedArgs {
     const void* target;  // [B, K+1, V]
@@ -70,12 +86,15 @@ struct FusedArgs {
     float inv_tau;             // 1 / T
     float beta;
     uint32_t* records;         // [B, K+1], zero between calls
+    uint32_t* dec;             // [B, K+1] decisions, zero between calls
+    int erridx;                // distil the first rejected row of each sequence (not `mask`)
+    int max_polls;             // looks at the earlier decisions before drawing speculatively
     int32_t* accepted_len;
     int32_t* out_tokens;
     uint8_t* reject_mask;
     float* row_loss_out;       // [B, K] or null
     void* grad_out;            // [B, K, V] or null
-    double* part_ws;           // [G] loss partials, zero between calls
+    double* part_ws;           // [G] loss partials ([B*K] row losses in the error-index mode), zero between calls
     uint32_t* done;            // workgroups finished, zero between calls
     float* loss_out;
     int nitems;                // B*K + B
@@ -90,7 +109,7 @@ struct FusedArgs {
 struct Meta {
     int kb, y;
     float u, u_res;
-    int on;  // distillation mask flag
+    int on;  // distillation mask flag; in the error-index mode: every proposal of the sequence is in [0, V)
 };
 
 __device__ inline Meta load_meta(const FusedArgs& a, int it) {
@@ -104,7 +123,18 @@ __device__ inline Meta load_meta(const FusedArgs& a, int it) {
     m.y = bonus ? 0 : a.tokens[ti];
     m.u = bonus ? 0.0f : a.u_accept[ti];
     m.u_res = a.u_resample[b];
-    m.on = bonus ? 0 : (a.mask ? int(a.mask[ti]) : 1);
+    if (a.erridx) {
+        // A proposal outside the vocabulary invalidates the whole sequence,
+        // wherever it sits: its rejected row is then not distilled.
+        int ok = m.kb >= 1 && m.kb <= a.K;
+        for (int j = 0; ok && j < m.kb; ++j) {
+            const int32_t yj = a.tokens[int64_t(b) * a.K + j];
+            ok = yj >= 0 && yj < a.V;
+        }
+        m.on = ok;
+    } else {
+        m.on = bonus ? 0 : (a.mask ? int(a.mask[ti]) : 1);
+    }
     return m;
 }
 
@@ -125,7 +155,8 @@ struct Item {
     int b, i;
     bool bonus;
     int vkind;    // verification: none, bad token or live
-    bool dist;    // distillation row with mask 1
+    bool dist;    // distillation row with mask 1 (error-index mode: decided after the test)
+    bool seq_ok;  // error-index mode: every proposal of the sequence is valid
     int y;
     float u, u_res;
     const char* trow;
@@ -138,6 +169,7 @@ __device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
     Item t;
     t.vkind = kItemNone;
     t.dist = false;
+    t.seq_ok = a.erridx ? m.on != 0 : true;
     t.trow = nullptr;
     t.drow = nullptr;
     t.grow = -1;
@@ -153,7 +185,7 @@ __device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
     const bool kb_ok = m.kb >= 1 && m.kb <= a.K;
     if (!t.bonus) {
         t.grow = t.b * a.K + i;
-        t.dist = m.on != 0;
+        t.dist = !a.erridx && m.on != 0;
         if (kb_ok && i < m.kb) t.vkind = (m.y < 0 || m.y >= a.V) ? kItemBadToken : kItemLive;
     } else if (kb_ok) {
         t.vkind = kItemLive;
@@ -182,6 +214,20 @@ __device__ inline bool known_rejection_ahead(const uint8_t* s_rej, int k, int se
     int kk = k - seq_step;
     while (kk > k - 3) kk -= seq_step;
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
+}
+
+// Wave 0: the decisions of positions 0..i-1 of one sequence (lane j:
+// position j).  2 if one of them stopped the test, 1 if all accepted, 0 if
+// still undecided after kMaxPolls looks.
+__device__ inline int poll_decisions(const uint32_t* dec, int i, int polls) {
+    const int lane = opaque_tid() & (kWave - 1);
+    for (int p = 0; p < polls; ++p) {
+        if (p > 0) __builtin_amdgcn_s_sleep(8);
+        const uint32_t d = lane < i ? load_relaxed(&dec[lane]) : uint32_t(kDecAccept);
+        if (__ballot(d == kDecStop) != 0) return 2;
+        if (__ballot(d != kDecAccept) == 0) return 1;
+    }
+    return 0;
 }
 
 // Inverse-CDF draw over the cached row pair.  mass(r, e, residual) gives the
@@ -275,13 +321,25 @@ struct FusedTail {
     const uint8_t* mask;
     int nrows;
     uint32_t* records;
+    uint32_t* dec;
     const int32_t* draft_len;
     const int32_t* tokens;
     int32_t* accepted_len;
     int32_t* out_tokens;
     uint8_t* reject_mask;
+    float* row_loss_out;
+    void* grad_out;
+    uint32_t row_bytes;
+    int erridx;
     int B, K;
 };
+
+// Rows whose gradient the last workgroup clears (error-index mode): rows
+// distilled before the earlier positions' outcomes were known that turn out
+// not to hold the first rejection.  One pass of the finalizer covers at most
+// W/16 sequences of at most 15 proposals or W/32 of 16, so at most 1024 rows
+// at W = 1024: the list is emptied after every pass.
+constexpr int kMaxExtraRows = 1024;
 
 // Every workgroup posts its loss partial and arrives; the last one
 //  - turns each sequence's records into the outputs (one segment of 16 or
@@ -290,15 +348,22 @@ struct FusedTail {
 //    vocabulary invalidates the sequence wherever it sits, a row without
 //    finite logits only if the test reaches it;
 //  - adds the partials in workgroup order and counts the mask (fixed order,
-//    fp64), writing {mean, sum};
-//  - reads every record and partial with an exchange that leaves zero.
+//    fp64), writing {mean, sum}; in the error-index mode it adds instead
+//    the divergence of each sequence's first rejected row, in sequence
+//    order, and clears the gradient rows and row losses of rows that were
+//    distilled speculatively and turn out not to be first;
+//  - reads every record, decision and partial with an exchange that leaves
+//    zero.
 // All of a pass's reads are issued before any is used (one round trip per
 // pass; positions beyond k_b were never posted and read as zero).
 template <int W>
 __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     constexpr int NW = W / kWave;
+    static_assert(W <= kMaxExtraRows, "one pass adds at most one row per thread to the list");
     __shared__ int s_last;
     __shared__ double s_sum[NW], s_cnt[NW];
+    __shared__ int s_nextra;
+    __shared__ int s_extra[kMaxExtraRows];
     // Thread indices from an opaque copy: nothing derived from them before
     // the item loop is kept alive across it.
     int tid = threadIdx.x;
@@ -307,24 +372,35 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     const int G = gridDim.x;
     __syncthreads();
     if (tid == 0) {
-        __hip_atomic_exchange(&a.part_ws[blockIdx.x], s_part[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (!a.erridx)
+            __hip_atomic_exchange(&a.part_ws[blockIdx.x], s_part[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = int(arrive(a.done)) == G - 1;  // after this workgroup's posts completed
+        s_nextra = 0;
     }
     __syncthreads();
     if (!s_last) return;
+    // Error-index mode: rows distilled speculatively were released to memory
+    // before their records were posted; see them before clearing any.
+    if (a.erridx) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     const int K = a.K;
     const int seg = K + 1 <= 16 ? 16 : 32;  // K <= 16
     const int per_pass = W / seg;
     const int j = tid & (seg - 1), base = lane & ~(seg - 1);
     const uint64_t segmask = (seg == 32 ? 0xFFFFFFFFull : 0xFFFFull) << base;
+    const int nchunks = int(a.row_bytes / 16);
+    double esum = 0.0, ecnt = 0.0;  // error-index mode: this thread's sequences, in order
     for (int b0 = 0; b0 < a.B; b0 += per_pass) {
         const int b = b0 + tid / seg;
         const bool on = b < a.B;
         const int kb = on ? (a.draft_len ? a.draft_len[b] : K) : 0;
         const uint32_t r = on && j <= K ? take_u32(&a.records[int64_t(b) * (K + 1) + j]) : 0u;
+        if (on && j < K) take_u32(&a.dec[int64_t(b) * (K + 1) + j]);
         const int32_t tk = on && j < K ? a.tokens[int64_t(b) * K + j] : -1;
         const bool kb_ok = kb >= 1 && kb <= K;
         const uint32_t st = r >> 28;
+        const bool drew = st == kRecReject || st == kRecRejectSpec;
+        double dj = 0.0;
+        if (a.erridx && on && j < K && drew) dj = take_f64(&a.part_ws[int64_t(b) * K + j]);
         const bool bad_token = (__ballot(j < kb && st == kRecBadToken) & segmask) != 0;
         const uint64_t stop = (__ballot(j < kb && st != kRecAccept) & segmask) >> base;
         const int acc = stop ? __builtin_ctzll(stop) : kb;
@@ -333,7 +409,7 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
         bool bad = !kb_ok || bad_token;
         int extra = -1;
         if (!bad) {
-            if (acc < kb ? sa == kRecReject : sa == kRecBonus)
+            if (acc < kb ? (sa == kRecReject || sa == kRecRejectSpec) : sa == kRecBonus)
                 extra = int(ra & 0x0FFFFFFFu);
             else
                 bad = true;  // a row without finite logits where the test stopped
@@ -345,10 +421,38 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
                 a.reject_mask[int64_t(b) * K + j] = (!bad && j == acc && acc < kb) ? 1 : 0;
             if (j == 0) a.accepted_len[b] = bad ? -1 : acc;
         }
+        if (a.erridx && on && j < K && drew) {
+            if (!bad && j == acc) {
+                esum += dj;  // the first rejection: its row is the one distilled
+                ecnt += 1.0;
+            } else {
+                // distilled speculatively, not first: its outputs become zero
+                if (a.row_loss_out) a.row_loss_out[int64_t(b) * K + j] = 0.0f;
+                s_extra[atomicAdd(&s_nextra, 1)] = b * K + j;
+            }
+        }
+        if (a.erridx) {
+            __syncthreads();
+            const int n = s_nextra;
+            if (n > 0 && a.grad_out) {
+                for (int e = 0; e < n; ++e) {
+                    const rsrc_t gr =
+                        make_rsrc(static_cast<char*>(a.grad_out) + int64_t(s_extra[e]) * a.row_bytes, a.row_bytes);
+                    for (int c = tid; c < nchunks; c += W) store_chunk_at(gr, c, chunk_t{0u, 0u, 0u, 0u});
+                }
+            }
+            __syncthreads();
+            if (tid == 0) s_nextra = 0;
+        }
     }
     double sm = 0.0, cn = 0.0;
-    for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
-    for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
+    if (a.erridx) {
+        sm = esum;
+        cn = ecnt;
+    } else {
+        for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
+        for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
+    }
     sm = wave_sum(sm);
     cn = wave_sum(cn);
     if (lane == 0) {
@@ -410,6 +514,11 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         s_tail.mask = a.mask;
         s_tail.nrows = a.B * a.K;
         s_tail.records = a.records;
+        s_tail.dec = a.dec;
+        s_tail.row_loss_out = a.row_loss_out;
+        s_tail.grad_out = a.grad_out;
+        s_tail.row_bytes = a.row_bytes;
+        s_tail.erridx = a.erridx;
         s_tail.draft_len = a.draft_len;
         s_tail.tokens = a.tokens;
         s_tail.accepted_len = a.accepted_len;
@@ -472,20 +581,18 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         const rsrc_t nsr = make_rsrc(nload && nxt.drow ? nxt.drow : a.target, nload && nxt.drow ? a.row_bytes : 0u);
         if (k >= 0) cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
         // A bonus row is needed only if every proposal of its sequence is
-        // accepted.  Besides this workgroup's own outcomes, the records that
-        // any workgroup has posted so far are consulted (each is written
-        // once per call; zero: not posted yet): one that is not an
-        // acceptance means the row is not needed.  Wave 0 reads them
-        // (k_b <= 16 lanes); the bonus rows come last, when most are posted.
+        // accepted.  Besides this workgroup's own outcomes, the decisions
+        // that any workgroup has posted so far are consulted (each is
+        // written once per call; zero: not posted yet): a stop means the row
+        // is not needed.  Wave 0 reads them (k_b <= 16 lanes); the bonus
+        // rows come last, when most are posted.
         bool bonus_stop = false;
         if (cur.bonus && cur.vkind == kItemLive && !cur_skip && k >= 0) {
             const int t = opaque_tid();  // nothing tid-derived is kept across the loop
             if (t < kWave) {
-                uint32_t r = 0u;
-                if (t < cur.i)
-                    r = __hip_atomic_load(&a.records[int64_t(cur.b) * (a.K + 1) + t], __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-                const uint64_t m = __ballot(r != 0u && (r >> 28) != kRecAccept);
+                uint32_t d = 0u;
+                if (t < cur.i) d = load_relaxed(&a.dec[int64_t(cur.b) * (a.K + 1) + t]);
+                const uint64_t m = __ballot(d == kDecStop);
                 if (t == 0) s_flag[k & 1] = m != 0 ? 1 : 0;
             }
             __syncthreads();
@@ -564,9 +671,13 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         // replaces it below.  Its row may still be distilled.
         uint32_t record = 0u;
         bool stopped = false;  // this item ended the test (or could not be tested)
+        bool distilled = false;
+        bool release_rows = false;  // error-index mode: this item's outputs may be cleared by the last workgroup
+        uint32_t* const dec_at = a.dec + int64_t(cur.b) * (a.K + 1) + cur.i;
         if (cur.vkind == kItemBadToken) {
             record = make_rec(kRecBadToken, 0);
             stopped = true;
+            if (opaque_tid() == 0 && k >= 0) __hip_atomic_exchange(dec_at, uint32_t(kDecStop), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         } else if (cur.vkind == kItemLive && !vlive) {
             record = make_rec(kRecBonusSkipped, 0);
             stopped = true;
@@ -601,6 +712,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             const float dTk = float(dTd - double(kc_t - kc_s));
 
             // ---- verification ----
+            bool spec = false;  // drew without knowing the earlier positions' outcomes
             if (vlive) {
                 const bool bad = !(St > 0.0 && St < 1.0e300) || (!cur.bonus && !(Ss > 0.0 && Ss < 1.0e300));
                 const bool earlier = known_rejection(s_rej, k, a.seq_step);
@@ -608,6 +720,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 if (bad) {
                     record = make_rec(kRecBadRow, 0);
                     stopped = true;
+                    if (!cur.bonus && opaque_tid() == 0)
+                        __hip_atomic_exchange(dec_at, uint32_t(kDecStop), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 } else if (!cur.bonus) {
                     // p(y)/q(y) = 2^e with e = (t_y - d_y) c2 - (T_t - T_s)
                     // in fp64; 2^e is split into an exact power of two and
@@ -623,9 +737,27 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         ratio = __builtin_ldexp(double(exp2_fast(float(e - fl))), int(fl));
                     }
                     const bool accept = double(cur.u) < ratio;
+                    // Posted now, so that later positions learn it before
+                    // this item's draw and distillation.
+                    if (opaque_tid() == 0)
+                        __hip_atomic_exchange(dec_at, uint32_t(accept ? kDecAccept : kDecStop), __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
                     stopped = !accept;
-                    want_draw = !accept && !earlier;
+                    want_draw = !accept && !earlier && cur.seq_ok;
                     record = accept ? make_rec(kRecAccept, 0) : make_rec(kRecRejectSkipped, 0);
+                    if (want_draw && cur.i > 0) {
+                        // Only the first rejection of a sequence draws (and,
+                        // in the error-index mode, is distilled): wave 0
+                        // looks at the earlier positions' decisions.
+                        if (opaque_tid() < kWave) {
+                            const int st = poll_decisions(a.dec + int64_t(cur.b) * (a.K + 1), cur.i, a.max_polls);
+                            if (opaque_tid() == 0) s_flag[k & 1] = st;
+                        }
+                        __syncthreads();
+                        const int st = s_flag[k & 1];
+                        want_draw = st != 2;
+                        spec = st == 0;
+                    }
                 } else {
                     stopped = true;
                     want_draw = !earlier;
@@ -665,13 +797,19 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     if (tok < 0 || tok >= a.V)
                         record = make_rec(kRecBadRow, 0);
                     else
-                        record = make_rec(cur.bonus ? kRecBonus : kRecReject, uint32_t(tok));
+                        record = make_rec(cur.bonus ? kRecBonus : (spec ? kRecRejectSpec : kRecReject), uint32_t(tok));
                 }
                 stopped = stopped || earlier;
             }
+            // The error-index mode distils the row whose draw made the
+            // correction (the first rejection, or a speculative one).
+            const uint32_t rst = record >> 28;
+            const bool dist_now = a.erridx ? (rst == kRecReject || rst == kRecRejectSpec) : cur.dist;
+            distilled = dist_now;
+            release_rows = a.erridx && spec && dist_now;
 
             // ---- distillation ----
-            if (cur.dist) {
+            if (dist_now) {
                 float acc0 = 0.0f, acc1 = 0.0f;
 #pragma unroll
                 for (int r = 0; r < CPT; ++r) {
@@ -764,11 +902,21 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 for (int r = 0; r < CPT; ++r) store_chunk<W>(gr, r, chunk_t{0u, 0u, 0u, 0u});
             }
         }
+        if (release_rows) {  // every wave's gradient stores complete before the release below
+            wait_memory();
+            __syncthreads();
+        }
         if (tid == 0 && k >= 0) {
             if (cur.grow >= 0) {
                 if (a.row_loss_out) a.row_loss_out[cur.grow] = float(D);
-                s_part[0] += D;  // this workgroup's rows, in item order
+                if (!a.erridx)
+                    s_part[0] += D;  // this workgroup's rows, in item order
+                else if (distilled)  // the last workgroup adds the first rejections' in sequence order
+                    __hip_atomic_exchange(&a.part_ws[cur.grow], D, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            // A speculative row's outputs are written back to memory before
+            // its record says so: the last workgroup may overwrite them.
+            if (release_rows) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
             if (cur.vkind != kItemNone)  // posted at the coherence point; waited for once, at the end
                 __hip_atomic_exchange(&a.records[int64_t(cur.b) * (a.K + 1) + cur.i], record, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
@@ -803,8 +951,8 @@ hipError_t launch_kind(const FusedLaunch& L, FusedArgs a) {
         r = t;
     }
     a.seq_step = a.B / g;
-    hipLaunchKernelGGL((verify_distill_kernel<Fmt, W, CPT, KIND>), dim3(grid), dim3(W), 0, L.stream, a);
-    return hipGetLastError();
+    const hipError_t e = launch_kernel(&verify_distill_kernel<Fmt, W, CPT, KIND>, dim3(grid), dim3(W), 0, L.stream, a);
+    return e;
 }
 
 template <typename Fmt, int W, int CPT>
@@ -833,6 +981,17 @@ hipError_t launch_fmt(const FusedLaunch& L, const FusedArgs& a) {
 
 }  // namespace
 
+// kMaxPolls, or the value of OSD_FUSED_POLLS (read once).
+int fused_max_polls() {
+    static const int v = [] {
+        const char* e = getenv("OSD_FUSED_POLLS");
+        if (e == nullptr || *e == 0) return kMaxPolls;
+        const int n = atoi(e);
+        return n < 0 ? kMaxPolls : (n > 4096 ? 4096 : n);
+    }();
+    return v;
+}
+
 hipError_t launch_verify_distill(const FusedLaunch& L) {
     FusedArgs a;
     a.target = L.target;
@@ -850,6 +1009,9 @@ hipError_t launch_verify_distill(const FusedLaunch& L) {
     a.inv_tau = float(1.0 / double(L.temperature));
     a.beta = L.beta;
     a.records = L.records;
+    a.dec = L.dec;
+    a.erridx = L.erridx;
+    a.max_polls = fused_max_polls();
     a.accepted_len = L.accepted_len;
     a.out_tokens = L.out_tokens;
     a.reject_mask = L.reject_mask;

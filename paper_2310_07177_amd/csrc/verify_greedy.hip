@@ -203,14 +203,16 @@ hipError_t launch_fmt(const VerifyLaunch& L, SegArgs a) {
     for (int64_t f = 0; f < units; f += kMaxGrid) {
         a.first = f;
         const unsigned g = unsigned(units - f < kMaxGrid ? units - f : kMaxGrid);
-        hipLaunchKernelGGL((verify_greedy_stats<Fmt, 4>), dim3(g), dim3(kW), 0, L.stream, a);
+        const hipError_t e = launch_kernel(&verify_greedy_stats<Fmt, 4>, dim3(g), dim3(kW), 0, L.stream, a);
+        if (e != hipSuccess) return e;
     }
     for (int64_t f = 0; f < a.B; f += kMaxGrid) {
         a.first = f;
         const unsigned g = unsigned(a.B - f < kMaxGrid ? a.B - f : kMaxGrid);
-        hipLaunchKernelGGL((verify_greedy_decide<Fmt>), dim3(g), dim3(kW), 0, L.stream, a);
+        const hipError_t e = launch_kernel(&verify_greedy_decide<Fmt>, dim3(g), dim3(kW), 0, L.stream, a);
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace

@@ -510,30 +510,31 @@ hipError_t launch_tile(const ShardLaunch& L) {
     const bool greedy = L.temperature == 0.0f;
     const float c2 = greedy ? 0.0f : float(1.4426950408889634 / double(L.temperature));
     const dim3 block(W);
+    hipError_t e;
     if (L.phase == 1) {
         StatsArgs a{L.target, L.draft, L.B, L.K, L.Vs, L.v_begin, L.V, L.tokens, L.draft_len, c2, L.stats};
         const dim3 grid(unsigned(L.B) * unsigned(L.K + 1));
         if (greedy)
-            hipLaunchKernelGGL((shard_stats_kernel<Fmt, W, CPT, VEC, true>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&shard_stats_kernel<Fmt, W, CPT, VEC, true>, grid, block, 0, L.stream, a);
         else
-            hipLaunchKernelGGL((shard_stats_kernel<Fmt, W, CPT, VEC, false>), grid, block, 0, L.stream, a);
+            e = launch_kernel(&shard_stats_kernel<Fmt, W, CPT, VEC, false>, grid, block, 0, L.stream, a);
     } else if (L.phase == 2) {
         MassArgs a{L.target, L.draft, L.B, L.K, L.Vs, L.G, L.tokens, L.draft_len, L.u_accept, c2, double(c2),
                    L.stats_in, L.mass};
         const size_t lds = size_t(L.G) * size_t(L.K + 1) * sizeof(osd_shard_row_stats);
         if (greedy)
-            hipLaunchKernelGGL((shard_mass_kernel<Fmt, W, CPT, VEC, true>), dim3(L.B), block, lds, L.stream, a);
+            e = launch_kernel(&shard_mass_kernel<Fmt, W, CPT, VEC, true>, dim3(L.B), block, lds, L.stream, a);
         else
-            hipLaunchKernelGGL((shard_mass_kernel<Fmt, W, CPT, VEC, false>), dim3(L.B), block, lds, L.stream, a);
+            e = launch_kernel(&shard_mass_kernel<Fmt, W, CPT, VEC, false>, dim3(L.B), block, lds, L.stream, a);
     } else {
         DrawArgs a{L.target, L.draft, L.B, L.K, L.Vs, L.v_begin, L.G, L.shard, L.tokens, L.draft_len,
                    L.u_resample, c2, L.mass_in, L.accepted_len, L.out_tokens, L.reject_mask};
         if (greedy)
-            hipLaunchKernelGGL((shard_draw_kernel<Fmt, W, CPT, VEC, true>), dim3(L.B), block, 0, L.stream, a);
+            e = launch_kernel(&shard_draw_kernel<Fmt, W, CPT, VEC, true>, dim3(L.B), block, 0, L.stream, a);
         else
-            hipLaunchKernelGGL((shard_draw_kernel<Fmt, W, CPT, VEC, false>), dim3(L.B), block, 0, L.stream, a);
+            e = launch_kernel(&shard_draw_kernel<Fmt, W, CPT, VEC, false>, dim3(L.B), block, 0, L.stream, a);
     }
-    return hipGetLastError();
+    return e;
 }
 
 template <typename Fmt, bool VEC>

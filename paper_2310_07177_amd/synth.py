@@ -245,3 +245,61 @@ def to_host_sample(x, idx):
     return dict(target=h(x["target"]), draft=h(x["draft"]), tokens=h(x["tokens"]), u_accept=h(x["u_accept"]),
                 u_resample=h(x["u_resample"]), draft_len=h(x["draft_len"]), T=x["T"], B=len(idx), K=x["K"],
                 V=x["V"], dtype=x["dtype"])
+
+
+def tree_parents(branching, max_nodes=64) -> np.ndarray:
+    """Parent array of a candidate tree built level by level: every node of
+    level l gets branching[l] children, nodes numbered breadth-first (so each
+    parent precedes its children), truncated to max_nodes.  [-1] is the root."""
+    parent = [-1]
+    level = [0]
+    for nb in branching:
+        nxt = []
+        for v in level:
+            for _ in range(nb):
+                if len(parent) >= max_nodes:
+                    break
+                nxt.append(len(parent))
+                parent.append(v)
+        level = nxt
+    return np.array(parent, np.int32)
+
+
+def random_tree_parents(g: np.random.Generator, N: int) -> np.ndarray:
+    """A random tree on N nodes: node n's parent is uniform over 0..n-1."""
+    par = np.full(N, -1, np.int32)
+    for n in range(1, N):
+        par[n] = g.integers(0, n)
+    return par
+
+
+def tree_inputs(B, parent, V, dtype="bf16", T=1.0, seed=0, target_std=2.0, draft_scale=1.0, draft_noise=1.0):
+    """Tree verification inputs: per sequence the tree `parent` ([N] shared,
+    or [B, N]); target rows ~ N(0, target_std^2), draft rows = draft_scale *
+    target + N(0, draft_noise^2); node n's token ~ softmax(draft[parent[n]] /
+    T) by Gumbel-max (the argmax at T == 0); uniforms on the 2^-24 grid."""
+    par = np.asarray(parent, np.int32)
+    if par.ndim == 1:
+        par = np.tile(par, (B, 1))
+    N = par.shape[1]
+    gl = rng(seed * 16 + SEED_LOGITS)
+    t = normals(gl, (B, N, V), target_std)
+    d = (np.float32(draft_scale) * t + normals(gl, (B, N, V), draft_noise)).astype(np.float32)
+    target, draft = store(t, dtype), store(d, dtype)
+    # proposals: node n's token is an independent draw from its parent's
+    # draft row (siblings are i.i.d. candidates)
+    bi = np.repeat(np.arange(B), N - 1)
+    pi = np.maximum(par[:, 1:], 0).reshape(-1)
+    tokens = np.zeros((B, N), np.int32)
+    tokens[:, 1:] = gumbel_max_tokens(rng(seed * 16 + SEED_TOKENS), draft[bi, pi], T).reshape(B, N - 1)
+    gu = rng(seed * 16 + SEED_UNIFORM)
+    return dict(target=target, draft=draft, parent=par, tokens=tokens, u_accept=uniforms(gu, (B, N)),
+                u_resample=uniforms(gu, B), T=T, B=B, N=N, V=V)
+
+
+def config_medusa_tree(seed=0, B=16, V=32000, branching=(4, 3, 2, 1), max_nodes=64):
+    """A Medusa-style candidate tree per sequence (Section 5, OSD + Medusa on
+    a Vicuna-7B-size vocabulary): branching 4, 3, 2, 1 by level, 64 nodes;
+    target ~ N(0, 3^2), draft = target + N(0, 1^2), T = 1."""
+    return tree_inputs(B, tree_parents(branching, max_nodes), V, "bf16", T=1.0, seed=seed, target_std=3.0,
+                       draft_noise=1.0)

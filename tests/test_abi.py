@@ -266,3 +266,22 @@ def test_verify_noalloc_rejects_before_touching_the_gpu():
     assert L.osd_verify_workspace_bytes(big, 8) > binding.OSD_VERIFY_NOALLOC_SCRATCH_BYTES
     assert L.osd_verify_noalloc(*args(big, 8)) == binding.OSD_ERR_SCRATCH
     assert L.osd_verify_workspace_bytes(1024, 8) <= binding.OSD_VERIFY_NOALLOC_SCRATCH_BYTES
+
+
+def test_verify_tree_rejects_bad_arguments():
+    """Host checks of osd_verify_tree (nothing is launched)."""
+    L = osd.lib()
+    def call(**kw):
+        a = dict(t=FAKE, d=FAKE, dtype=1, B=2, N=5, V=64, par=FAKE, tok=FAKE, ua=FAKE, ur=FAKE, T=1.0,
+                 acc=FAKE, toks=FAKE, nodes=None, ws=FAKE, wsb=1 << 20)
+        a.update(kw)
+        return L.osd_verify_tree(a["t"], a["d"], a["dtype"], a["B"], a["N"], a["V"], a["par"], a["tok"], a["ua"],
+                                 a["ur"], a["T"], a["acc"], a["toks"], a["nodes"], a["ws"], a["wsb"], None)
+    assert call(t=None) == -1 and call(par=None) == -1 and call(tok=None) == -1 and call(acc=None) == -1
+    assert call(d=None) == -1 and call(ua=None) == -1 and call(ur=None) == -1
+    assert call(N=0) == -1 and call(N=65) == -1 and call(B=0) == -1 and call(V=0) == -1 and call(dtype=3) == -1
+    assert call(V=32769) == -2 and call(dtype=0, V=16385) == -2
+    assert call(T=-1.0) == -1 and call(T=float("nan")) == -1
+    assert call(ws=None) == -4 and call(wsb=8) == -4
+    assert L.osd_verify_tree_workspace_bytes(4, 64) >= 4 * (4 + 4 * 64)
+    assert L.osd_verify_tree_workspace_bytes(4, 65) == 0 and L.osd_verify_tree_workspace_bytes(0, 4) == 0

@@ -261,3 +261,200 @@ def test_fused_nan_logits_give_invalid_rows(osd):
     rr = {k: (v[keep] if isinstance(v, np.ndarray) and v.shape[:1] == (8,) else v) for k, v in rv.items()}
     compare_verify(rr, acc[keep], toks[keep], rmask[keep], "fused nan rows")
     assert np.isfinite(loss).all()
+
+
+# --------------------------------------------------------------------------
+# Error-index mode: distil the row at each sequence's first rejection
+# --------------------------------------------------------------------------
+
+def run_rejected(osd, x, kind, beta):
+    import torch
+    out = osd.osd_verify_distill_rejected(to_device(x["target"]), to_device(x["draft"]),
+                                          to_device(x["tokens"].astype(np.int32)), to_device(x["u_accept"]),
+                                          to_device(x["u_resample"]), x["T"], kind, beta,
+                                          draft_len=to_device(x.get("draft_len")))
+    torch.cuda.synchronize()
+    acc, toks, rmask, loss, rows, g = out
+    if g.dtype == torch.bfloat16:
+        g = g.cpu().view(torch.int16).numpy().view(np.uint16)
+    else:
+        g = g.cpu().numpy()
+    return (acc.cpu().numpy(), toks.cpu().numpy(), rmask.cpu().numpy(), loss.cpu().numpy(),
+            rows.cpu().numpy(), g)
+
+
+def check_rejected(osd, x, kind, beta, label, max_excluded_frac=0.1):
+    """Against ref.verify, then ref.distill with the verification's reject
+    mask (the kernel's own mask, which equals the oracle's on every sequence
+    compared exactly; a sequence inside the margin band may legitimately
+    reject elsewhere, and its distilled row follows its own outcome)."""
+    acc, toks, rmask, loss, rows, g = run_rejected(osd, x, kind, beta)
+    B, K, V = x["target"].shape[0], x["target"].shape[1] - 1, x["target"].shape[2]
+    rv = ref.verify(x["target"], x["draft"], x["tokens"], x["u_accept"], x["u_resample"], x["T"],
+                    draft_len=x.get("draft_len"))
+    n, ex = compare_verify(rv, acc, toks, rmask, label)
+    assert ex <= max(1, max_excluded_frac * B)
+    rd = ref.distill(x["target"], x["draft"], kind, beta=beta, tau=x["T"], mask=rmask, B=B, K=K,
+                     teacher_batch_stride=(K + 1) * V, student_batch_stride=K * V)
+    compare_losses(rows, rd["row_loss"], label=f"{label} row loss")
+    compare_losses(loss, [rd["loss_mean"], rd["loss_sum"]], label=f"{label} loss")
+    if g.dtype == np.uint16:
+        gx = compare_grad_bf16(g, rd["grad"], label)
+        gf = synth.bf16_to_f32(g)
+    else:
+        compare_grad_f32(g, rd["grad"], label)
+        gx, gf = 0, g
+    off = rmask == 0
+    assert not rows[off].any() and not gf[off].any(), "rows outside the first rejections must be zero"
+    print(f"[{label}] compared {n} sequences, excluded {ex}; {int(rmask.sum())} rows distilled; "
+          f"loss {loss.tolist()}; {gx} midpoint gradient elements excluded", flush=True)
+    return acc, rmask, loss
+
+
+@pytest.mark.parametrize("sigma", [0.25, 1.0, 2.0])
+def test_rejected_llama_vocab(osd, sigma):
+    """B=8 k=5 V=32000 bf16, forward KL on the rejected positions (the
+    workload's own reading of which rows are distilled), three acceptance
+    rates."""
+    for seed in range(3):
+        check_rejected(osd, synth.config_llama_vocab(sigma, seed), "fkl", 0.5, f"rejected llama sigma={sigma} seed={seed}")
+
+
+@pytest.mark.parametrize("kind", ["jsd", "rkl", "fkl"])
+def test_rejected_t5_vocab_full_batch(osd, kind):
+    check_rejected(osd, synth.config_t5_vocab(0), kind, 0.5, f"rejected t5 {kind}")
+
+
+def test_rejected_ragged_and_invalid(osd):
+    """Ragged lengths; invalid lengths and tokens (a bad token anywhere in a
+    sequence leaves its rejected row undistilled); a row without finite
+    logits; p(y) = 0 at position 0."""
+    x = synth.verify_inputs(12, 6, 5008, "bf16", T=1.0, seed=5, ragged=True, draft_noise=1.0)
+    V = x["target"].shape[2]
+    x["draft_len"][0] = 0
+    x["draft_len"][1] = 7
+    x["tokens"][2, x["draft_len"][2] - 1] = V    # out of range at the last position
+    x["target"][4, 0, :] = 0xFF80
+    x["draft_len"][5] = 3
+    x["target"][5, 0, :] = 0xFF80
+    x["target"][5, 0, 17] = synth.to_bf16(np.float32([0.0]))[0]
+    x["draft"][5, 0, :] = synth.to_bf16(np.float32([0.0]))[0]
+    x["tokens"][5, 0] = 3
+    acc, rmask, _ = check_rejected(osd, x, "jsd", 0.5, "rejected ragged + invalid")
+    assert acc[:3].tolist() == [-1] * 3 and acc[4] == -1 and acc[5] == 0
+    assert not rmask[:5].any() and rmask[5, 0] == 1
+
+
+@pytest.mark.parametrize("V,dtype", [(4100, "f32"), (1001, "bf16"), (40000, "bf16")])
+def test_rejected_vocab_sizes(osd, V, dtype):
+    """fp32 rows, an unaligned row length and a vocabulary above the
+    streaming tiles (the last two take osd_verify + osd_distill_loss_grad
+    inside the entry point)."""
+    x = synth.verify_inputs(6, 4, V, dtype, T=0.9, seed=V % 89, target_std=2.5, draft_noise=0.8)
+    check_rejected(osd, x, "rkl", 0.5, f"rejected V={V} {dtype}")
+
+
+def test_rejected_matches_separate_calls(osd):
+    """The same step as osd_verify, then osd_distill_loss_grad on its
+    reject_mask: identical outputs (the two verifications' draws agree
+    outside the margin band; row losses and gradients bit for bit), and two
+    fused calls are bitwise equal."""
+    import torch
+    x = synth.config_t5_vocab(3)
+    B, K, V = x["B"], x["K"], x["V"]
+    a = run_rejected(osd, x, "jsd", 0.5)
+    b = run_rejected(osd, x, "jsd", 0.5)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+    acc, toks, rmask = osd.osd_verify(to_device(x["target"]), to_device(x["draft"]),
+                                      to_device(x["tokens"].astype(np.int32)), to_device(x["u_accept"]),
+                                      to_device(x["u_resample"]), x["T"])
+    loss, rows, g = osd.osd_distill_loss_grad(to_device(x["target"]), to_device(x["draft"]), "jsd", 0.5, x["T"],
+                                              mask=rmask, B=B, K=K, teacher_batch_stride=(K + 1) * V,
+                                              student_batch_stride=K * V)
+    torch.cuda.synchronize()
+    rv = ref.verify(x["target"], x["draft"], x["tokens"], x["u_accept"], x["u_resample"], x["T"])
+    from tests._helpers import at_risk
+    ok = ~at_risk(rv)
+    assert np.array_equal(a[2][ok], rmask.cpu().numpy()[ok])
+    assert np.array_equal(a[4][ok], rows.cpu().numpy()[ok])
+    assert np.array_equal(a[5][ok], g.cpu().view(torch.int16).numpy().view(np.uint16)[ok])
+    compare_losses(a[3], loss.cpu().numpy(), rtol=1e-6, label="fused vs separate loss")
+
+
+def test_rejected_without_reject_mask_output(osd):
+    """reject_mask is optional: the streaming path and the two-call path
+    (which then keeps the mask in the workspace) give the same results."""
+    import ctypes
+    import torch
+    from paper_2310_07177_amd import binding
+    L = binding.lib()
+    for V in (8192, 40000):
+        x = synth.verify_inputs(8, 4, V, "bf16", T=1.0, seed=V % 7, draft_noise=1.0)
+        want = run_rejected(osd, x, "fkl", 0.5)
+        B, K = 8, 4
+        dev = torch.device("cuda")
+        acc = torch.empty(B, dtype=torch.int32, device=dev)
+        toks = torch.empty(B, K + 1, dtype=torch.int32, device=dev)
+        loss = torch.empty(2, dtype=torch.float32, device=dev)
+        rows = torch.empty(B, K, dtype=torch.float32, device=dev)
+        g = torch.empty(B, K, V, dtype=torch.bfloat16, device=dev)
+        ws = torch.zeros(L.osd_verify_distill_workspace_bytes(B, K), dtype=torch.uint8, device=dev)
+        t, d = to_device(x["target"]), to_device(x["draft"])
+        y, ua, ur = to_device(x["tokens"].astype(np.int32)), to_device(x["u_accept"]), to_device(x["u_resample"])
+        P = lambda z: ctypes.c_void_p(z.data_ptr())
+        st = L.osd_verify_distill_rejected(P(t), P(d), binding.OSD_BF16, B, K, V, P(y), None, P(ua), P(ur),
+                                           ctypes.c_float(1.0), P(acc), P(toks), None, binding.OSD_FKL,
+                                           ctypes.c_float(0.5), P(loss), P(rows), P(g), P(ws), ws.numel(),
+                                           ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        assert st == 0
+        torch.cuda.synchronize()
+        assert np.array_equal(acc.cpu().numpy(), want[0]) and np.array_equal(toks.cpu().numpy(), want[1])
+        assert np.array_equal(loss.cpu().numpy(), want[3]) and np.array_equal(rows.cpu().numpy(), want[4])
+        assert np.array_equal(g.cpu().view(torch.int16).numpy().view(np.uint16), want[5])
+        assert int(ws.count_nonzero()) == 0, "the workspace is left zero"
+
+
+SPECULATIVE = r'''
+import sys
+sys.path.insert(0, ".")
+import numpy as np
+from paper_2310_07177_amd import synth
+from tests import test_fused_gpu as t
+import paper_2310_07177_amd as osd
+osd.lib()
+import ctypes
+_hip = ctypes.CDLL("libamdhip64.so")
+_hip.hipGetErrorString.restype = ctypes.c_char_p
+_orig = osd.binding.OsdError.__init__
+def _init(self, fn, status):
+    e = _hip.hipGetLastError()
+    print("HIP last error", e, _hip.hipGetErrorString(e), flush=True)
+    _orig(self, fn, status)
+osd.binding.OsdError.__init__ = _init
+# every rejecting workgroup at a position > 0 that has not seen an earlier
+# rejection itself draws and distils without looking at the decisions
+t.check_rejected(osd, synth.config_t5_vocab(0), "jsd", 0.5, "speculative rejected t5 jsd")
+t.check_rejected(osd, synth.config_llama_vocab(2.0, 1), "fkl", 0.5, "speculative rejected llama sigma=2")
+x = synth.verify_inputs(40, 8, 8192, "f32", T=0.8, seed=71, ragged=True, draft_noise=1.5)
+t.check_rejected(osd, x, "rkl", 0.5, "speculative rejected ragged f32")
+t.check_fused(osd, synth.config_t5_vocab(1), "jsd", 0.5, np.ones((64, 8), np.uint8), "speculative masked t5 jsd")
+print("SPECULATIVE_OK", flush=True)
+'''
+
+
+def test_rejected_speculative_rows_are_cleared(osd):
+    """With the fused kernel's bound on looks at earlier decisions set to 0
+    (OSD_FUSED_POLLS, read once per process, so in a child process), every
+    rejection at a position > 0 is drawn and distilled speculatively; the
+    last workgroup must clear the rows that turn out not to be first.  The
+    results must still equal the oracle's."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, OSD_FUSED_POLLS="0")
+    r = subprocess.run([sys.executable, "-u", "-c", SPECULATIVE], cwd=root, env=env, capture_output=True, text=True,
+                       timeout=150)
+    print(r.stdout[-3000:], r.stderr[-3000:], flush=True)
+    assert r.returncode == 0 and "SPECULATIVE_OK" in r.stdout
