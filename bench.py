@@ -55,6 +55,9 @@ def parse():
     p.add_argument("--streams", type=int, default=2,
                    help="independent steps in flight: consecutive steps alternate between this many "
                         "streams, each call with its own workspace")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the other workloads (Llama-vocab, distillation buffer, large vocabulary, "
+                        "tree, error-index mode) and the read ceiling")
     p.add_argument("--only", default=None,
                    help="profiling aid: run only the named loops, comma-separated "
                         "(verify,greedy,jsd,rkl,fused,sample_prop,sample_mix,shard_stats,shard_step,copy)")
@@ -114,10 +117,40 @@ def shard_stats_bytes(klen, Vs, elem=2):
     return rows * Vs * elem + 4 * int(klen.sum()) + 4 * len(klen) + 40 * int((klen + 1).sum())
 
 
+def verify_bytes_ragged(klen, V, elem=2):
+    """Algorithmic bytes of one osd_verify call with proposal lengths klen:
+    target rows 0..k_b and draft rows 0..k_b-1 of each sequence read once,
+    the proposals, uniforms and outputs (K = max k_b) once."""
+    K = int(klen.max())
+    rows = int((2 * klen + 1).sum())
+    B = len(klen)
+    return rows * V * elem + 8 * int(klen.sum()) + 4 * B + 4 * B + 4 * B * (K + 1) + B * K
+
+
+def tree_bytes(parent, V, elem=2):
+    """Algorithmic bytes of one osd_verify_tree call: every node's target row
+    and every inner node's draft row read once, the tree (parents, tokens,
+    uniforms) read and the outputs written."""
+    B, N = parent.shape
+    inner = sum(len(set(int(v) for v in parent[b, 1:])) for b in range(B))
+    return (B * N + inner) * V * elem + 12 * B * N + 4 * B + 8 * B * N
+
+
+# Other workloads (each reported with its oracle baseline on a sample):
+# Llama vocabulary (B = 8, k = 5, V = 32000, sigma in {0.25, 1, 2}, FKL on the
+# rejected rows), the distillation buffer (N = 16384 rows, V = 32000, JSD on a
+# 40 % mask), the large-vocabulary serving step (B = 256, k_b ~ U{1..8},
+# V = 128256, FKL on the rejected rows) and a Medusa-shaped candidate tree
+# (B = 16, 64 nodes, V = 32000).
+C4_N, C4_V = 16384, 32000
+TREE_B, TREE_V = 16, 32000
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2310_07177_amd", "csrc", "*"))):
-        h.update(open(f, "rb").read())
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2310_07177_amd", "csrc", "**", "*"), recursive=True)):
+        if os.path.isfile(f):
+            h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -167,6 +200,235 @@ def cpu_baseline():
             "sample": f"{reps} full batch(es) of B=64 k=8 V=32128 bf16 (verify T=0.7 + JSD "
                       f"beta=0.5 tau=0.7 with gradient), {el:.1f} s single-threaded fp64 on one core "
                       f"of {os.cpu_count()} ({model})"}
+
+
+def other_configs(torch, osd, L, binding, synth, dev, stream, call, time_loop, t_, kernels, x3, sets3, R3, hs):
+    """The remaining workloads, each timed like the step's entry points (a
+    captured loop of calls on the side stream, median of 5 replays), with
+    the oracle timed on a sample of the same recipe; then the read ceiling."""
+    import numpy as np
+    from oracle import ref
+    P = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+    f_rej, fv, fd, ftree = L.osd_verify_distill_rejected, L.osd_verify, L.osd_distill_loss_grad, L.osd_verify_tree
+    out = {}
+
+    def line(name, us, nbytes, units, unit_name):
+        gbs = nbytes / (us * 1e-6) / 1e9
+        d = {"us_per_call": round(us, 3), "algorithmic_bytes": int(nbytes), "achieved_GBps": round(gbs, 1),
+             "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), unit_name + "_per_s": round(units / (us * 1e-6), 1)}
+        print(f"# {name}: {us:.2f} us/call, {gbs:.0f} GB/s ({100 * gbs / PEAK_HBM_GBS:.1f}% of peak), "
+              f"{units / (us * 1e-6) / 1e6:.2f} M {unit_name}/s", file=sys.stderr, flush=True)
+        return d
+
+    def oracle_rate(fn, units, budget=3.0):
+        t0, reps = time.perf_counter(), 0
+        while True:
+            fn()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > budget or reps >= 200:
+                break
+        return {"value": round(reps * units / el, 2), "cores": 1, "kind": "oracle",
+                "sample": f"{reps} call(s) in {el:.1f} s single-threaded fp64"}
+
+    ws_vd = torch.zeros(L.osd_verify_distill_workspace_bytes(256, 8), dtype=torch.uint8, device=dev)
+    ws_v = torch.zeros(L.osd_verify_workspace_bytes(256, 8), dtype=torch.uint8, device=dev)
+    ws_d = torch.zeros(L.osd_distill_workspace_bytes(C4_N, 1), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def rejected_legs(tag, xs, Bc, Kc, Vc, T, kind, klen_np):
+        """The error-index mode (one call) and the two-call path (osd_verify,
+        then osd_distill_loss_grad on its reject_mask) over rotating sets."""
+        outs = []
+        for s in xs:
+            outs.append(dict(acc=torch.empty(Bc, dtype=torch.int32, device=dev),
+                             toks=torch.empty(Bc, Kc + 1, dtype=torch.int32, device=dev),
+                             rmask=torch.empty(Bc, Kc, dtype=torch.uint8, device=dev),
+                             loss=torch.empty(2, dtype=torch.float32, device=dev),
+                             rows=torch.empty(Bc, Kc, dtype=torch.float32, device=dev),
+                             grad=torch.empty(Bc, Kc, Vc, dtype=torch.bfloat16, device=dev)))
+        dl = [P(s.get("dlen")) for s in xs]
+        cT = ctypes.c_float(T)
+        rej = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, Bc, Kc, Vc, P(s["tokens"]), dl[j], P(s["ua"]),
+                P(s["ur"]), cT, P(o["acc"]), P(o["toks"]), P(o["rmask"]), kind, ctypes.c_float(0.5), P(o["loss"]),
+                P(o["rows"]), P(o["grad"]), P(ws_vd), ws_vd.numel(), hs) for j, (s, o) in enumerate(zip(xs, outs))]
+        ver = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, Bc, Kc, Vc, P(s["tokens"]), dl[j], P(s["ua"]),
+                P(s["ur"]), cT, P(o["acc"]), P(o["toks"]), P(o["rmask"]), P(ws_v), ws_v.numel(), hs)
+               for j, (s, o) in enumerate(zip(xs, outs))]
+        dis = [(P(s["target"]), (Kc + 1) * Vc, P(s["draft"]), Kc * Vc, binding.OSD_BF16, Bc, Kc, Vc, P(o["rmask"]),
+                kind, ctypes.c_float(0.5), cT, P(o["loss"]), P(o["rows"]), P(o["grad"]), P(ws_d), ws_d.numel(), hs)
+               for s, o in zip(xs, outs)]
+        n = len(xs)
+        iters = max(20, min(200, 4 * n))
+        ms_rej = time_loop(lambda r: call(f_rej, rej[r % n]), iters)
+        ms_ver = time_loop(lambda r: call(fv, ver[r % n]), iters)
+        ms_two = time_loop(lambda r: (call(fv, ver[r % n]), call(fd, dis[r % n])), iters)
+        torch.cuda.synchronize()
+        masked = int(outs[0]["rmask"].sum())
+        vb = verify_bytes_ragged(klen_np, Vc)
+        db = masked * 2 * Vc * 2 + Bc * Kc * Vc * 2 + Bc * Kc + 4 * Bc * Kc + 8
+        pos = int(klen_np.sum())
+        return {"rejected_one_call": line(f"{tag} verify + distil rejected rows, one call", ms_rej * 1e3, vb + db,
+                                          pos, "positions"),
+                "verify_alone": line(f"{tag} osd_verify", ms_ver * 1e3, vb, pos, "positions"),
+                "two_calls": line(f"{tag} osd_verify + osd_distill_loss_grad(reject_mask)", ms_two * 1e3, vb + db,
+                                  pos, "positions"),
+                "distilled_rows": masked}
+
+    # ---- Llama vocabulary: B=8, k=5, V=32000, sigma 0.25 / 1 / 2, FKL on the rejected rows
+    c2 = {}
+    for sigma in (0.25, 1.0, 2.0):
+        xc = synth.config_llama_vocab(sigma, 0)
+        base = dict(target=t_(xc["target"]), draft=t_(xc["draft"]), tokens=t_(xc["tokens"].astype(np.int32)),
+                    ua=t_(xc["u_accept"]), ur=t_(xc["u_resample"]))
+        per = (base["target"].numel() + base["draft"].numel()) * 2
+        xs = [{k: v.clone() for k, v in base.items()} for _ in range(max(2, math.ceil(2 * INFINITY_CACHE / per)))]
+        klen = np.full(xc["B"], xc["K"], np.int64)
+        c2[f"sigma={sigma}"] = rejected_legs(f"llama sigma={sigma}", xs, xc["B"], xc["K"], xc["V"], 1.0,
+                                            binding.OSD_FKL, klen)
+        del xs, base
+
+        def oracle_c2(xc=xc):
+            r = ref.verify(xc["target"], xc["draft"], xc["tokens"], xc["u_accept"], xc["u_resample"], 1.0)
+            ref.distill(xc["target"], xc["draft"], "fkl", tau=1.0, mask=r["reject_mask"], B=xc["B"], K=xc["K"],
+                        teacher_batch_stride=(xc["K"] + 1) * xc["V"], student_batch_stride=xc["K"] * xc["V"])
+        c2[f"sigma={sigma}"]["cpu_baseline"] = dict(oracle_rate(oracle_c2, xc["B"] * xc["K"]), unit="positions/s")
+    out["llama_vocab_B8_k5_V32000"] = c2
+    torch.cuda.empty_cache()
+
+    # ---- T5 vocabulary (the step's batch), JSD on the rejected rows only
+    t5 = rejected_legs("t5 JSD", [{**s, "dlen": None} for s in sets3], B, K, V, T_VERIFY, binding.OSD_JSD,
+                       np.full(B, K, np.int64))
+    out["t5_vocab_B64_k8_V32128_rejected_rows"] = t5
+
+    # ---- distillation buffer: N=16384, V=32000, JSD(0.5), tau=1, 40 % mask (drawn on the device)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4 * 16 + synth.SEED_LOGITS)
+    zipf = torch.from_numpy(synth.zipf_bias(C4_V, 0)).to(dev)
+    teacher = torch.randn(C4_N, C4_V, generator=gen, device=dev) * 3.0 + zipf
+    student = (teacher + torch.randn(C4_N, C4_V, generator=gen, device=dev)).to(torch.bfloat16)
+    teacher = teacher.to(torch.bfloat16)
+    mask = (torch.rand(C4_N, 1, generator=gen, device=dev) < 0.4).to(torch.uint8)
+    c4_loss = torch.empty(2, dtype=torch.float32, device=dev)
+    c4_rows = torch.empty(C4_N, 1, dtype=torch.float32, device=dev)
+    c4_grad = torch.empty(C4_N, C4_V, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    c4_args = (P(teacher), C4_V, P(student), C4_V, binding.OSD_BF16, C4_N, 1, C4_V, P(mask), binding.OSD_JSD,
+               ctypes.c_float(0.5), ctypes.c_float(1.0), P(c4_loss), P(c4_rows), P(c4_grad), P(ws_d), ws_d.numel(),
+               hs)
+    ms = time_loop(lambda r: call(fd, c4_args), 20)
+    masked = int(mask.sum())
+    c4 = line("distillation buffer JSD", ms * 1e3, distill_bytes(C4_N, 1, C4_V, masked), C4_N, "rows")
+    c4["masked_rows"] = masked
+    xs4 = synth.config_distill_buffer(N=64, V=C4_V, seed=0)
+    c4["cpu_baseline"] = dict(oracle_rate(lambda: ref.distill(xs4["teacher"], xs4["student"], "jsd", beta=0.5,
+                                                              tau=1.0, mask=xs4["mask"]), 64),
+                              unit="rows/s", sample_rows=64)
+    out["distillation_buffer_N16384_V32000"] = c4
+    del teacher, student, mask, c4_grad
+    torch.cuda.empty_cache()
+
+    # ---- large vocabulary: B=256, k_b ~ U{1..8}, V=128256, T=0.8, FKL on the rejected rows
+    x5 = synth.config_large_vocab_device(seed=0)
+    s5 = dict(target=x5["target"], draft=x5["draft"], tokens=x5["tokens"], ua=x5["u_accept"], ur=x5["u_resample"],
+              dlen=x5["draft_len"])
+    klen5 = x5["draft_len"].cpu().numpy().astype(np.int64)
+    c5 = rejected_legs("large vocab", [s5], x5["B"], x5["K"], x5["V"], x5["T"], binding.OSD_FKL, klen5)
+    h5 = synth.config_large_vocab(seed=0, B=4)
+
+    def oracle_c5():
+        r = ref.verify(h5["target"], h5["draft"], h5["tokens"], h5["u_accept"], h5["u_resample"], h5["T"],
+                       draft_len=h5["draft_len"])
+        ref.distill(h5["target"], h5["draft"], "fkl", tau=h5["T"], mask=r["reject_mask"], B=4, K=h5["K"],
+                    teacher_batch_stride=(h5["K"] + 1) * h5["V"], student_batch_stride=h5["K"] * h5["V"])
+    c5["cpu_baseline"] = dict(oracle_rate(oracle_c5, int(h5["draft_len"].sum())), unit="positions/s",
+                              sample_sequences=4)
+    out["large_vocab_B256_V128256_ragged"] = c5
+    del x5, s5
+    torch.cuda.empty_cache()
+
+    # ---- Medusa-shaped candidate tree: B=16, 64 nodes (branching 4, 3, 2, 1), V=32000, T=1 (drawn on the device)
+    par_np = synth.tree_parents((4, 3, 2, 1))
+    N = len(par_np)
+    gt = torch.Generator(device=dev)
+    gt.manual_seed(6 * 16 + synth.SEED_LOGITS)
+    tsets = []
+    per = TREE_B * N * TREE_V * 2 * 2
+    for _ in range(max(2, math.ceil(2 * INFINITY_CACHE / per))):
+        tt = torch.randn(TREE_B, N, TREE_V, generator=gt, device=dev) * 3.0
+        dd = tt + torch.randn(TREE_B, N, TREE_V, generator=gt, device=dev)
+        parent = torch.from_numpy(np.tile(par_np, (TREE_B, 1))).to(dev)
+        rows = dd[:, parent[0, 1:].long()]  # each node's parent row
+        gum = -torch.log(-torch.log(torch.rand(rows.shape, generator=gt, device=dev).clamp_min(1e-30)))
+        toks = torch.zeros(TREE_B, N, dtype=torch.int32, device=dev)
+        toks[:, 1:] = torch.argmax(rows.to(torch.bfloat16).float() + gum, dim=-1).to(torch.int32)
+        del rows, gum
+        tsets.append(dict(target=tt.to(torch.bfloat16), draft=dd.to(torch.bfloat16), parent=parent, tokens=toks,
+                          ua=torch.rand(TREE_B, N, generator=gt, device=dev),
+                          ur=torch.rand(TREE_B, generator=gt, device=dev),
+                          acc=torch.empty(TREE_B, dtype=torch.int32, device=dev),
+                          out=torch.empty(TREE_B, N, dtype=torch.int32, device=dev),
+                          nodes=torch.empty(TREE_B, N, dtype=torch.int32, device=dev)))
+        del tt, dd
+    ws_t = torch.zeros(L.osd_verify_tree_workspace_bytes(TREE_B, N), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    targs = [(P(s["target"]), P(s["draft"]), binding.OSD_BF16, TREE_B, N, TREE_V, P(s["parent"]), P(s["tokens"]),
+              P(s["ua"]), P(s["ur"]), ctypes.c_float(1.0), P(s["acc"]), P(s["out"]), P(s["nodes"]), P(ws_t),
+              ws_t.numel(), hs) for s in tsets]
+    ms = time_loop(lambda r: call(ftree, targs[r % len(targs)]), 100)
+    tree = line("Medusa-shaped tree", ms * 1e3, tree_bytes(np.tile(par_np, (TREE_B, 1)), TREE_V),
+                TREE_B * (N - 1), "candidates")
+    tree["mean_accepted"] = round(float(tsets[0]["acc"].float().mean()), 3)
+    ht = synth.tree_inputs(2, par_np, TREE_V, "bf16", T=1.0, seed=0, target_std=3.0)
+    tree["cpu_baseline"] = dict(oracle_rate(lambda: ref.verify_tree(ht["target"], ht["draft"], ht["parent"],
+                                                                    ht["tokens"], ht["u_accept"], ht["u_resample"],
+                                                                    1.0), 2 * (N - 1)),
+                                unit="candidates/s", sample_sequences=2)
+    out["medusa_tree_B16_N64_V32000"] = tree
+    del tsets
+    torch.cuda.empty_cache()
+
+    # ---- read ceiling: a pure-read kernel on buffers of the step's sizes
+    out["read_ceiling"] = read_ceiling(torch, dev, stream, time_loop, kernels)
+    return out
+
+
+def read_ceiling(torch, dev, stream, time_loop, kernels):
+    """Best time of a pure-read kernel (libosd_probe.so, built from
+    csrc/probe/read_ceiling.hip) over rotating buffers of verify's and the
+    fused step's algorithmic bytes, and each kernel's share of it."""
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2310_07177_amd", "libosd_probe.so"))
+    lib.osd_probe_read.restype = ctypes.c_int
+    lib.osd_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                   ctypes.c_void_p]
+    hs = ctypes.c_void_p(stream.cuda_stream)
+    sink = torch.zeros(65536, dtype=torch.int32, device=dev)
+    res = {}
+    for name in ("verify", "verify_distill"):
+        nbytes = kernels[name]["algorithmic_bytes"] // 16 * 16
+        nbuf = max(2, math.ceil(2 * INFINITY_CACHE / nbytes))
+        bufs = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(nbuf)]
+        best = None
+        for blocks in (1024, 2048, 4096, 8192):
+            for unroll in (2, 4, 8):
+                def fn(r, blocks=blocks, unroll=unroll):
+                    st = lib.osd_probe_read(ctypes.c_void_p(bufs[r % nbuf].data_ptr()), nbytes, blocks, unroll,
+                                            ctypes.c_void_p(sink.data_ptr()), hs)
+                    if st != 0:
+                        raise RuntimeError("osd_probe_read failed")
+                ms = time_loop(fn, 40)
+                if best is None or ms < best[0]:
+                    best = (ms, blocks, unroll)
+        gbs = nbytes / (best[0] * 1e-3) / 1e9
+        k = kernels[name]
+        res[name] = {"bytes": nbytes, "us": round(best[0] * 1e3, 3), "GBps": round(gbs, 1),
+                     "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "blocks": best[1], "unroll": best[2],
+                     "kernel_frac_of_ceiling": round(k["achieved_GBps"] / gbs, 4)}
+        print(f"# read ceiling at {name}'s {nbytes / 1e6:.1f} MB: {best[0] * 1e3:.2f} us, {gbs:.0f} GB/s "
+              f"({100 * gbs / PEAK_HBM_GBS:.1f}% of peak); {name} reaches {100 * k['achieved_GBps'] / gbs:.1f}% "
+              "of it", file=sys.stderr, flush=True)
+        del bufs
+    return res
 
 
 def main():
@@ -488,6 +750,9 @@ def main():
           f"of peak); one rank's 3-phase step: {ms_shs * 1e3:.2f} us, {sh_pos / (ms_shs * 1e-3) / 1e6:.2f} M "
           "positions/s", file=sys.stderr, flush=True)
 
+    configs = None if args.no_configs else other_configs(
+        torch, osd, L, binding, synth, dev, stream, call, time_loop, t_, kernels, x, sets, R, hs)
+
     # The step is one kernel.
     dom = "verify_distill"
     kd = kernels[dom]
@@ -519,6 +784,8 @@ def main():
         "single_stream_ms_per_step": round(ms_one, 6),
         "sharded_verify": sharded,
     }
+    if configs is not None:
+        out["other_configs"] = configs
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)

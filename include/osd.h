@@ -367,9 +367,10 @@ int osd_sample(const void* p_logits, int64_t p_row_stride,
  * OSD_ERR_INVALID_ARG for a bad dtype, sizes <= 0, K > OSD_MAX_K, G outside
  * 1..OSD_MAX_SHARDS, shard outside [0, G), a slice outside [0, V), T < 0 or
  * not finite, a needed NULL pointer or a misaligned record array;
- * OSD_ERR_UNSUPPORTED for V_g > osd_max_vocab(dtype) or V > 524288 (the
- * whole row's fixed-point mass must stay below 2^63); OSD_ERR_DEVICE for a
- * failed launch.  Nothing is enqueued on an error.
+ * OSD_ERR_UNSUPPORTED for V_g above 65536 (bf16) or 32768 (fp32) -- a rank
+ * holds its slice in registers -- or V > 524288 (the whole row's
+ * fixed-point mass must stay below 2^63); OSD_ERR_DEVICE for a failed
+ * launch.  Nothing is enqueued on an error.
  */
 #define OSD_MAX_SHARDS 64
 

@@ -13,6 +13,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libosd.so")
+PROBE_LIB = os.path.join(HERE, "libosd_probe.so")
 SOURCES = ["osd_api.hip", "verify.hip", "distill.hip", "verify_greedy.hip", "distill_stream.hip", "verify_distill.hip",
            "sample.hip", "verify_shard.hip", "verify_tree.hip"]
 
@@ -52,6 +53,13 @@ def build(verbose: bool = False) -> str:
     subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs,
                    check=True)
     os.replace(tmp, LIB)
+    # The benchmark's read-ceiling probe, a library of its own.
+    probe = os.path.join(CSRC, "probe", "read_ceiling.hip")
+    tmp = PROBE_LIB + ".tmp"
+    r = subprocess.run([HIPCC] + FLAGS + ["-shared", "-o", tmp, probe], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {probe}:\n{r.stdout}{r.stderr}")
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

@@ -352,6 +352,211 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
     if (wid == 0) reduce_loss(a, n, D);
 }
 
+// Rows too long to hold (beyond 8 chunks per thread of 1024 threads): the
+// passes of distill_kernel with the rows streamed from memory, one 1024-thread
+// workgroup per row.  Pass 1 reads both rows for the statistics; pass 2 reads
+// them again for the divergence (and, for FKL, whose gradient needs only the
+// normalisers, writes the gradient); RKL and JSD read them a third time for
+// the gradient, which needs the row's divergence.  The re-reads of a row pair
+// follow its first read closely and mostly hit the Infinity Cache.  Nothing
+// but scalars is held across passes, so nothing spills at any row length.
+constexpr int kLongW = 1024;
+constexpr int kLongUnroll = 4;
+
+template <typename Fmt, bool VEC, int KIND>
+__global__ __launch_bounds__(kLongW, 1) void distill_long_kernel(DistillArgs a) {
+    constexpr int W = kLongW, NW = W / kWave, EPC = Fmt::kPerChunk, U = kLongUnroll;
+    __shared__ float s_max[2][NW];
+    __shared__ double s_sum[2][NW];
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int K = a.K, V = a.V;
+    const int n = blockIdx.x;
+    const int b = n / K, i = n - b * K;
+    const bool on = a.mask == nullptr || a.mask[n] != 0;
+    void* grow = a.grad_out ? static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes : nullptr;
+    const int nchunks = (V + EPC - 1) / EPC;
+    const int R = (nchunks + W - 1) / W;
+    double D = 0.0;
+
+    if (!on) {
+        if (grow)
+            for (int r = 0; r < R; ++r) store_grad_chunk<Fmt, W, 1, VEC>(grow, r, chunk_t{0u, 0u, 0u, 0u}, V);
+    } else {
+        const char* trow = static_cast<const char*>(a.teacher) + (int64_t(b) * a.tstride + int64_t(i) * V) * Fmt::kBytes;
+        const char* srow = static_cast<const char*>(a.student) + (int64_t(b) * a.sstride + int64_t(i) * V) * Fmt::kBytes;
+        const float c2 = a.c2;
+        // Pass 1: statistics (fp64 terms for FKL and RKL, as distill_kernel).
+        float Kt = kNegInf, Ks = kNegInf;
+        double dt = 0.0, ds = 0.0;
+        {
+            float ft = 0.0f, fs = 0.0f;
+            for (int r0 = 0; r0 < R; r0 += U) {
+                chunk_t xt[U], xs[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    xt[u] = stream_chunk<Fmt, VEC>(trow, (r0 + u) * W + tid, nchunks, V);
+                    xs[u] = stream_chunk<Fmt, VEC>(srow, (r0 + u) * W + tid, nchunks, V);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if constexpr (KIND == 2) {
+                        fold_chunk<Fmt>(xt[u], c2, Kt, ft);
+                        fold_chunk<Fmt>(xs[u], c2, Ks, fs);
+                    } else {
+                        fold_chunk<Fmt>(xt[u], c2, Kt, dt);
+                        fold_chunk<Fmt>(xs[u], c2, Ks, ds);
+                    }
+                }
+            }
+            if constexpr (KIND == 2) {
+                dt = ft;
+                ds = fs;
+            }
+        }
+        wave_merge_stats(Kt, dt);
+        wave_merge_stats(Ks, ds);
+        if (lane == 0) {
+            s_max[0][wid] = Kt;
+            s_max[1][wid] = Ks;
+            s_sum[0][wid] = dt;
+            s_sum[1][wid] = ds;
+        }
+        __syncthreads();
+        Kt = s_max[0][0];
+        Ks = s_max[1][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            Kt = fmaxf(Kt, s_max[0][w]);
+            Ks = fmaxf(Ks, s_max[1][w]);
+        }
+        double St = 0.0, Ss = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            St += rescale(s_sum[0][w], s_max[0][w], Kt);
+            Ss += rescale(s_sum[1][w], s_max[1][w], Ks);
+        }
+        const double ktd = double(Kt) + log2(St), ksd = double(Ks) + log2(Ss);
+        const float kt = float(ktd), ks = float(ksd), dk = float(ktd - ksd);
+        const float beta = a.beta, omb = 1.0f - a.beta;
+        const bool q_only = a.beta == 0.0f;  // JSD at beta = 0: m = q, log2(q/m) = 0
+        const float ln2 = float(kLn2);
+        const float fkl_scale = a.inv_tau;
+
+        // Pass 2: divergence terms in log2 units (FKL: and its gradient, with
+        // fewer rounds in flight, as it also holds the gradient's values).
+        constexpr int U2 = KIND == 0 ? 2 : U;
+        float acc0 = 0.0f, acc1 = 0.0f;
+        for (int r0 = 0; r0 < R; r0 += U2) {
+            chunk_t xt[U2], xs[U2];
+#pragma unroll
+            for (int u = 0; u < U2; ++u) {
+                xt[u] = stream_chunk<Fmt, VEC>(trow, (r0 + u) * W + tid, nchunks, V);
+                xs[u] = stream_chunk<Fmt, VEC>(srow, (r0 + u) * W + tid, nchunks, V);
+            }
+#pragma unroll
+            for (int u = 0; u < U2; ++u) {
+                float c0 = 0.0f, c1 = 0.0f;
+                float g[EPC];
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const float t = Fmt::get(xt[u], e), sx = Fmt::get(xs[u], e);
+                    if constexpr (KIND == 0 || KIND == 1) {
+                        const float lr = fmaxf(fminf(__builtin_fmaf(t - sx, c2, -dk), -kLogFloor), kLogFloor);
+                        if constexpr (KIND == 0) {
+                            const float p = exp2_fast(__builtin_fmaf(t, c2, -kt));
+                            c0 = __builtin_fmaf(p, lr, c0);
+                            const float q = exp2_fast(fmaxf(__builtin_fmaf(sx, c2, -ks), kLogFloor));
+                            g[e] = (q - p) * fkl_scale;
+                        } else {
+                            const float q = exp2_fast(__builtin_fmaf(sx, c2, -ks));
+                            c0 = __builtin_fmaf(-q, lr, c0);
+                        }
+                    } else {
+                        const float lp = fmaxf(__builtin_fmaf(t, c2, -kt), kLogFloor);
+                        const float lq = fmaxf(__builtin_fmaf(sx, c2, -ks), kLogFloor);
+                        const float p = exp2_fast(lp), q = exp2_fast(lq);
+                        const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                        const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                        c0 = __builtin_fmaf(p, -L, c0);
+                        c1 = __builtin_fmaf(q, q_only ? 0.0f : d - L, c1);
+                    }
+                }
+                acc0 = acc0 + c0;
+                acc1 = acc1 + c1;
+                if constexpr (KIND == 0) {
+                    if (grow) store_grad_chunk<Fmt, W, 1, VEC>(grow, r0 + u, pack_grad<Fmt>(g), V);
+                }
+            }
+        }
+        {
+            const double d0 = wave_sum(double(acc0));
+            const double d1 = wave_sum(double(acc1));
+            __syncthreads();  // s_sum is reused
+            if (lane == 0) {
+                s_sum[0][wid] = d0;
+                s_sum[1][wid] = d1;
+            }
+        }
+        __syncthreads();
+        double A0 = 0.0, A1 = 0.0;
+        for (int w = 0; w < NW; ++w) {
+            A0 += s_sum[0][w];
+            A1 += s_sum[1][w];
+        }
+        if constexpr (KIND == 2)
+            D = kLn2 * (double(a.beta) * A0 + (1.0 - double(a.beta)) * A1);
+        else
+            D = kLn2 * A0;
+
+        // Pass 3 (RKL, JSD): the gradient, which needs the row's divergence.
+        if constexpr (KIND != 0) {
+            if (grow) {
+                const float shift = KIND == 1 ? float(D) : float(kLn2 * A1);
+                const float scale = (KIND == 2 ? omb : 1.0f) * a.inv_tau;
+                for (int r0 = 0; r0 < R; r0 += U) {
+                    chunk_t xt[U], xs[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        xt[u] = stream_chunk<Fmt, VEC>(trow, (r0 + u) * W + tid, nchunks, V);
+                        xs[u] = stream_chunk<Fmt, VEC>(srow, (r0 + u) * W + tid, nchunks, V);
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        float g[EPC];
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) {
+                            const float lp = fmaxf(__builtin_fmaf(Fmt::get(xt[u], e), c2, -kt), kLogFloor);
+                            const float lq = fmaxf(__builtin_fmaf(Fmt::get(xs[u], e), c2, -ks), kLogFloor);
+                            const float q = exp2_fast(lq);
+                            float lr;
+                            if constexpr (KIND == 1) {
+                                lr = lq - lp;
+                            } else {
+                                const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                                lr = q_only ? 0.0f : d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                            }
+                            g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
+                        }
+                        store_grad_chunk<Fmt, W, 1, VEC>(grow, r0 + u, pack_grad<Fmt>(g), V);
+                    }
+                }
+            }
+        }
+    }
+    if (a.row_loss_out && tid == 0) a.row_loss_out[n] = float(D);
+    if (wid == 0) reduce_loss(a, n, D);
+}
+
+template <typename Fmt, bool VEC>
+hipError_t launch_long(const DistillLaunch& L, const DistillArgs& a) {
+    const dim3 grid(unsigned(L.B) * unsigned(L.K)), block(kLongW);
+    switch (L.kind) {
+        case 0: return launch_kernel(&distill_long_kernel<Fmt, VEC, 0>, grid, block, 0, L.stream, a);
+        case 1: return launch_kernel(&distill_long_kernel<Fmt, VEC, 1>, grid, block, 0, L.stream, a);
+        default: return launch_kernel(&distill_long_kernel<Fmt, VEC, 2>, grid, block, 0, L.stream, a);
+    }
+}
+
 template <typename Fmt, int W, int CPT, bool VEC>
 hipError_t launch_kind(const DistillLaunch& L, const DistillArgs& a) {
     const dim3 grid(unsigned(L.B) * unsigned(L.K)), block(W);
@@ -372,7 +577,8 @@ hipError_t launch_tile(const DistillLaunch& L, const DistillArgs& a) {
 template <typename Fmt>
 hipError_t launch_fmt(const DistillLaunch& L, const DistillArgs& a) {
     RowTile t;
-    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    if (!pick_tile(L.V, Fmt::kPerChunk, &t))
+        return L.vec ? launch_long<Fmt, true>(L, a) : launch_long<Fmt, false>(L, a);
     switch (t.W * 100 + t.CPT) {
         case 25601: return launch_tile<Fmt, 256, 1>(L, a);
         case 25602: return launch_tile<Fmt, 256, 2>(L, a);
@@ -380,7 +586,6 @@ hipError_t launch_fmt(const DistillLaunch& L, const DistillArgs& a) {
         case 51204: return launch_tile<Fmt, 512, 4>(L, a);
         case 51208: return launch_tile<Fmt, 512, 8>(L, a);
         case 102408: return launch_tile<Fmt, 1024, 8>(L, a);
-        case 102416: return launch_tile<Fmt, 1024, 16>(L, a);
         default: return hipErrorInvalidValue;
     }
 }

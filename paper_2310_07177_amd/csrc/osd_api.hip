@@ -402,6 +402,10 @@ int shard_common(const void* target, int dtype, int B, int K, int V_shard, float
     if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
     if (B <= 0 || K <= 0 || V_shard <= 0 || K > OSD_MAX_K) return OSD_ERR_INVALID_ARG;
     if (!sizes_ok(B, K, V_shard, dtype)) return OSD_ERR_UNSUPPORTED;
+    // A rank's slice is held in registers: at most 8 chunks per thread of a
+    // 1024-thread workgroup (65536 bf16 or 32768 fp32 logits).
+    osd::RowTile t;
+    if (!osd::pick_tile(V_shard, per_chunk(dtype), &t)) return OSD_ERR_UNSUPPORTED;
     if (!(temperature >= 0.0f) || isinf(temperature)) return OSD_ERR_INVALID_ARG;
     if (!target || !draft_tokens) return OSD_ERR_INVALID_ARG;
     return OSD_OK;

@@ -382,6 +382,57 @@ __device__ inline void row_stats2_tail(const chunk_t (&a)[CPT], const chunk_t (&
     }
 }
 
+// Fold one chunk into a thread's (K, S) exactly as row_stats does for each
+// of its chunks (for rows streamed from memory rather than held).
+template <typename Fmt>
+__device__ inline void fold_chunk(const chunk_t& x, float c2, float& K, float& S) {
+    constexpr int EPC = Fmt::kPerChunk;
+    const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(x) * c2));
+    S = rescale(S, K, kn);
+    K = kn;
+    const float kx = fmaxf(K, -3.0e38f);  // see row_stats
+    float e8[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) e8[e] = exp2_fast(__builtin_fmaf(Fmt::get(x, e), c2, -kx));
+#pragma unroll
+    for (int w = 1; w < EPC; w <<= 1)
+#pragma unroll
+        for (int e = 0; e < EPC; e += 2 * w) e8[e] = e8[e] + e8[e + w];
+    S = S + e8[0];
+}
+
+// fold_chunk with every term accumulated in fp64 (as the fp64 row_stats).
+template <typename Fmt>
+__device__ inline void fold_chunk(const chunk_t& x, float c2, float& K, double& S) {
+    constexpr int EPC = Fmt::kPerChunk;
+    const float kn = fmaxf(K, ceilf(chunk_max<Fmt>(x) * c2));
+    S = rescale(S, K, kn);
+    K = kn;
+    const float kx = fmaxf(K, -3.0e38f);
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int e = 0; e < EPC; e += 2) {
+        s0 += double(exp2_fast(__builtin_fmaf(Fmt::get(x, e), c2, -kx)));
+        s1 += double(exp2_fast(__builtin_fmaf(Fmt::get(x, e + 1), c2, -kx)));
+    }
+    S += s0 + s1;
+}
+
+// Chunk ch of a row streamed from memory, or padding past its end.  VEC:
+// a 16-byte load (a chunk past the row re-reads the last one, replaced by
+// padding); otherwise element loads.
+template <typename Fmt, bool VEC>
+__device__ inline chunk_t stream_chunk(const void* row, int ch, int nchunks, int V) {
+    if constexpr (VEC) {
+        const bool in = ch < nchunks;
+        const chunk_t v = __builtin_nontemporal_load(static_cast<const chunk_t*>(row) + (in ? ch : nchunks - 1));
+        const chunk_t pad = pad_chunk<Fmt>();
+        return chunk_t{in ? v.x : pad.x, in ? v.y : pad.y, in ? v.z : pad.z, in ? v.w : pad.w};
+    } else {
+        return ch < nchunks ? Fmt::load_scalar(row, int64_t(ch) * Fmt::kPerChunk, V) : pad_chunk<Fmt>();
+    }
+}
+
 // fp64 accumulation of every term (for quantities first-order sensitive to
 // the normaliser).
 template <typename Fmt, int CPT>

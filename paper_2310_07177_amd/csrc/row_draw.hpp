@@ -117,3 +117,89 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
 }
 
 }  // namespace osd
+
+namespace osd {
+
+// Rounds of a row streamed by a workgroup of W threads: chunk r*W + tid in
+// round r.  The streamed kernels hold at most kMaxStreamRounds rounds' worth of
+// cell totals in LDS (16 rounds of 1024 threads: 131072 bf16 or 65536 fp32
+// logits per row).
+constexpr int kMaxStreamRounds = 16;
+
+// Inverse-CDF draw over a row that is streamed from memory instead of held in
+// registers.  masses(r, m) fills m[0..EPC) with the non-negative fp32 masses
+// of this thread's chunk in round r (0 for padding); it is called once per
+// round in pass A and once more, for the winning round, by the winning wave in
+// pass B, and must return the same values both times.  Cells are (round,
+// wave); chunk masses are summed left to right in fp32 and converted exactly
+// to 2^-SH fixed point, as in draw_inverse_cdf, so the CDF cells partition
+// [0, Z) exactly.  Returns the token on one thread and -1 on the others;
+// *z_zero is set (uniformly) when the total mass is zero.  s_tot holds
+// R * (W / 64) cells.  All threads call it.
+template <int SH, int W, int EPC, typename MassFn>
+__device__ int draw_inverse_cdf_streamed(int R, MassFn masses, float u, unsigned long long* s_tot,
+                                         DrawShared* s_draw, bool* z_zero) {
+    constexpr int NW = W / kWave;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int cells = R * NW;
+    for (int r = 0; r < R; ++r) {
+        float m[EPC];
+        masses(r, m);
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) s = s + m[e];
+        const uint64_t t = wave_sum(mass_to_fixed<SH>(s));
+        if (lane == 0) s_tot[r * NW + wid] = t;
+    }
+    __syncthreads();
+    if (wid == 0) {
+        uint64_t z = 0;
+        for (int c0 = lane; c0 < cells; c0 += kWave) z += s_tot[c0];
+        z = wave_sum(z);
+        if (lane == 0) s_draw->cell_round = -1;
+        if (z > 0) {
+            uint64_t c = static_cast<uint64_t>(double(u) * double(z));
+            if (c >= z) c = z - 1;
+            uint64_t carry = 0;
+            for (int base = 0; base < cells; base += kWave) {
+                const int idx = base + lane;
+                const uint64_t v = idx < cells ? uint64_t(s_tot[idx]) : 0;
+                const uint64_t incl = wave_inclusive_scan(v) + carry;
+                const uint64_t lo = incl - v;
+                if (v > 0 && lo <= c && c < incl) {
+                    s_draw->cell_round = idx / NW;
+                    s_draw->cell_wave = idx % NW;
+                    s_draw->target = c - lo;
+                }
+                carry = static_cast<uint64_t>(__shfl(static_cast<unsigned long long>(incl), kWave - 1, kWave));
+            }
+        }
+    }
+    __syncthreads();
+    const int nstar = s_draw->cell_round;
+    *z_zero = nstar < 0;
+    if (nstar < 0 || wid != s_draw->cell_wave) return -1;
+    float m[EPC];
+    masses(nstar, m);
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) s = s + m[e];
+    const uint64_t v = mass_to_fixed<SH>(s);
+    const uint64_t incl = wave_inclusive_scan(v);
+    const uint64_t lo = incl - v;
+    const uint64_t target = s_draw->target;
+    if (!(v > 0 && lo <= target && target < incl)) return -1;
+    const uint64_t want = target - lo;
+    float run = 0.0f;
+    int pick = -1, last_pos = -1;
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        run = run + m[e];
+        if (m[e] > 0.0f) last_pos = e;
+        if (pick < 0 && mass_to_fixed<SH>(run) > want) pick = e;
+    }
+    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+    return (nstar * W + tid) * EPC + pick;
+}
+
+}  // namespace osd

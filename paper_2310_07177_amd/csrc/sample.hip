@@ -182,6 +182,94 @@ hipError_t launch_mode(const SampleLaunch& L, const SampleArgs& a) {
     return e;
 }
 
+// A mixture of rows too long to hold as a pair (beyond 8 chunks per thread of
+// 1024 threads): the statistics and the draw of sample_kernel with both rows
+// streamed from memory, one 1024-thread workgroup per row pair.
+constexpr int kLongW = 1024;
+constexpr int kLongUnroll = 4;
+
+template <typename Fmt, bool VEC>
+__global__ __launch_bounds__(kLongW, 1) void sample_mix_long_kernel(SampleArgs a) {
+    constexpr int W = kLongW, NW = W / kWave, EPC = Fmt::kPerChunk, U = kLongUnroll;
+    __shared__ float s_max[2][NW];
+    __shared__ double s_sum[2][NW];
+    __shared__ int s_tok;
+    __shared__ unsigned long long s_tot[kMaxStreamRounds * NW];
+    __shared__ DrawShared s_draw;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int n = blockIdx.x;
+    const int V = a.V;
+    const char* prow = a.p + int64_t(n) * a.p_stride;
+    const char* qrow = a.q + int64_t(n) * a.q_stride;
+    const int nchunks = (V + EPC - 1) / EPC;
+    const int R = (nchunks + W - 1) / W;
+    const float c2 = a.c2;
+    float Kp = kNegInf, Kq = kNegInf, sp = 0.0f, sq = 0.0f;
+    for (int r0 = 0; r0 < R; r0 += U) {
+        chunk_t xp[U], xq[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            xp[u] = stream_chunk<Fmt, VEC>(prow, (r0 + u) * W + tid, nchunks, V);
+            xq[u] = stream_chunk<Fmt, VEC>(qrow, (r0 + u) * W + tid, nchunks, V);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            fold_chunk<Fmt>(xp[u], c2, Kp, sp);
+            fold_chunk<Fmt>(xq[u], c2, Kq, sq);
+        }
+    }
+    {
+        double dp = sp, dq = sq;
+        wave_merge_stats(Kp, dp);
+        wave_merge_stats(Kq, dq);
+        if (lane == 0) {
+            s_max[0][wid] = Kp;
+            s_max[1][wid] = Kq;
+            s_sum[0][wid] = dp;
+            s_sum[1][wid] = dq;
+        }
+    }
+    if (tid == 0) s_tok = -1;
+    __syncthreads();
+    Kp = s_max[0][0];
+    Kq = s_max[1][0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+        Kp = fmaxf(Kp, s_max[0][w]);
+        Kq = fmaxf(Kq, s_max[1][w]);
+    }
+    double Sp = 0.0, Sq = 0.0;
+    for (int w = 0; w < NW; ++w) {
+        Sp += rescale(s_sum[0][w], s_max[0][w], Kp);
+        Sq += rescale(s_sum[1][w], s_max[1][w], Kq);
+    }
+    const bool bad = !(Kp > kNegInf && Kp < -kNegInf) || !usable_sum(Sp) || !(Kq > kNegInf && Kq < -kNegInf) ||
+                     !usable_sum(Sq);
+    if (bad) {
+        if (tid == 0) a.out[n] = -1;
+        return;
+    }
+    const float wp = float(double(a.beta) / Sp), wq = float((1.0 - double(a.beta)) / Sq);
+    const float kp = Kp, kq = Kq;
+    auto masses = [&](int r, float (&m)[EPC]) {
+        const int ch = r * W + tid;
+        const chunk_t tc = stream_chunk<Fmt, VEC>(prow, ch, nchunks, V);
+        const chunk_t dc = stream_chunk<Fmt, VEC>(qrow, ch, nchunks, V);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+            const float et = exp2_fast(__builtin_fmaf(Fmt::get(tc, e), c2, -kp));
+            const float ed = exp2_fast(__builtin_fmaf(Fmt::get(dc, e), c2, -kq));
+            m[e] = __builtin_fmaf(wp, et, wq * ed);
+        }
+    };
+    bool z_zero = false;
+    const int tok = draw_inverse_cdf_streamed<kShiftMix, W, EPC>(R, masses, a.u[n], s_tot, &s_draw, &z_zero);
+    if (tok >= 0) s_tok = tok;
+    __syncthreads();
+    if (tid == 0) a.out[n] = s_tok;
+}
+
 template <typename Fmt, int W, int CPT>
 hipError_t launch_tile(const SampleLaunch& L, const SampleArgs& a) {
     if (L.temperature == 0.0f) return launch_mode<Fmt, W, CPT, kModeGreedy>(L, a);
@@ -192,7 +280,17 @@ hipError_t launch_tile(const SampleLaunch& L, const SampleArgs& a) {
 template <typename Fmt>
 hipError_t launch_fmt(const SampleLaunch& L, const SampleArgs& a) {
     RowTile t;
-    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) {
+        // Longer rows: a mixture streams its row pair; one row (or an
+        // argmax) fits the resident 1024 x 16 tile without spilling.
+        const bool mix = L.temperature > 0.0f && L.beta > 0.0f && L.beta < 1.0f;
+        const dim3 grid(unsigned(L.N)), block(kLongW);
+        if (mix)
+            return L.vec ? launch_kernel(&sample_mix_long_kernel<Fmt, true>, grid, block, 0, L.stream, a)
+                         : launch_kernel(&sample_mix_long_kernel<Fmt, false>, grid, block, 0, L.stream, a);
+        if (L.temperature == 0.0f) return launch_mode<Fmt, 1024, 16, kModeGreedy>(L, a);
+        return launch_mode<Fmt, 1024, 16, kModeOne>(L, a);
+    }
     // Fewer rows than two per CU: the rows' latency is the cost, so each row
     // gets the widest workgroup (half the elements per thread).
     if (L.N < 2 * L.cus && t.W < 1024) {
@@ -208,7 +306,6 @@ hipError_t launch_fmt(const SampleLaunch& L, const SampleArgs& a) {
         case 51204: return launch_tile<Fmt, 512, 4>(L, a);
         case 51208: return launch_tile<Fmt, 512, 8>(L, a);
         case 102408: return launch_tile<Fmt, 1024, 8>(L, a);
-        case 102416: return launch_tile<Fmt, 1024, 16>(L, a);
         default: return hipErrorInvalidValue;
     }
 }

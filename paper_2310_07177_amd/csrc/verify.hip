@@ -401,6 +401,198 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void verify_kernel(V
     }
 }
 
+// Rows too long to hold (more than 8 chunks per thread of a 1024-thread
+// workgroup): the same per-row protocol as verify_kernel, with the rows
+// streamed from memory.  The statistics take one pass over the row pair (four
+// rounds of loads in flight per thread); the workgroup that draws streams the
+// row pair again (pass A of draw_inverse_cdf_streamed) and its winning wave
+// reloads one round (pass B).  Nothing is held across passes but (K, S), so
+// no register spills at any row length.
+constexpr int kLongW = 1024;
+constexpr int kLongUnroll = 4;
+
+template <typename Fmt, bool VEC>
+__global__ __launch_bounds__(kLongW, 1) void verify_long_kernel(VerifyArgs a) {
+    constexpr int W = kLongW, NW = W / kWave, EPC = Fmt::kPerChunk, U = kLongUnroll;
+    __shared__ float s_max[2][NW];
+    __shared__ double s_sum[2][NW];
+    __shared__ int s_flag;
+    __shared__ int s_tok;
+    __shared__ unsigned long long s_tot[kMaxStreamRounds * NW];
+    __shared__ DrawShared s_draw;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int B = a.B, K = a.K, V = a.V;
+    const bool bonus = int(blockIdx.x) >= B * K;
+    int b, i;
+    if (!bonus) {
+        i = blockIdx.x / B;
+        b = blockIdx.x - i * B;
+    } else {
+        b = blockIdx.x - B * K;
+        i = -1;
+    }
+    const int kb = a.draft_len ? a.draft_len[b] : K;
+    if (kb < 1 || kb > K) {
+        if (bonus) write_invalid(a, b);
+        return;
+    }
+    if (bonus) {
+        i = kb;
+    } else if (i >= kb) {
+        return;
+    }
+    const int y = bonus ? 0 : a.tokens[int64_t(b) * K + i];
+    if (!bonus && (y < 0 || y >= V)) {
+        if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadToken, 0));
+        return;
+    }
+    if (bonus) {
+        if (wid == 0) {
+            const int st = poll_earlier(a, b, i, 1);
+            if (lane == 0) s_flag = st;
+            if (st == 2) publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
+        }
+        __syncthreads();
+        if (s_flag == 2) return;
+    }
+    const char* trow = static_cast<const char*>(a.target) + (int64_t(b) * (K + 1) + i) * int64_t(V) * Fmt::kBytes;
+    const char* drow =
+        bonus ? trow : static_cast<const char*>(a.draft) + (int64_t(b) * K + i) * int64_t(V) * Fmt::kBytes;
+    uint32_t ty_raw = 0u, dy_raw = 0u;
+    if (!bonus) {
+        ty_raw = Fmt::load_raw(trow, y);
+        dy_raw = Fmt::load_raw(drow, y);
+    }
+    const float c2 = a.c2;
+    const int nchunks = (V + EPC - 1) / EPC;
+    const int R = (nchunks + W - 1) / W;
+
+    // Statistics, U rounds of loads at a time.
+    float Kt = kNegInf, Kd = kNegInf, st = 0.0f, sd = 0.0f;
+    for (int r0 = 0; r0 < R; r0 += U) {
+        chunk_t xt[U], xd[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ch = (r0 + u) * W + tid;
+            xt[u] = stream_chunk<Fmt, VEC>(trow, ch, nchunks, V);
+            if (!bonus) xd[u] = stream_chunk<Fmt, VEC>(drow, ch, nchunks, V);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            fold_chunk<Fmt>(xt[u], c2, Kt, st);
+            if (!bonus) fold_chunk<Fmt>(xd[u], c2, Kd, sd);
+        }
+    }
+    {
+        double dt = st, dd = sd;
+        wave_merge_stats(Kt, dt);
+        wave_merge_stats(Kd, dd);
+        if (lane == 0) {
+            s_max[0][wid] = Kt;
+            s_max[1][wid] = Kd;
+            s_sum[0][wid] = dt;
+            s_sum[1][wid] = dd;
+        }
+    }
+    if (tid == 0) s_tok = -1;
+    __syncthreads();
+    Kt = s_max[0][0];
+    Kd = s_max[1][0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+        Kt = fmaxf(Kt, s_max[0][w]);
+        Kd = fmaxf(Kd, s_max[1][w]);
+    }
+    double St = 0.0, Sd = 0.0;
+    for (int w = 0; w < NW; ++w) {
+        St += rescale(s_sum[0][w], s_max[0][w], Kt);
+        Sd += rescale(s_sum[1][w], s_max[1][w], Kd);
+    }
+    const bool bad = !(Kt > kNegInf && Kt < -kNegInf) || !usable_sum(St) ||
+                     (!bonus && (!(Kd > kNegInf && Kd < -kNegInf) || !usable_sum(Sd)));
+    if (bad) {
+        if (wid == 0) publish(a, b, i, kb, make_rec(kRecBadRow, 0));
+        return;
+    }
+    // Wave 0 decides whether this workgroup draws (as verify_kernel).
+    if (wid == 0) {
+        int flag = 1;
+        if (!bonus) {
+            const float ty = Fmt::from_raw(ty_raw), dy = Fmt::from_raw(dy_raw);
+            const double e = (double(ty) * a.c2d - double(Kt)) - (double(dy) * a.c2d - double(Kd));
+            double ratio;
+            if (!(e > -2000.0)) {
+                ratio = 0.0;
+            } else if (e > 2000.0) {
+                ratio = __builtin_huge_val();
+            } else {
+                const double n = floor(e);
+                ratio = __builtin_ldexp(double(exp2_fast(float(e - n))), int(n)) * (Sd / St);
+            }
+            const double u = a.u_accept[int64_t(b) * K + i];
+            if (u < ratio) {
+                flag = 0;
+                publish(a, b, i, kb, make_rec(kRecAccept, 0));
+            } else {
+                if (lane == 0) publish_u32(a.records + int64_t(b) * (K + 1) + i, make_rec(kRecRejectPending, 0));
+                if (i > 0 && poll_earlier(a, b, i, kMaxPolls) == 2) {
+                    flag = 0;
+                    publish(a, b, i, kb, make_rec(kRecRejectSkipped, 0));
+                }
+            }
+        } else if (poll_earlier(a, b, i, kMaxPolls) == 2) {
+            flag = 0;
+            publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
+        }
+        if (lane == 0) s_flag = flag;
+    }
+    __syncthreads();
+    if (s_flag == 0) return;
+
+    // The draw, the masses of verify_kernel on the streamed chunks.
+    const float rho = bonus ? 0.0f : float(St / Sd);
+    const float u = a.u_resample[b];
+    bool use_p = bonus;
+    for (int attempt = 0; attempt < 2; ++attempt) {
+        const bool p_only = use_p;
+        const float kt = Kt, kd = Kd;
+        auto masses = [&](int r, float (&m)[EPC]) {
+            const int ch = r * W + tid;
+            const chunk_t tc = stream_chunk<Fmt, VEC>(trow, ch, nchunks, V);
+            const chunk_t dc = p_only ? tc : stream_chunk<Fmt, VEC>(drow, ch, nchunks, V);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const float pt = exp2_fast(__builtin_fmaf(Fmt::get(tc, e), c2, -kt));
+                if (p_only) {
+                    m[e] = pt;
+                } else {
+                    const float qt = exp2_fast(__builtin_fmaf(Fmt::get(dc, e), c2, -kd));
+                    m[e] = fmaxf(__builtin_fmaf(-qt, rho, pt), 0.0f);
+                }
+            }
+        };
+        bool z_zero = false;
+        const int tok = draw_inverse_cdf_streamed<kFixedShift, W, EPC>(R, masses, u, s_tot, &s_draw, &z_zero);
+        if (tok >= 0) s_tok = tok;
+        if (!z_zero || use_p) break;
+        use_p = true;
+        __syncthreads();  // s_tot and s_draw are reused
+    }
+    __syncthreads();
+    if (wid == 0) {
+        const int tok = s_tok;
+        publish(a, b, i, kb, tok >= 0 ? make_rec(bonus ? kRecBonus : kRecReject, uint32_t(tok)) : make_rec(kRecBadRow, 0));
+    }
+}
+
+template <typename Fmt>
+hipError_t launch_long(const VerifyLaunch& L, const VerifyArgs& a) {
+    const dim3 grid(unsigned(L.B) * unsigned(L.K + 1)), block(kLongW);
+    return L.vec ? launch_kernel(&verify_long_kernel<Fmt, true>, grid, block, 0, L.stream, a)
+                 : launch_kernel(&verify_long_kernel<Fmt, false>, grid, block, 0, L.stream, a);
+}
+
 template <typename Fmt, int W, int CPT>
 hipError_t launch_tile(const VerifyLaunch& L, const VerifyArgs& a) {
     const dim3 grid(unsigned(L.B) * unsigned(L.K + 1)), block(W);
@@ -423,7 +615,16 @@ hipError_t launch_tile(const VerifyLaunch& L, const VerifyArgs& a) {
 template <typename Fmt>
 hipError_t launch_fmt(const VerifyLaunch& L, const VerifyArgs& a) {
     RowTile t;
-    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) return hipErrorInvalidValue;
+    if (!pick_tile(L.V, Fmt::kPerChunk, &t)) {
+        if (L.V > max_vocab_for(Fmt::kPerChunk)) return hipErrorInvalidValue;
+        // Rows longer than the largest resident tile: streamed (sampling).
+        // Greedy rows of that length take the resident 1024 x 16 tile, which
+        // holds one row per thread without spilling.
+        if (L.temperature > 0.0f) return launch_long<Fmt>(L, a);
+        const dim3 grid(unsigned(L.B) * unsigned(L.K + 1)), block(1024);
+        return L.vec ? launch_kernel(&verify_kernel<Fmt, 1024, 16, true, true>, grid, block, 0, L.stream, a)
+                     : launch_kernel(&verify_kernel<Fmt, 1024, 16, false, true>, grid, block, 0, L.stream, a);
+    }
     switch (t.W * 100 + t.CPT) {
         case 25601: return launch_tile<Fmt, 256, 1>(L, a);
         case 25602: return launch_tile<Fmt, 256, 2>(L, a);
@@ -431,18 +632,22 @@ hipError_t launch_fmt(const VerifyLaunch& L, const VerifyArgs& a) {
         case 51204: return launch_tile<Fmt, 512, 4>(L, a);
         case 51208: return launch_tile<Fmt, 512, 8>(L, a);
         case 102408: return launch_tile<Fmt, 1024, 8>(L, a);
-        case 102416: return launch_tile<Fmt, 1024, 16>(L, a);
         default: return hipErrorInvalidValue;
     }
 }
 
 }  // namespace
 
-int max_vocab_for(int per_chunk) { return 1024 * 16 * per_chunk; }
+// The largest row every entry point takes: 16 rounds of 1024 threads
+// (131072 bf16 or 65536 fp32 logits); the streamed kernels' cell tables are
+// sized for it.
+int max_vocab_for(int per_chunk) { return 1024 * kMaxStreamRounds * per_chunk; }
 
+// Register-resident tiles (a row pair in registers, at most 8 chunks per
+// thread); longer rows are streamed.
 bool pick_tile(int V, int per_chunk, RowTile* t) {
     static const RowTile tiles[] = {{256, 1}, {256, 2}, {256, 4}, {512, 4},
-                                    {512, 8}, {1024, 8}, {1024, 16}};
+                                    {512, 8}, {1024, 8}};
     for (const RowTile& c : tiles)
         if (int64_t(V) <= int64_t(c.W) * c.CPT * per_chunk) {
             *t = c;

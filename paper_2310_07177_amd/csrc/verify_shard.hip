@@ -548,7 +548,6 @@ hipError_t launch_fmt(const ShardLaunch& L) {
         case 51204: return launch_tile<Fmt, 512, 4, VEC>(L);
         case 51208: return launch_tile<Fmt, 512, 8, VEC>(L);
         case 102408: return launch_tile<Fmt, 1024, 8, VEC>(L);
-        case 102416: return launch_tile<Fmt, 1024, 16, VEC>(L);
         default: return hipErrorInvalidValue;
     }
 }

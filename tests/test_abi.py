@@ -285,3 +285,11 @@ def test_verify_tree_rejects_bad_arguments():
     assert call(ws=None) == -4 and call(wsb=8) == -4
     assert L.osd_verify_tree_workspace_bytes(4, 64) >= 4 * (4 + 4 * 64)
     assert L.osd_verify_tree_workspace_bytes(4, 65) == 0 and L.osd_verify_tree_workspace_bytes(0, 4) == 0
+
+
+def test_sharded_slices_beyond_the_register_tile_are_unsupported():
+    """A rank's slice is held in registers: up to 65536 bf16 / 32768 fp32."""
+    L = osd.lib()
+    args = lambda Vs, dt: (FAKE, FAKE, dt, 2, 3, Vs, 0, 2 * Vs, FAKE, None, ctypes.c_float(1.0), FAKE, None)
+    assert L.osd_shard_verify_stats(*args(65537, 1)) == -2
+    assert L.osd_shard_verify_stats(*args(32769, 0)) == -2

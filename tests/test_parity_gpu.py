@@ -453,3 +453,38 @@ def test_verify_nan_logits_give_invalid_rows(osd):
     compare_verify(rr, acc[keep], toks[keep], rmask[keep], "nan rows")
     if r["accepted_len"][2] == 0:
         assert acc[2] == 0  # the NaN row 1 was never reached
+
+
+# --------------------------------------------------------------------------
+# Rows longer than the register-resident tiles (streamed kernels)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("V,dtype", [(70001, "bf16"), (131072, "bf16"), (40000, "f32"), (65536, "f32")])
+def test_verify_long_rows(osd, V, dtype):
+    """Beyond 8 chunks per thread of 1024 threads the rows are streamed
+    (sampling) or take the 1024 x 16 greedy tile; aligned and unaligned rows,
+    up to the largest vocabulary the library takes."""
+    x = synth.verify_inputs(6, 4, V, dtype, T=0.9, seed=V % 101, target_std=3.0, draft_noise=0.7, ragged=True)
+    check_verify(osd, x, f"long rows V={V} {dtype}", max_excluded_frac=0.35)
+    xg = synth.verify_inputs(6, 4, V, dtype, T=0.0, seed=V % 103, target_std=3.0, draft_noise=0.3)
+    check_verify(osd, xg, f"long rows greedy V={V} {dtype}", max_excluded_frac=0.0)
+
+
+@pytest.mark.parametrize("kind,beta", [("fkl", 0.5), ("rkl", 0.5), ("jsd", 0.3), ("jsd", 0.0)])
+@pytest.mark.parametrize("V,dtype", [(70001, "bf16"), (40000, "f32")])
+def test_distill_long_rows(osd, kind, beta, V, dtype):
+    """Streamed distillation: three passes over each masked row pair (two for
+    FKL), zero rows for the unmasked ones; -inf entries on both sides."""
+    g = np.random.default_rng(V + int(beta * 10))
+    B, K = 2, 3
+    t = g.normal(0, 2.5, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    holes = g.random((B, K, V)) < 0.1
+    t[holes] = -np.inf
+    s[holes] = -np.inf
+    # one-sided holes on the side that keeps the divergence finite: the
+    # teacher's for FKL and JSD (p = 0 < q), the student's for RKL (q = 0 < p)
+    (s if kind == "rkl" else t)[0, 1, :100] = -np.inf
+    mask = np.array([[1, 1, 0], [0, 1, 1]], np.uint8)
+    tt, ss = (synth.to_bf16(t), synth.to_bf16(s)) if dtype == "bf16" else (t, s)
+    check_distill(osd, tt, ss, kind, beta, 0.8, mask, f"long rows {kind} beta={beta} V={V} {dtype}")

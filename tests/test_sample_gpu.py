@@ -98,6 +98,11 @@ def test_sample_large_vocab(osd):
     x = synth.sample_inputs(16, 128256, "bf16", seed=8)
     check(osd, x["p"], x["q"], 0.8, 0.5, x["u"], "V=128256 mixed")
     check(osd, None, x["q"], 0.8, 0.0, x["u"], "V=128256 q")
+    # rows longer than the register tiles: a streamed mixture, aligned and not
+    for V, dt in ((70001, "bf16"), (40000, "f32")):
+        y = synth.sample_inputs(12, V, dt, seed=V % 13)
+        check(osd, y["p"], y["q"], 0.9, 0.3, y["u"], f"V={V} {dt} mixed (streamed)", max_excluded=4)
+        check(osd, y["p"], None, 0.0, 1.0, None, f"V={V} {dt} greedy", max_excluded=0)
 
 
 def test_sample_unaligned_row_stride(osd):
