@@ -36,7 +36,7 @@ VerifyWs verify_layout(int B, int K) {
 }
 
 struct DistillWs {
-    size_t done, slab_cnt, slabs, rows, total;
+    size_t done, slab_cnt, slabs, rows, split, total;
     int nslabs;
 };
 // Counters first, at offsets that do not depend on B*K beyond their own
@@ -49,7 +49,8 @@ DistillWs distill_layout(int B, int K) {
     w.slab_cnt = 16;
     w.slabs = round_up(w.slab_cnt + size_t(w.nslabs) * 4, kAlign);
     w.rows = w.slabs + round_up(size_t(w.nslabs) * 16, kAlign);
-    w.total = w.rows + round_up(R * 8, kAlign);
+    w.split = w.rows + round_up(R * 8, kAlign);
+    w.total = w.split + round_up(R * osd::kSplitBytesPerRow, kAlign);
     return w;
 }
 
@@ -226,6 +227,7 @@ int osd_distill_loss_grad(const void* teacher_logits, int64_t teacher_batch_stri
     L.grad_out = grad_out;
     char* w = static_cast<char*>(workspace);
     L.row_loss_ws = reinterpret_cast<double*>(w + ws.rows);
+    L.split_ws = w + ws.split;
     L.slab_ws = reinterpret_cast<double*>(w + ws.slabs);
     L.slab_counters = reinterpret_cast<uint32_t*>(w + ws.slab_cnt);
     L.done_counter = reinterpret_cast<uint32_t*>(w + ws.done);

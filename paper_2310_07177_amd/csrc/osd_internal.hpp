@@ -80,6 +80,7 @@ struct DistillLaunch {
     float* loss_out;
     float* row_loss_out;
     void* grad_out;
+    void* split_ws;            // rows longer than the resident tiles: per-segment records, zero on entry and exit
     double* row_loss_ws;       // [B*K]
     double* slab_ws;           // [nslabs]
     uint32_t* slab_counters;   // [nslabs] zero on entry and exit
@@ -90,6 +91,11 @@ struct DistillLaunch {
 };
 
 constexpr int kSlabRows = 64;
+// Segments per row of the split distillation (16 x 8192 bf16 or 16 x 4096 fp32
+// logits) and the workspace bytes per row they take: a 32-byte record and two
+// fp64 partials per segment.
+constexpr int kMaxSplitSegments = 16;
+constexpr size_t kSplitBytesPerRow = size_t(kMaxSplitSegments) * (32 + 16);
 // Row counts up to this are reduced in one level (see distill.hip).
 constexpr int kOneLevelRows = 1024;
 
