@@ -353,41 +353,56 @@ __global__ __launch_bounds__(W, min_waves_per_simd(W, CPT)) void distill_kernel(
 }
 
 // Rows too long to hold (beyond 8 chunks per thread of 1024 threads) are
-// split into segments of kSegChunks chunks, each its own 256-thread
-// workgroup, and the row is reduced across its segments in phases, one kernel
-// each (so every row, masked or not, spreads over many CUs):
-//   1. statistics: each segment's (K, S) of both rows -> SegRec; segments of
-//      rows with mask 0 write their part of the zero gradient row instead;
-//   2. divergence: each segment merges its row's S records in segment order
-//      (every segment obtains the same normalisers), re-reads its part of the
-//      row pair and sums its divergence terms -> SegPart; FKL, whose gradient
-//      needs only the normalisers, writes its gradient segment here;
-//   3. (RKL, JSD) gradient: each segment adds the row's partials in segment
-//      order and writes its gradient segment;
-//   F. one wave per row adds the partials (in the same order), writes the
-//      row's divergence, enters the masked-loss reduction, and clears the
-//      records and partials it read (the workspace is left zero; every
-//      record and partial a phase reads was written by an earlier phase of
-//      the same call, so nothing depends on that).
-// The formulas are distill_kernel's.  Re-reads of a segment follow its first
-// read closely (Infinity Cache).
+// split into segments of kSegChunks chunks, one 256-thread workgroup each,
+// which keeps its segment of both rows in registers and cooperates with the
+// other segments of its row through device memory:
+//   1. each segment folds its (K, S) pair of both rows and publishes it;
+//      every segment reads all the row's records and merges them in segment
+//      order (the same normalisers in every workgroup);
+//   2. each segment sums its divergence terms and publishes the partials;
+//      FKL's gradient needs only the normalisers and is written here;
+//   3. RKL and JSD read all the row's partials, add them in segment order and
+//      write their gradient segment.
+// Published words go out as plain agent-scope atomic stores that are never
+// zero (each value is stored bit-inverted, and no value a segment publishes
+// has all bits set), so a reader polls the words themselves: a zero word is
+// not yet published.  Once a segment has read everything it needs it
+// arrives at the row's counter; the last arriver adds the partials in
+// segment order, writes the row's divergence, enters the masked-loss
+// reduction and clears the row's words and counter (the workspace is left
+// zero).  Rows with mask 0 write their zero gradient segments and take no
+// part in the exchange.
+//
+// A wait is bounded (kSplitPolls polls, or the value of OSD_SPLIT_POLLS).  A
+// workgroup whose siblings have not all published in time computes the
+// missing records (or partials) itself, re-reading every segment of the row
+// with the same thread layout and reduction order, so that the result is the
+// same bit for bit; it still publishes and arrives, so the row completes as
+// usual.
+// The formulas are distill_kernel's.
 constexpr int kSegW = 256;
 constexpr int kSegCPT = 4;
 constexpr int kSegChunks = kSegW * kSegCPT;
-
-struct SegRec {
-    double st, ss;
-    float kt, ks;
-    double pad;
-};
-static_assert(sizeof(SegRec) == 32, "two records per 64 bytes");
+constexpr int kSplitPolls = 256;
+constexpr int kSegNW = kSegW / kWave;
 
 struct SplitArgs {
     DistillArgs d;
-    SegRec* rec;     // [rows, nseg]
-    double* part;    // [rows, nseg, 2]
+    uint64_t* rec;   // [rows, kMaxSplitSegments, 3]: ~S_t, ~S_s, ~(K_t | K_s << 32) (bits)
+    uint64_t* part;  // [rows, kMaxSplitSegments, 2]: ~A0, ~A1 (bits)
+    uint32_t* cnt;   // [rows, 4]: arrivals (word 0)
     int nseg;
     int nchunks;
+    int polls;
+};
+
+struct SegShared {
+    float k[2][kSegNW];
+    double s[2][kSegNW];
+    float rk[kMaxSplitSegments][2];   // records merged by this workgroup
+    double rs[kMaxSplitSegments][2];
+    double pa[kMaxSplitSegments][2];  // partials
+    int flag;
 };
 
 __device__ inline bool row_on(const DistillArgs& a, int n) { return a.mask == nullptr || a.mask[n] != 0; }
@@ -398,38 +413,14 @@ __device__ inline const char* row_ptr(const void* base, int64_t stride, int n, i
     return static_cast<const char*>(base) + (int64_t(b) * stride + int64_t(i) * V) * Fmt::kBytes;
 }
 
-// The row's normalisers from its segments' records, merged in segment order
-// (the same result in every workgroup that reads them).
-__device__ inline void merge_records(const SegRec* r, int nseg, float& Kt, double& St, float& Ks, double& Ss) {
-    Kt = Ks = kNegInf;
-    for (int s = 0; s < nseg; ++s) {
-        Kt = fmaxf(Kt, r[s].kt);
-        Ks = fmaxf(Ks, r[s].ks);
-    }
-    St = Ss = 0.0;
-    for (int s = 0; s < nseg; ++s) {
-        St += rescale(r[s].st, r[s].kt, Kt);
-        Ss += rescale(r[s].ss, r[s].ks, Ks);
-    }
-}
-
-// The row's divergence from its segments' partials, in segment order.
-template <int KIND>
-__device__ inline double row_divergence(const double* part, int nseg, float beta, double& A1) {
-    double A0 = 0.0;
-    A1 = 0.0;
-    for (int s = 0; s < nseg; ++s) {
-        A0 += part[2 * s];
-        A1 += part[2 * s + 1];
-    }
-    if constexpr (KIND == 2)
-        return kLn2 * (double(beta) * A0 + (1.0 - double(beta)) * A1);
-    else
-        return kLn2 * A0;
-}
-
 // Chunk r of this thread in segment s.
 __device__ inline int seg_chunk(int s, int r) { return s * kSegChunks + r * kSegW + int(threadIdx.x); }
+
+template <typename Fmt, bool VEC>
+__device__ inline void seg_load(chunk_t (&x)[kSegCPT], const char* row, int s, int nchunks, int V) {
+#pragma unroll
+    for (int r = 0; r < kSegCPT; ++r) x[r] = stream_chunk<Fmt, VEC>(row, seg_chunk(s, r), nchunks, V);
+}
 
 template <typename Fmt, bool VEC>
 __device__ inline void put_chunk(void* row, int ch, int nchunks, const chunk_t& c, int V) {
@@ -453,146 +444,131 @@ __device__ inline void put_chunk(void* row, int ch, int nchunks, const chunk_t& 
     }
 }
 
-// Workgroup totals of two doubles (every thread gets them).
-__device__ inline void seg_sum2(double& x, double& y, double* s_a) {
-    constexpr int NW = kSegW / kWave;
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    x = wave_sum(x);
-    y = wave_sum(y);
-    if (lane == 0) {
-        s_a[wid] = x;
-        s_a[NW + wid] = y;
-    }
-    __syncthreads();
-    x = 0.0;
-    y = 0.0;
-    for (int w = 0; w < NW; ++w) {
-        x += s_a[w];
-        y += s_a[NW + w];
-    }
-}
-
-template <typename Fmt, bool VEC, int KIND>
-__global__ __launch_bounds__(kSegW) void split_stats_kernel(SplitArgs sa) {
-    constexpr int NW = kSegW / kWave, EPC = Fmt::kPerChunk;
-    __shared__ float s_k[2][NW];
-    __shared__ double s_s[2][NW];
-    const DistillArgs& a = sa.d;
-    const int n = blockIdx.x / sa.nseg, s = blockIdx.x - n * sa.nseg;
+// Segment statistics of both rows, reduced over the workgroup; slot `slot`
+// of sh.rk / sh.rs receives them.  Opens with a barrier (sh.k, sh.s reuse).
+// A segment's chunks come from a source: src(r, t, s) yields chunk r of
+// this thread for both rows (held in registers, or loaded on demand -- the
+// arithmetic is the same either way).
+template <typename Fmt, int KIND, typename Src>
+__device__ inline void seg_stats(Src src, float c2, SegShared& sh, int slot) {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-    const int K = a.K, V = a.V, nchunks = sa.nchunks;
-    if (!row_on(a, n)) {
-        if (a.grad_out) {
-            void* grow = static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes;
-#pragma unroll
-            for (int r = 0; r < kSegCPT; ++r) put_chunk<Fmt, VEC>(grow, seg_chunk(s, r), nchunks, chunk_t{0u, 0u, 0u, 0u}, V);
-        }
-        return;
-    }
-    const char* trow = row_ptr<Fmt>(a.teacher, a.tstride, n, K, V);
-    const char* srow = row_ptr<Fmt>(a.student, a.sstride, n, K, V);
-    chunk_t xt[kSegCPT], xs[kSegCPT];
-#pragma unroll
-    for (int r = 0; r < kSegCPT; ++r) {
-        xt[r] = stream_chunk<Fmt, VEC>(trow, seg_chunk(s, r), nchunks, V);
-        xs[r] = stream_chunk<Fmt, VEC>(srow, seg_chunk(s, r), nchunks, V);
-    }
-    const float c2 = a.c2;
     float Kt = kNegInf, Ks = kNegInf;
     double dt = 0.0, ds = 0.0;
     if constexpr (KIND == 2) {
         float ft = 0.0f, fs = 0.0f;
 #pragma unroll
         for (int r = 0; r < kSegCPT; ++r) {
-            fold_chunk<Fmt>(xt[r], c2, Kt, ft);
-            fold_chunk<Fmt>(xs[r], c2, Ks, fs);
+            chunk_t ct, cs;
+            src(r, ct, cs);
+            fold_chunk<Fmt>(ct, c2, Kt, ft);
+            fold_chunk<Fmt>(cs, c2, Ks, fs);
         }
         dt = ft;
         ds = fs;
     } else {
 #pragma unroll
         for (int r = 0; r < kSegCPT; ++r) {
-            fold_chunk<Fmt>(xt[r], c2, Kt, dt);
-            fold_chunk<Fmt>(xs[r], c2, Ks, ds);
+            chunk_t ct, cs;
+            src(r, ct, cs);
+            fold_chunk<Fmt>(ct, c2, Kt, dt);
+            fold_chunk<Fmt>(cs, c2, Ks, ds);
         }
     }
     wave_merge_stats(Kt, dt);
     wave_merge_stats(Ks, ds);
+    __syncthreads();
     if (lane == 0) {
-        s_k[0][wid] = Kt;
-        s_k[1][wid] = Ks;
-        s_s[0][wid] = dt;
-        s_s[1][wid] = ds;
+        sh.k[0][wid] = Kt;
+        sh.k[1][wid] = Ks;
+        sh.s[0][wid] = dt;
+        sh.s[1][wid] = ds;
     }
     __syncthreads();
-    if (tid == 0) {
-        float kt = s_k[0][0], ks = s_k[1][0];
-        for (int w = 1; w < NW; ++w) {
-            kt = fmaxf(kt, s_k[0][w]);
-            ks = fmaxf(ks, s_k[1][w]);
+    if (tid == 0) {  // one value at a time: few registers beside the held segment
+        float kt = sh.k[0][0], ks = sh.k[1][0];
+#pragma unroll 1
+        for (int w = 1; w < kSegNW; ++w) {
+            kt = fmaxf(kt, sh.k[0][w]);
+            ks = fmaxf(ks, sh.k[1][w]);
         }
         double St = 0.0, Ss = 0.0;
-        for (int w = 0; w < NW; ++w) {
-            St += rescale(s_s[0][w], s_k[0][w], kt);
-            Ss += rescale(s_s[1][w], s_k[1][w], ks);
+#pragma unroll 1
+        for (int w = 0; w < kSegNW; ++w) {
+            St += rescale(sh.s[0][w], sh.k[0][w], kt);
+            Ss += rescale(sh.s[1][w], sh.k[1][w], ks);
         }
-        SegRec r;
-        r.st = St;
-        r.ss = Ss;
-        r.kt = kt;
-        r.ks = ks;
-        r.pad = 0.0;
-        sa.rec[int64_t(n) * sa.nseg + s] = r;
+        sh.rk[slot][0] = kt;
+        sh.rk[slot][1] = ks;
+        sh.rs[slot][0] = St;
+        sh.rs[slot][1] = Ss;
     }
 }
 
-// The row's normalisers in the forms distill_kernel uses.
+// A value every thread of the workgroup holds alike, kept in a scalar register.
+__device__ inline float uniform_f32(float v) {
+    return __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(v)));
+}
+
+// The row's normalisers in the forms distill_kernel uses, from the records
+// in sh, merged in segment order.
 struct RowNorm {
     float kt, ks, dk;
 };
-__device__ inline RowNorm row_norm(const SplitArgs& sa, int n) {
-    float Kt, Ks;
-    double St, Ss;
-    merge_records(sa.rec + int64_t(n) * sa.nseg, sa.nseg, Kt, St, Ks, Ss);
+__device__ inline RowNorm merge_norm(const SegShared& sh, int nseg) {
+    float Kt = kNegInf, Ks = kNegInf;
+#pragma unroll 2
+    for (int s = 0; s < nseg; ++s) {
+        Kt = fmaxf(Kt, sh.rk[s][0]);
+        Ks = fmaxf(Ks, sh.rk[s][1]);
+    }
+    double St = 0.0, Ss = 0.0;
+#pragma unroll 2
+    for (int s = 0; s < nseg; ++s) {
+        St += rescale(sh.rs[s][0], sh.rk[s][0], Kt);
+        Ss += rescale(sh.rs[s][1], sh.rk[s][1], Ks);
+    }
     const double ktd = double(Kt) + log2(St), ksd = double(Ks) + log2(Ss);
-    return RowNorm{float(ktd), float(ksd), float(ktd - ksd)};
+    return RowNorm{uniform_f32(float(ktd)), uniform_f32(float(ksd)), uniform_f32(float(ktd - ksd))};
 }
 
-template <typename Fmt, bool VEC, int KIND>
-__global__ __launch_bounds__(kSegW) void split_loss_kernel(SplitArgs sa) {
-    constexpr int NW = kSegW / kWave, EPC = Fmt::kPerChunk;
-    __shared__ double s_a[2 * NW];
-    const DistillArgs& a = sa.d;
-    const int n = blockIdx.x / sa.nseg, s = blockIdx.x - n * sa.nseg;
-    if (!row_on(a, n)) return;
-    const int K = a.K, V = a.V, nchunks = sa.nchunks;
-    const char* trow = row_ptr<Fmt>(a.teacher, a.tstride, n, K, V);
-    const char* srow = row_ptr<Fmt>(a.student, a.sstride, n, K, V);
-    chunk_t xt[kSegCPT], xs[kSegCPT];
-#pragma unroll
-    for (int r = 0; r < kSegCPT; ++r) {
-        xt[r] = stream_chunk<Fmt, VEC>(trow, seg_chunk(s, r), nchunks, V);
-        xs[r] = stream_chunk<Fmt, VEC>(srow, seg_chunk(s, r), nchunks, V);
+// The row's divergence from the partials in sh, added in segment order.
+template <int KIND>
+__device__ inline double merge_divergence(const SegShared& sh, int nseg, float beta, double& A1) {
+    double A0 = 0.0;
+    A1 = 0.0;
+#pragma unroll 2
+    for (int s = 0; s < nseg; ++s) {
+        A0 += sh.pa[s][0];
+        A1 += sh.pa[s][1];
     }
-    const RowNorm rn = row_norm(sa, n);
+    if constexpr (KIND == 2)
+        return kLn2 * (double(beta) * A0 + (1.0 - double(beta)) * A1);
+    else
+        return kLn2 * A0;
+}
+
+// The segment's divergence partials, reduced over the workgroup into slot
+// `slot` of sh.pa.
+template <typename Fmt, int KIND, typename Src>
+__device__ inline void seg_partial(Src src, const RowNorm& rn, const DistillArgs& a, SegShared& sh, int slot) {
+    constexpr int EPC = Fmt::kPerChunk;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const float c2 = a.c2, beta = a.beta, omb = 1.0f - a.beta;
     const bool q_only = a.beta == 0.0f;
-    void* grow = a.grad_out ? static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes : nullptr;
     float acc0 = 0.0f, acc1 = 0.0f;
 #pragma unroll
     for (int r = 0; r < kSegCPT; ++r) {
         float c0 = 0.0f, c1 = 0.0f;
-        float g[EPC];
+        chunk_t ct, cs;
+        src(r, ct, cs);
 #pragma unroll
         for (int e = 0; e < EPC; ++e) {
-            const float t = Fmt::get(xt[r], e), sx = Fmt::get(xs[r], e);
+            const float t = Fmt::get(ct, e), sx = Fmt::get(cs, e);
             if constexpr (KIND == 0 || KIND == 1) {
                 const float lr = fmaxf(fminf(__builtin_fmaf(t - sx, c2, -rn.dk), -kLogFloor), kLogFloor);
                 if constexpr (KIND == 0) {
                     const float p = exp2_fast(__builtin_fmaf(t, c2, -rn.kt));
                     c0 = __builtin_fmaf(p, lr, c0);
-                    const float q = exp2_fast(fmaxf(__builtin_fmaf(sx, c2, -rn.ks), kLogFloor));
-                    g[e] = (q - p) * a.inv_tau;
                 } else {
                     const float q = exp2_fast(__builtin_fmaf(sx, c2, -rn.ks));
                     c0 = __builtin_fmaf(-q, lr, c0);
@@ -606,46 +582,40 @@ __global__ __launch_bounds__(kSegW) void split_loss_kernel(SplitArgs sa) {
                 c0 = __builtin_fmaf(p, -L, c0);
                 c1 = __builtin_fmaf(q, q_only ? 0.0f : d - L, c1);
             }
+            if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);  // 4 elements in flight
         }
         acc0 = acc0 + c0;
         acc1 = acc1 + c1;
-        if constexpr (KIND == 0) {
-            if (grow) put_chunk<Fmt, VEC>(grow, seg_chunk(s, r), nchunks, pack_grad<Fmt>(g), V);
-        }
+        __builtin_amdgcn_sched_barrier(0);
     }
-    double A0 = double(acc0), A1 = double(acc1);
-    seg_sum2(A0, A1, s_a);
-    if (threadIdx.x == 0) {
-        double* p = sa.part + (int64_t(n) * sa.nseg + s) * 2;
-        p[0] = A0;
-        p[1] = A1;
+    const double d0 = wave_sum(double(acc0)), d1 = wave_sum(double(acc1));
+    __syncthreads();
+    if (lane == 0) {
+        sh.s[0][wid] = d0;
+        sh.s[1][wid] = d1;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double A0 = 0.0, A1 = 0.0;
+#pragma unroll 1
+        for (int w = 0; w < kSegNW; ++w) {
+            A0 += sh.s[0][w];
+            A1 += sh.s[1][w];
+        }
+        sh.pa[slot][0] = A0;
+        sh.pa[slot][1] = A1;
     }
 }
 
 template <typename Fmt, bool VEC, int KIND>
-__global__ __launch_bounds__(kSegW) void split_grad_kernel(SplitArgs sa) {
+__device__ inline void seg_grad(const chunk_t (&xt)[kSegCPT], const chunk_t (&xs)[kSegCPT], const RowNorm& rn,
+                                const DistillArgs& a, double D, double A1, void* grow, int s, int nchunks) {
     constexpr int EPC = Fmt::kPerChunk;
-    const DistillArgs& a = sa.d;
-    const int n = blockIdx.x / sa.nseg, s = blockIdx.x - n * sa.nseg;
-    if (!row_on(a, n) || !a.grad_out) return;
-    const int K = a.K, V = a.V, nchunks = sa.nchunks;
-    const char* trow = row_ptr<Fmt>(a.teacher, a.tstride, n, K, V);
-    const char* srow = row_ptr<Fmt>(a.student, a.sstride, n, K, V);
-    chunk_t xt[kSegCPT], xs[kSegCPT];
-#pragma unroll
-    for (int r = 0; r < kSegCPT; ++r) {
-        xt[r] = stream_chunk<Fmt, VEC>(trow, seg_chunk(s, r), nchunks, V);
-        xs[r] = stream_chunk<Fmt, VEC>(srow, seg_chunk(s, r), nchunks, V);
-    }
-    const RowNorm rn = row_norm(sa, n);
-    double A1;
-    const double D = row_divergence<KIND>(sa.part + int64_t(n) * sa.nseg * 2, sa.nseg, a.beta, A1);
     const float c2 = a.c2, beta = a.beta, omb = 1.0f - a.beta;
     const bool q_only = a.beta == 0.0f;
     const float ln2 = float(kLn2);
-    const float shift = KIND == 1 ? float(D) : float(kLn2 * A1);
+    const float shift = uniform_f32(KIND == 1 ? float(D) : float(kLn2 * A1));
     const float scale = (KIND == 2 ? omb : 1.0f) * a.inv_tau;
-    void* grow = static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes;
 #pragma unroll
     for (int r = 0; r < kSegCPT; ++r) {
         float g[EPC];
@@ -654,61 +624,230 @@ __global__ __launch_bounds__(kSegW) void split_grad_kernel(SplitArgs sa) {
             const float lp = fmaxf(__builtin_fmaf(Fmt::get(xt[r], e), c2, -rn.kt), kLogFloor);
             const float lq = fmaxf(__builtin_fmaf(Fmt::get(xs[r], e), c2, -rn.ks), kLogFloor);
             const float q = exp2_fast(lq);
-            float lr;
-            if constexpr (KIND == 1) {
-                lr = lq - lp;
+            if constexpr (KIND == 0) {
+                g[e] = (q - exp2_fast(lp)) * scale;
             } else {
-                const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
-                lr = q_only ? 0.0f : d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                float lr;
+                if constexpr (KIND == 1) {
+                    lr = lq - lp;
+                } else {
+                    const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
+                    lr = q_only ? 0.0f : d - log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
+                }
+                g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
             }
-            g[e] = (q * scale) * __builtin_fmaf(lr, ln2, -shift);
+            if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
         }
-        put_chunk<Fmt, VEC>(grow, seg_chunk(s, r), nchunks, pack_grad<Fmt>(g), V);
+        put_chunk<Fmt, VEC>(grow, seg_chunk(s, r), nchunks, pack_grad<Fmt>(g), a.V);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
-// One wave per row: the row's divergence, the masked-loss reduction, and the
-// records and partials cleared.
-template <int KIND>
-__global__ __launch_bounds__(kWave) void split_finish_kernel(SplitArgs sa) {
-    const DistillArgs& a = sa.d;
-    const int n = blockIdx.x;
-    const int lane = threadIdx.x;
-    const bool on = row_on(a, n);
-    double D = 0.0;
-    if (on) {
-        double A1;
-        D = row_divergence<KIND>(sa.part + int64_t(n) * sa.nseg * 2, sa.nseg, a.beta, A1);
+__device__ inline uint64_t load_u64(const uint64_t* p) {
+    return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void store_u64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t pack_k(float kt, float ks) {
+    return uint64_t(__float_as_uint(kt)) | (uint64_t(__float_as_uint(ks)) << 32);
+}
+
+// Wave 0 polls the published words of the row's other segments: lane j < nseg
+// (j != s) reads the `words` words of segment j until every one is non-zero
+// or the polls run out.  On success, lane j leaves them (un-inverted) in
+// w[0..words).  Every thread gets the outcome.
+template <int WORDS>
+__device__ inline bool poll_words(const uint64_t* base, int nseg, int s, int polls, uint64_t (&w)[WORDS],
+                                  SegShared& sh) {
+    const int tid = threadIdx.x;
+    if (tid < kWave) {
+        const bool mine = tid < nseg && tid != s;
+        bool ok = false;
+        for (int p = 0; p < polls; ++p) {
+            if (p > 0) __builtin_amdgcn_s_sleep(8);
+            bool ready = true;
+            if (mine) {
+#pragma unroll
+                for (int k = 0; k < WORDS; ++k) {
+                    w[k] = load_u64(base + int64_t(tid) * WORDS + k);
+                    ready = ready && w[k] != 0;
+                }
+            }
+            if (__ballot(!ready) == 0) {
+                ok = true;
+                break;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < WORDS; ++k) w[k] = ~w[k];
+        if (tid == 0) sh.flag = ok;
     }
-    if (a.row_loss_out && lane == 0) a.row_loss_out[n] = float(D);
-    if (on) {
-        // Rows with mask 0 wrote neither.
-        for (int j = lane; j < sa.nseg; j += kWave) {
-            SegRec z;
-            z.st = z.ss = 0.0;
-            z.kt = z.ks = 0.0f;
-            z.pad = 0.0;
-            sa.rec[int64_t(n) * sa.nseg + j] = z;
-            sa.part[(int64_t(n) * sa.nseg + j) * 2] = 0.0;
-            sa.part[(int64_t(n) * sa.nseg + j) * 2 + 1] = 0.0;
+    __syncthreads();
+    return sh.flag != 0;
+}
+
+// Arrival at the row's counter once this workgroup's published words are
+// complete; the returned count is awaited only where it is used.
+__device__ inline uint32_t arrive_row(uint32_t* counter) {
+    wait_memory();
+    return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename Fmt, bool VEC, int KIND>
+__global__ __launch_bounds__(kSegW) void split_row_kernel(SplitArgs sa) {
+    __shared__ SegShared sh;
+    const DistillArgs& a = sa.d;
+    const int nseg = sa.nseg, nchunks = sa.nchunks, V = a.V;
+    const int n = blockIdx.x / nseg, s = blockIdx.x - n * nseg;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    void* grow = a.grad_out ? static_cast<char*>(a.grad_out) + int64_t(n) * V * Fmt::kBytes : nullptr;
+    if (!row_on(a, n)) {
+        if (grow) {
+#pragma unroll
+            for (int r = 0; r < kSegCPT; ++r) put_chunk<Fmt, VEC>(grow, seg_chunk(s, r), nchunks, chunk_t{0u, 0u, 0u, 0u}, V);
+        }
+        if (s == 0 && wid == 0) {
+            if (a.row_loss_out && lane == 0) a.row_loss_out[n] = 0.0f;
+            reduce_loss(a, n, 0.0);
+        }
+        return;
+    }
+    const char* trow = row_ptr<Fmt>(a.teacher, a.tstride, n, a.K, V);
+    const char* srow = row_ptr<Fmt>(a.student, a.sstride, n, a.K, V);
+    uint64_t* rec = sa.rec + int64_t(n) * kMaxSplitSegments * 3;
+    uint64_t* part = sa.part + int64_t(n) * kMaxSplitSegments * 2;
+    uint32_t* cnt = sa.cnt + int64_t(n) * 4;
+    const float c2 = a.c2;
+
+    chunk_t xt[kSegCPT], xs[kSegCPT];
+    seg_load<Fmt, VEC>(xt, trow, s, nchunks, V);
+    seg_load<Fmt, VEC>(xs, srow, s, nchunks, V);
+    const auto held = [&](int r, chunk_t& ct, chunk_t& cs) {
+        ct = xt[r];
+        cs = xs[r];
+    };
+
+    // 1. statistics
+    seg_stats<Fmt, KIND>(held, c2, sh, s);
+    if (tid == 0) {
+        store_u64(&rec[3 * s], ~uint64_t(__double_as_longlong(sh.rs[s][0])));
+        store_u64(&rec[3 * s + 1], ~uint64_t(__double_as_longlong(sh.rs[s][1])));
+        store_u64(&rec[3 * s + 2], ~pack_k(sh.rk[s][0], sh.rk[s][1]));
+    }
+    {
+        uint64_t w[3];
+        const bool ok = poll_words<3>(rec, nseg, s, sa.polls, w, sh);
+        if (ok) {
+            if (tid < nseg && tid != s) {
+                sh.rs[tid][0] = __longlong_as_double(w[0]);
+                sh.rs[tid][1] = __longlong_as_double(w[1]);
+                sh.rk[tid][0] = __uint_as_float(uint32_t(w[2]));
+                sh.rk[tid][1] = __uint_as_float(uint32_t(w[2] >> 32));
+            }
+        } else {
+            for (int j = 0; j < nseg; ++j) {
+                if (j == s) continue;
+                const auto loaded = [&](int r, chunk_t& ct, chunk_t& cs) {
+                    ct = stream_chunk<Fmt, VEC>(trow, seg_chunk(j, r), nchunks, V);
+                    cs = stream_chunk<Fmt, VEC>(srow, seg_chunk(j, r), nchunks, V);
+                };
+                seg_stats<Fmt, KIND>(loaded, c2, sh, j);
+            }
+            // the segment is read again rather than held across the loop above
+            seg_load<Fmt, VEC>(xt, trow, s, nchunks, V);
+            seg_load<Fmt, VEC>(xs, srow, s, nchunks, V);
         }
     }
-    reduce_loss(a, n, D);
+    __syncthreads();
+    const RowNorm rn = merge_norm(sh, nseg);
+    opaque(xt);  // each pass unpacks the held chunks afresh (bounded VGPRs)
+    opaque(xs);
+
+    // 2. divergence
+    seg_partial<Fmt, KIND>(held, rn, a, sh, s);
+    if (tid == 0) {
+        store_u64(&part[2 * s], ~uint64_t(__double_as_longlong(sh.pa[s][0])));
+        store_u64(&part[2 * s + 1], ~uint64_t(__double_as_longlong(sh.pa[s][1])));
+    }
+    uint32_t prev = 0;
+    double D = 0.0, A1 = 0.0;
+    if constexpr (KIND == 0) {
+        if (tid == 0) prev = arrive_row(&cnt[0]);
+        opaque(xt);
+        opaque(xs);
+        if (grow) seg_grad<Fmt, VEC, KIND>(xt, xs, rn, a, 0.0, 0.0, grow, s, nchunks);
+    } else {
+        // 3. gradient
+        uint64_t w[2];
+        const bool ok = poll_words<2>(part, nseg, s, sa.polls, w, sh);
+        if (ok) {
+            if (tid < nseg && tid != s) {
+                sh.pa[tid][0] = __longlong_as_double(w[0]);
+                sh.pa[tid][1] = __longlong_as_double(w[1]);
+            }
+        } else {
+            for (int j = 0; j < nseg; ++j) {
+                if (j == s) continue;
+                const auto loaded = [&](int r, chunk_t& ct, chunk_t& cs) {
+                    ct = stream_chunk<Fmt, VEC>(trow, seg_chunk(j, r), nchunks, V);
+                    cs = stream_chunk<Fmt, VEC>(srow, seg_chunk(j, r), nchunks, V);
+                };
+                seg_partial<Fmt, KIND>(loaded, rn, a, sh, j);
+            }
+            seg_load<Fmt, VEC>(xt, trow, s, nchunks, V);
+            seg_load<Fmt, VEC>(xs, srow, s, nchunks, V);
+        }
+        __syncthreads();
+        if (tid == 0) prev = arrive_row(&cnt[0]);
+        D = merge_divergence<KIND>(sh, nseg, a.beta, A1);
+        opaque(xt);
+        opaque(xs);
+        if (grow) seg_grad<Fmt, VEC, KIND>(xt, xs, rn, a, D, A1, grow, s, nchunks);
+    }
+    if (tid == 0) sh.flag = prev == uint32_t(nseg - 1);
+    __syncthreads();
+    if (sh.flag == 0) return;
+    // The row's last arriver: every segment has read what it needed.
+    if constexpr (KIND == 0) {
+        if (tid < nseg && tid != s) {
+            sh.pa[tid][0] = __longlong_as_double(~load_u64(&part[2 * tid]));
+            sh.pa[tid][1] = __longlong_as_double(~load_u64(&part[2 * tid + 1]));
+        }
+        __syncthreads();
+        D = merge_divergence<KIND>(sh, nseg, a.beta, A1);
+    }
+    if (tid < nseg) {
+        store_u64(&rec[3 * tid], 0ull);
+        store_u64(&rec[3 * tid + 1], 0ull);
+        store_u64(&rec[3 * tid + 2], 0ull);
+        store_u64(&part[2 * tid], 0ull);
+        store_u64(&part[2 * tid + 1], 0ull);
+    }
+    if (tid == 0) __hip_atomic_store(&cnt[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (wid == 0) {
+        if (a.row_loss_out && lane == 0) a.row_loss_out[n] = float(D);
+        reduce_loss(a, n, D);
+    }
 }
 
 template <typename Fmt, bool VEC, int KIND>
 hipError_t launch_split_kind(const DistillLaunch& L, const SplitArgs& sa) {
     const unsigned rows = unsigned(L.B) * unsigned(L.K);
-    const dim3 grid(rows * unsigned(sa.nseg)), block(kSegW);
-    hipError_t e = launch_kernel(&split_stats_kernel<Fmt, VEC, KIND>, grid, block, 0, L.stream, sa);
-    if (e != hipSuccess) return e;
-    e = launch_kernel(&split_loss_kernel<Fmt, VEC, KIND>, grid, block, 0, L.stream, sa);
-    if (e != hipSuccess) return e;
-    if constexpr (KIND != 0) {
-        e = launch_kernel(&split_grad_kernel<Fmt, VEC, KIND>, grid, block, 0, L.stream, sa);
-        if (e != hipSuccess) return e;
-    }
-    return launch_kernel(&split_finish_kernel<KIND>, dim3(rows), dim3(kWave), 0, L.stream, sa);
+    return launch_kernel(&split_row_kernel<Fmt, VEC, KIND>, dim3(rows * unsigned(sa.nseg)), dim3(kSegW), 0, L.stream,
+                         sa);
+}
+
+// kSplitPolls, or the value of OSD_SPLIT_POLLS (read once; 0 makes every
+// workgroup compute its row's records and partials itself).
+int split_polls() {
+    static const int v = [] {
+        const char* e = getenv("OSD_SPLIT_POLLS");
+        if (e == nullptr || *e == 0) return kSplitPolls;
+        const int k = atoi(e);
+        return k < 0 ? kSplitPolls : (k > 65536 ? 65536 : k);
+    }();
+    return v;
 }
 
 template <typename Fmt, bool VEC>
@@ -718,9 +857,13 @@ hipError_t launch_split(const DistillLaunch& L, const DistillArgs& a) {
     sa.nchunks = (L.V + Fmt::kPerChunk - 1) / Fmt::kPerChunk;
     sa.nseg = (sa.nchunks + kSegChunks - 1) / kSegChunks;
     if (sa.nseg > kMaxSplitSegments) return hipErrorInvalidValue;
-    sa.rec = static_cast<SegRec*>(L.split_ws);
-    sa.part = reinterpret_cast<double*>(static_cast<char*>(L.split_ws) +
-                                        size_t(L.B) * size_t(L.K) * kMaxSplitSegments * sizeof(SegRec));
+    const size_t rows = size_t(L.B) * size_t(L.K);
+    char* w = static_cast<char*>(L.split_ws);
+    sa.rec = reinterpret_cast<uint64_t*>(w);
+    sa.part = reinterpret_cast<uint64_t*>(w + rows * kMaxSplitSegments * 24);
+    sa.cnt = reinterpret_cast<uint32_t*>(w + rows * kMaxSplitSegments * 40);
+    sa.polls = split_polls();
+    if (rows * size_t(sa.nseg) > size_t(0x7FFFFFFF)) return hipErrorInvalidValue;
     switch (L.kind) {
         case 0: return launch_split_kind<Fmt, VEC, 0>(L, sa);
         case 1: return launch_split_kind<Fmt, VEC, 1>(L, sa);

@@ -92,10 +92,10 @@ struct DistillLaunch {
 
 constexpr int kSlabRows = 64;
 // Segments per row of the split distillation (16 x 8192 bf16 or 16 x 4096 fp32
-// logits) and the workspace bytes per row they take: a 32-byte record and two
-// fp64 partials per segment.
+// logits) and the workspace bytes per row they take: a 24-byte record and two
+// fp64 partials per segment, and four 32-bit counters.
 constexpr int kMaxSplitSegments = 16;
-constexpr size_t kSplitBytesPerRow = size_t(kMaxSplitSegments) * (32 + 16);
+constexpr size_t kSplitBytesPerRow = size_t(kMaxSplitSegments) * (24 + 16) + 16;
 // Row counts up to this are reduced in one level (see distill.hip).
 constexpr int kOneLevelRows = 1024;
 

@@ -470,13 +470,10 @@ def test_verify_long_rows(osd, V, dtype):
     check_verify(osd, xg, f"long rows greedy V={V} {dtype}", max_excluded_frac=0.0)
 
 
-@pytest.mark.parametrize("kind,beta", [("fkl", 0.5), ("rkl", 0.5), ("jsd", 0.3), ("jsd", 0.0)])
-@pytest.mark.parametrize("V,dtype", [(70001, "bf16"), (40000, "f32")])
-def test_distill_long_rows(osd, kind, beta, V, dtype):
-    """Streamed distillation: three passes over each masked row pair (two for
-    FKL), zero rows for the unmasked ones; -inf entries on both sides."""
+def long_rows_case(kind, beta, V, dtype, B=2, K=3):
+    """Row pairs longer than the resident tiles, with -inf entries on both
+    sides, and a mask that leaves some rows out."""
     g = np.random.default_rng(V + int(beta * 10))
-    B, K = 2, 3
     t = g.normal(0, 2.5, (B, K, V)).astype(np.float32)
     s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
     holes = g.random((B, K, V)) < 0.1
@@ -485,6 +482,73 @@ def test_distill_long_rows(osd, kind, beta, V, dtype):
     # one-sided holes on the side that keeps the divergence finite: the
     # teacher's for FKL and JSD (p = 0 < q), the student's for RKL (q = 0 < p)
     (s if kind == "rkl" else t)[0, 1, :100] = -np.inf
-    mask = np.array([[1, 1, 0], [0, 1, 1]], np.uint8)
+    mask = (g.random((B, K)) < 0.6).astype(np.uint8)
+    mask[0, :2] = (1, 1)
+    mask[-1, -1] = 0
     tt, ss = (synth.to_bf16(t), synth.to_bf16(s)) if dtype == "bf16" else (t, s)
+    return tt, ss, mask
+
+
+# 16-byte rows (vector loads and stores) and odd rows (element accesses), up
+# to 16 segments of 8192 bf16 / 4096 fp32 logits per row.
+LONG_ROWS = [(70001, "bf16"), (131072, "bf16"), (40000, "f32"), (65535, "f32")]
+
+
+@pytest.mark.parametrize("kind,beta", [("fkl", 0.5), ("rkl", 0.5), ("jsd", 0.3), ("jsd", 0.0)])
+@pytest.mark.parametrize("V,dtype", LONG_ROWS)
+def test_distill_long_rows(osd, kind, beta, V, dtype):
+    """Split-row distillation: each row pair cut into segments that exchange
+    their statistics and partial sums; zero rows for the unmasked ones."""
+    tt, ss, mask = long_rows_case(kind, beta, V, dtype)
     check_distill(osd, tt, ss, kind, beta, 0.8, mask, f"long rows {kind} beta={beta} V={V} {dtype}")
+
+
+def test_distill_long_rows_many(osd):
+    """64 long rows at once (1024 segment workgroups), half of them masked."""
+    tt, ss, mask = long_rows_case("jsd", 0.5, 131072, "bf16", B=8, K=8)
+    check_distill(osd, tt, ss, "jsd", 0.5, 1.0, mask, "long rows many jsd")
+
+
+SPLIT_CASES = [("fkl", 0.5, 131072, "bf16"), ("jsd", 0.3, 70001, "bf16"), ("rkl", 0.5, 40000, "f32"),
+               ("jsd", 0.0, 65535, "f32")]
+
+SPLIT_FALLBACK = r'''
+import sys
+sys.path.insert(0, ".")
+import numpy as np
+from tests import test_parity_gpu as t
+import paper_2310_07177_amd as osd
+out = {}
+for kind, beta, V, dtype in t.SPLIT_CASES:
+    tt, ss, mask = t.long_rows_case(kind, beta, V, dtype)
+    loss, rows, g = t.check_distill(osd, tt, ss, kind, beta, 0.8, mask, f"fallback {kind} V={V} {dtype}")
+    for name, v in (("loss", loss), ("rows", rows), ("grad", g)):
+        out[f"{kind}{V}{dtype}{name}"] = v
+np.savez(sys.argv[1], **out)
+print("FALLBACK_OK", flush=True)
+'''
+
+
+def test_distill_long_rows_fallback_is_bit_identical(osd, tmp_path):
+    """With the bound on a segment's waits for its siblings set to 0
+    (OSD_SPLIT_POLLS, read once per process, so in a child process), every
+    segment computes its row's statistics and partial sums itself from
+    memory.  The results must equal the oracle's and, bit for bit, those of
+    the exchanging path."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    path = str(tmp_path / "fallback.npz")
+    env = dict(os.environ, OSD_SPLIT_POLLS="0")
+    r = subprocess.run([sys.executable, "-u", "-c", SPLIT_FALLBACK, path], cwd=root, env=env,
+                       capture_output=True, text=True, timeout=150)
+    print(r.stdout[-3000:], r.stderr[-3000:], flush=True)
+    assert r.returncode == 0 and "FALLBACK_OK" in r.stdout
+    got = np.load(path)
+    for kind, beta, V, dtype in SPLIT_CASES:
+        tt, ss, mask = long_rows_case(kind, beta, V, dtype)
+        loss, rows, g = run_distill(osd, tt, ss, kind, beta, 0.8, mask, None, None, None, None)
+        for name, v in (("loss", loss), ("rows", rows), ("grad", g)):
+            w = got[f"{kind}{V}{dtype}{name}"]
+            assert np.array_equal(v.view(np.uint8), w.view(np.uint8)), f"{kind} V={V} {dtype} {name}"
