@@ -83,6 +83,7 @@ struct FusedArgs {
     const uint8_t* mask;       // [B, K] distillation mask or null (all rows)
     float c2;                  // log2(e) / T
     double c2d;
+    double betad, ombd;        // beta and 1 - beta in fp64 (scalar operands of the JSD combination)
     float inv_tau;             // 1 / T
     float beta;
     uint32_t* records;         // [B, K+1], zero between calls
@@ -864,7 +865,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 block_sum2<NW>(A0, A1, s_a);
                 // Terms were accumulated in log2 units.
                 if constexpr (KIND == 2)
-                    D = kLn2 * (double(a.beta) * A0 + (1.0 - double(a.beta)) * A1);
+                    D = kLn2 * (a.betad * A0 + a.ombd * A1);
                 else if constexpr (KIND == 0)
                     D = kLn2 * A0;
                 else
@@ -1006,6 +1007,8 @@ hipError_t launch_verify_distill(const FusedLaunch& L) {
     a.mask = L.mask;
     a.c2 = float(1.4426950408889634 / double(L.temperature));
     a.c2d = double(a.c2);
+    a.betad = double(a.beta);
+    a.ombd = 1.0 - double(a.beta);
     a.inv_tau = float(1.0 / double(L.temperature));
     a.beta = L.beta;
     a.records = L.records;
