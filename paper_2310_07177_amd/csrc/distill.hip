@@ -907,7 +907,7 @@ hipError_t launch_fmt(const DistillLaunch& L, const DistillArgs& a) {
 }  // namespace
 
 hipError_t launch_distill(const DistillLaunch& L) {
-    DistillArgs a;
+    DistillArgs a{};
     a.teacher = L.teacher;
     a.tstride = L.teacher_stride;
     a.student = L.student;

@@ -386,7 +386,7 @@ bool pick_stream_tile(int V, int per_chunk, RowTile* t) {
 }
 
 hipError_t launch_distill_stream(const DistillLaunch& L) {
-    StreamDistillArgs a;
+    StreamDistillArgs a{};
     a.teacher = L.teacher;
     a.tstride = L.teacher_stride;
     a.student = L.student;

@@ -313,7 +313,7 @@ hipError_t launch_fmt(const SampleLaunch& L, const SampleArgs& a) {
 }  // namespace
 
 hipError_t launch_sample(const SampleLaunch& L) {
-    SampleArgs a;
+    SampleArgs a{};
     // One-row modes sample the row with weight 1: p when beta == 1, q when
     // beta == 0 (the row with weight 0 is never read).
     const bool q_only = L.beta == 0.0f;

@@ -657,7 +657,7 @@ bool pick_tile(int V, int per_chunk, RowTile* t) {
 }
 
 hipError_t launch_verify(const VerifyLaunch& L) {
-    VerifyArgs a;
+    VerifyArgs a{};
     a.target = L.target;
     a.draft = L.draft;
     a.B = L.B;

@@ -994,7 +994,7 @@ int fused_max_polls() {
 }
 
 hipError_t launch_verify_distill(const FusedLaunch& L) {
-    FusedArgs a;
+    FusedArgs a{};
     a.target = L.target;
     a.draft = L.draft;
     a.B = L.B;
@@ -1007,10 +1007,10 @@ hipError_t launch_verify_distill(const FusedLaunch& L) {
     a.mask = L.mask;
     a.c2 = float(1.4426950408889634 / double(L.temperature));
     a.c2d = double(a.c2);
-    a.betad = double(a.beta);
-    a.ombd = 1.0 - double(a.beta);
-    a.inv_tau = float(1.0 / double(L.temperature));
     a.beta = L.beta;
+    a.betad = double(L.beta);
+    a.ombd = 1.0 - double(L.beta);
+    a.inv_tau = float(1.0 / double(L.temperature));
     a.records = L.records;
     a.dec = L.dec;
     a.erridx = L.erridx;

@@ -228,7 +228,7 @@ bool greedy_segments(int V, int per_chunk, int* nseg) {
 }
 
 hipError_t launch_verify_greedy(const VerifyLaunch& L) {
-    SegArgs a;
+    SegArgs a{};
     a.target = L.target;
     a.B = L.B;
     a.K = L.K;

@@ -428,7 +428,7 @@ bool pick_tree_tile(int V, int per_chunk, RowTile* t) {
 }
 
 hipError_t launch_verify_tree(const TreeLaunch& L) {
-    TreeArgs a;
+    TreeArgs a{};
     a.target = L.target;
     a.draft = L.draft;
     a.B = L.B;
