@@ -82,6 +82,8 @@ __device__ inline Row decode_row(const StreamDistillArgs& a, int n, bool on) {
 template <typename Fmt, int W, int CPT, int KIND>
 __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs a) {
     constexpr int NW = W / kWave, EPC = Fmt::kPerChunk, NG = EPC / 4;
+    // JSD caches exponentials (the others, exponents): see the statistics pass.
+    constexpr bool XV = KIND == 2;
     __shared__ float s_k[2 * NW];
     __shared__ double s_s[2 * NW];
     __shared__ double s_a[2 * NW];
@@ -96,8 +98,6 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
     const float c2 = a.c2;
     const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
     const float beta = a.beta, omb = 1.0f - a.beta;
-    // JSD at beta = 0: the mixture is q itself, and every log2(q/m) is 0.
-    const bool q_only = a.beta == 0.0f;
 
     chunk_t rt[CPT], rs[CPT];
     float c1[CPT][EPC];
@@ -146,6 +146,26 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
         const bool live = cur.on;
         float kc_t = 0.0f, kc_s = 0.0f;
         double S_t = 0.0, S_s = 0.0;
+        if constexpr (XV) {
+            // JSD caches each element's 2^(x c2 - k) itself, so the thread's
+            // shift k is taken over all its chunks: every cached value is at
+            // most 1 and no sum leaves the fp32 range.
+            if (live) {
+                float mt = kNegInf, ms = kNegInf;
+#pragma unroll
+                for (int r = 0; r < CPT; ++r) {
+                    chunk_t xt = rt[r], xs = rs[r];
+                    if (r == CPT - 1 && !last_ok) {
+                        xt = pad_chunk<Fmt>();
+                        xs = pad_chunk<Fmt>();
+                    }
+                    mt = fmaxf(mt, chunk_max<Fmt>(xt));
+                    ms = fmaxf(ms, chunk_max<Fmt>(xs));
+                }
+                kc_t = shift_of_max(mt, c2);
+                kc_s = shift_of_max(ms, c2);
+            }
+        }
 #pragma unroll
         for (int r = 0; r < CPT; ++r) {
             if (live) {
@@ -154,7 +174,7 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                     xt = pad_chunk<Fmt>();
                     xs = pad_chunk<Fmt>();
                 }
-                if (r == 0) {
+                if (!XV && r == 0) {
                     kc_t = first_chunk_shift<Fmt>(xt, c2);
                     kc_s = first_chunk_shift<Fmt>(xs, c2);
                 }
@@ -168,18 +188,24 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                         const float t = Fmt::get(xt, e), s = Fmt::get(xs, e);
                         const float vt = __builtin_fmaf(t, c2, -kc_t);
                         const float vs = __builtin_fmaf(s, c2, -kc_s);
+                        const float et = exp2_fast(vt), es = exp2_fast(vs);
                         // (the first term starts the sums: 0 + x would cost an add)
-                        st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
-                        ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
-                        // Both exponents, for every kind: each side's
-                        // probability is rebuilt from its own exponent, so
-                        // a -inf logit on either side alone gives that side
-                        // 0 and the other its true value.  One floor
-                        // suffices: with the target's exponent finite, a
-                        // draft exponent of -inf still gives q = 0, and two
-                        // -inf exponents give a finite difference.
-                        c0v[j] = fmaxf(vt, kLogFloor);
-                        c1[r][e] = vs;
+                        st = e == 0 ? et : st + et;
+                        ss = e == 0 ? es : ss + es;
+                        if constexpr (XV) {
+                            c0v[j] = et;
+                            c1[r][e] = es;
+                        } else {
+                            // Both exponents: each side's probability is
+                            // rebuilt from its own exponent, so a -inf logit
+                            // on either side alone gives that side 0 and the
+                            // other its true value.  One floor suffices: with
+                            // the target's exponent finite, a draft exponent
+                            // of -inf still gives q = 0, and two -inf
+                            // exponents give a finite difference.
+                            c0v[j] = fmaxf(vt, kLogFloor);
+                            c1[r][e] = vs;
+                        }
                     }
                     lc.store(r, g, f32x4_t{c0v[0], c0v[1], c0v[2], c0v[3]});
                 }
@@ -206,10 +232,10 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             // Exponent range exceeded by an element far above the first
             // chunk's maximum: rescale exactly from the cached exponents.
             float ks_t = kc_t, ks_s = kc_s;
-            if (S_t >= 1.0e300) {  // (a NaN sum stays NaN: it marks a NaN logit)
+            if (!XV && S_t >= 1.0e300) {  // (a NaN sum stays NaN: it marks a NaN logit)
                 ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float { return lc.load(r, e / 4)[e % 4]; });
             }
-            if (S_s >= 1.0e300) {
+            if (!XV && S_s >= 1.0e300) {
                 ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float { return c1[r][e]; });
             }
             float Kt = ks_t, Ks = ks_s;
@@ -224,6 +250,10 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             // exponents as the sums (so the normalisers and the log-ratios
             // agree: rows with p ~ q keep their small divergence accurate).
             const float dTk = float(dTd - double(kc_t - kc_s));
+            // JSD: p = e_t at and q = e_s as, the cached values times the
+            // thread's scale 2^(k - K) / S (fp64, rounded once).
+            const float at = float(__builtin_ldexp(1.0 / St, int(fmaxf(kc_t - Kt, -2048.0f))));
+            const float as = float(__builtin_ldexp(1.0 / Ss, int(fmaxf(kc_s - Ks, -2048.0f))));
 
             // ---- loss pass (from the cache) ----
             float acc0 = 0.0f, acc1 = 0.0f;
@@ -238,16 +268,18 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
                     for (int j = 0; j < 4; ++j) {
                         const int e = 4 * g + j;
                         if constexpr (KIND == 2) {
-                            const float lp = c0v[j] - ct, lq = c1[r][e] - cs;
-                            // log2 m = lp + L, L = log2(beta + (1 - beta) 2^(lq - lp)): the
-                            // mixture's log relative to p, a number near 0 when p ~ q, so the
-                            // rounding of log2 m does not bias every term of a small divergence.
-                            // The ratio is clamped to 2^+-126; both limits stay exact enough
-                            // (the vanishing side carries no weight).
-                            const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
-                            const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
-                            const float p = exp2_fast(lp), q = exp2_fast(lq);
-                            const float x = q_only ? 0.0f : d - L;  // log2(q/m); m = q at beta = 0
+                            const float p = c0v[j] * at, q = c1[r][e] * as;
+                            // rho = q/p, clamped to 2^+-126 (both limits stay exact enough:
+                            // the vanishing side carries no weight).  log2 m = log2 p + L,
+                            // L = log2(beta + (1 - beta) rho): the mixture's log relative
+                            // to p, a number near 0 when p ~ q, so the rounding of a log
+                            // does not bias every term of a small divergence.  At beta = 0,
+                            // L is d itself (the same log of the same value): x = 0.
+                            const float rho = __builtin_amdgcn_fmed3f(
+                                q * __builtin_amdgcn_rcpf(fmaxf(p, 0x1p-126f)), 0x1p-126f, 0x1p126f);
+                            const float d = log2_fast(rho);
+                            const float L = log2_fast(__builtin_fmaf(omb, rho, beta));
+                            const float x = d - L;  // log2(q/m)
                             a0 = __builtin_fmaf(p, -L, a0);
                             a1 = __builtin_fmaf(q, x, a1);
                             c0v[j] = x;

@@ -84,10 +84,15 @@ __device__ inline float scalar_load_logit(const void* row, int j) {
 // later exponent is taken relative to it; a row whose later elements exceed
 // it by more than the fp32 exponent range is caught by the caller (the sum
 // overflows) and rescaled exactly.
+// The shift of a maximum m: ceil(m * c2), or 0 when m is not finite.
+__device__ inline float shift_of_max(float m, float c2) {
+    const float k = ceilf(m * c2);
+    return (k > -3.0e38f && k < 3.0e38f) ? k : 0.0f;
+}
+
 template <typename Fmt>
 __device__ inline float first_chunk_shift(const chunk_t& c, float c2) {
-    const float k = ceilf(chunk_max<Fmt>(c) * c2);
-    return (k > -3.0e38f && k < 3.0e38f) ? k : 0.0f;
+    return shift_of_max(chunk_max<Fmt>(c), c2);
 }
 
 // The thread index through an opaque copy: lane and wave numbers derived from

@@ -113,8 +113,18 @@ struct Meta {
     int on;  // distillation mask flag; in the error-index mode: every proposal of the sequence is in [0, V)
 };
 
-__device__ inline Meta load_meta(const FusedArgs& a, int it) {
+// An item's arguments in two steps, so that the loads are issued before the
+// first rows and waited for after them: issue_meta reads every word the
+// item needs (in the error-index mode also all K proposals of its sequence,
+// K <= 16), finish_meta combines them.
+struct MetaLoads {
     Meta m;
+    int32_t seq[OSD_MAX_K];
+};
+
+__device__ inline MetaLoads issue_meta(const FusedArgs& a, int it) {
+    MetaLoads r;
+    Meta& m = r.m;
     const int BK = a.B * a.K;
     const bool bonus = it >= BK;
     const int i = bonus ? 0 : it / a.B;
@@ -124,17 +134,22 @@ __device__ inline Meta load_meta(const FusedArgs& a, int it) {
     m.y = bonus ? 0 : a.tokens[ti];
     m.u = bonus ? 0.0f : a.u_accept[ti];
     m.u_res = a.u_resample[b];
+    m.on = a.erridx ? 0 : (bonus ? 0 : (a.mask ? int(a.mask[ti]) : 1));
+#pragma unroll
+    for (int j = 0; j < OSD_MAX_K; ++j) r.seq[j] = (a.erridx && j < a.K) ? a.tokens[int64_t(b) * a.K + j] : 0;
+    return r;
+}
+
+__device__ inline Meta finish_meta(const FusedArgs& a, const MetaLoads& r) {
+    Meta m = r.m;
     if (a.erridx) {
         // A proposal outside the vocabulary invalidates the whole sequence,
         // wherever it sits: its rejected row is then not distilled.
         int ok = m.kb >= 1 && m.kb <= a.K;
-        for (int j = 0; ok && j < m.kb; ++j) {
-            const int32_t yj = a.tokens[int64_t(b) * a.K + j];
-            ok = yj >= 0 && yj < a.V;
-        }
+#pragma unroll
+        for (int j = 0; j < OSD_MAX_K; ++j)
+            if (j < m.kb) ok = ok && r.seq[j] >= 0 && r.seq[j] < a.V;
         m.on = ok;
-    } else {
-        m.on = bonus ? 0 : (a.mask ? int(a.mask[ti]) : 1);
     }
     return m;
 }
@@ -199,21 +214,52 @@ __device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
     return t;
 }
 
+// The items of workgroup g of G: the row pairs g, g + G, ... below B*K, then
+// the bonus rows b < B with (K-1)*B + b = g (mod G).  Each bonus row goes to
+// the workgroup that tests position K-1 of its sequence: by the time that
+// position is tested an earlier rejection of the sequence is usually posted,
+// so its items seldom draw, while the workgroups of position 0 draw for most
+// sequences.  Row pairs k and k - seq_step of a workgroup share a sequence;
+// a bonus row shares its sequence with the workgroup's row pair at position
+// K-1.  Every field is uniform over the workgroup.
+struct Schedule {
+    int g, G, B, BK, nrp, b0, nk, seq_step;
+    __device__ int item(int k) const { return k < nrp ? g + k * G : BK + b0 + (k - nrp) * G; }
+    // The latest earlier item of the workgroup in the same sequence, or < 0.
+    __device__ int prev_same(int k) const {
+        if (k < nrp) return k - seq_step;
+        const int b = b0 + (k - nrp) * G;
+        return (BK - B + b - g) / G;
+    }
+};
+
+__device__ inline Schedule make_schedule(const FusedArgs& a, int g, int G) {
+    Schedule s;
+    s.g = g;
+    s.G = G;
+    s.B = a.B;
+    s.BK = a.B * a.K;
+    s.nrp = g < s.BK ? (s.BK - g + G - 1) / G : 0;
+    s.b0 = ((g - (s.BK - a.B)) % G + G) % G;
+    s.nk = s.nrp + (s.b0 < a.B ? (a.B - s.b0 + G - 1) / G : 0);
+    s.seq_step = a.seq_step;
+    return s;
+}
+
 // s_rej[k] = 1 if item k of this workgroup or an earlier item of the same
-// sequence ended the test (or could not be tested).  The previous item of
-// the same sequence is k - seq_step.  Read after a barrier of item k (every
-// item has one), the entries up to k - 1 are visible.
-__device__ inline bool known_rejection(const uint8_t* s_rej, int k, int seq_step) {
-    const int kk = k - seq_step;
+// sequence ended the test (or could not be tested).  Read after a barrier of
+// item k (every item has one), the entries up to k - 1 are visible.
+__device__ inline bool known_rejection(const uint8_t* s_rej, const Schedule& sc, int k) {
+    const int kk = sc.prev_same(k);
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
 }
 // The same, asked at the start of item k - 1 (to decide whether item k's
 // rows are read).  Items end without a workgroup barrier, so only entries up
 // to k - 3 are certainly visible to every wave then (entry j is written by
 // thread 0 at the end of item j, before it reaches a barrier of item j + 1).
-__device__ inline bool known_rejection_ahead(const uint8_t* s_rej, int k, int seq_step) {
-    int kk = k - seq_step;
-    while (kk > k - 3) kk -= seq_step;
+__device__ inline bool known_rejection_ahead(const uint8_t* s_rej, const Schedule& sc, int k) {
+    int kk = sc.prev_same(k);
+    while (kk > k - 3) kk = sc.prev_same(kk);
     return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
 }
 
@@ -389,6 +435,13 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     const int j = tid & (seg - 1), base = lane & ~(seg - 1);
     const uint64_t segmask = (seg == 32 ? 0xFFFFFFFFull : 0xFFFFull) << base;
     const int nchunks = int(a.row_bytes / 16);
+    // The loss partials and the mask are requested before the records, so
+    // that one round trip brings all of them.
+    double sm = 0.0, cn = 0.0;
+    if (!a.erridx) {
+        for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
+        for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
+    }
     double esum = 0.0, ecnt = 0.0;  // error-index mode: this thread's sequences, in order
     for (int b0 = 0; b0 < a.B; b0 += per_pass) {
         const int b = b0 + tid / seg;
@@ -446,13 +499,9 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
             if (tid == 0) s_nextra = 0;
         }
     }
-    double sm = 0.0, cn = 0.0;
     if (a.erridx) {
         sm = esum;
         cn = ecnt;
-    } else {
-        for (int g = tid; g < G; g += W) sm += take_f64(&a.part_ws[g]);
-        for (int r = tid; r < a.nrows; r += W) cn += (a.mask == nullptr || a.mask[r] != 0) ? 1.0 : 0.0;
     }
     sm = wave_sum(sm);
     cn = wave_sum(cn);
@@ -476,6 +525,8 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
 template <typename Fmt, int W, int CPT, int KIND>
 __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     constexpr int NW = W / kWave, EPC = Fmt::kPerChunk, NG = EPC / 4;
+    // JSD caches exponentials (the others, exponents): see the statistics pass.
+    constexpr bool XV = KIND == 2;
     // Items end without a barrier, so a wave can be one item ahead of
     // another: the scratch written once per item is double-buffered by item
     // parity (every item has at least one barrier, so never two ahead).
@@ -492,6 +543,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ double s_part[1];
     __shared__ FusedTail s_tail;
     __shared__ f32x4_t s_c0[CPT * NG * W];
+    __shared__ double s_ln2;
     const LdsCache<W, EPC> lc{s_c0};
 
     const int tid = threadIdx.x;
@@ -499,15 +551,15 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     const float c2 = a.c2;
     const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
     const float beta = a.beta, omb = 1.0f - a.beta;
-    // JSD at beta = 0: the mixture is q itself, and every log2(q/m) is 0.
-    const bool q_only = a.beta == 0.0f;
 
     chunk_t rt[CPT], rs[CPT];
     float c1[CPT][EPC];
 
-    const int nk = (a.nitems - int(blockIdx.x) + G - 1) / G;
+    const Schedule sc = make_schedule(a, int(blockIdx.x), G);
+    const int nk = sc.nk;
     for (int j = tid; j < kMaxItems; j += W) s_rej[j] = 0;  // ordered before any read by the staging barrier
     if (tid == 0) {
+        s_ln2 = kLn2;     // ordered before any read by the prologue's barrier
         s_part[0] = 0.0;  // read and written by thread 0 only
         s_tail.part_ws = a.part_ws;
         s_tail.done = a.done;
@@ -528,11 +580,38 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         s_tail.B = a.B;
         s_tail.K = a.K;
     }
-    // The pipeline starts one step early: step -1 computes nothing; it issues
-    // the loads of the first item from the same code as every later step and
-    // then stages the item arguments.  The first item's rows are read before its
-    // arguments are known (in bounds either way; a bonus row, whose index is
-    // k_b, reads k_b directly).
+    // Prologue: the item arguments are requested first (a few words per
+    // item), then the first item's rows, so that waiting for the arguments
+    // does not wait for the rows (loads complete in order) and the first
+    // statistics pass folds its chunks in as they land.  The first item's
+    // rows are requested before its arguments are known (in bounds either
+    // way; a bonus row, whose index is k_b, reads k_b directly).
+    {
+        const int t = opaque_tid();
+        MetaLoads ml{};
+        if (t < nk) ml = issue_meta(a, sc.item(t));
+        Meta m0;
+        m0.kb = a.K;
+        m0.y = 0;
+        m0.u = 0.0f;
+        m0.u_res = 0.0f;
+        m0.on = 1;
+        const int it0 = sc.item(0);
+        if (it0 >= sc.BK && it0 < a.nitems && a.draft_len) m0.kb = scalar_load(a.draft_len + (it0 - sc.BK));
+        const Item first = decode_item<Fmt>(a, it0, m0);
+        const bool fload = first.trow != nullptr;
+        const rsrc_t ftr = make_rsrc(fload ? first.trow : a.target, fload ? a.row_bytes : 0u);
+        const rsrc_t fsr =
+            make_rsrc(fload && first.drow ? first.drow : a.target, fload && first.drow ? a.row_bytes : 0u);
+#pragma unroll
+        for (int r = 0; r < CPT; ++r) {
+            rt[r] = load_chunk<W>(ftr, r);
+            rs[r] = load_chunk<W>(fsr, r);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (t < nk) s_meta[t] = finish_meta(a, ml);
+        __syncthreads();
+    }
     Item cur;
     cur.vkind = kItemNone;
     cur.dist = false;
@@ -546,22 +625,12 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     cur.drow = nullptr;
     cur.grow = -1;
     int cur_skip = 0;
-    for (int k = -1, it = int(blockIdx.x) - G; it < a.nitems; it += G, ++k) {
+    for (int k = 0; k < nk; ++k) {
+        const int it = sc.item(k);
         Item nxt;
         bool nload;
         int nxt_skip = 0;
-        if (k < 0) {
-            Meta m0;
-            m0.kb = a.K;
-            m0.y = 0;
-            m0.u = 0.0f;
-            m0.u_res = 0.0f;
-            m0.on = 1;
-            if (it + G >= a.B * a.K && it + G < a.nitems && a.draft_len)
-                m0.kb = scalar_load(a.draft_len + (it + G - a.B * a.K));
-            nxt = decode_item<Fmt>(a, it + G, m0);
-            nload = nxt.trow != nullptr;
-        } else {
+        {
             Meta mn;
             mn.kb = 0;
             mn.y = 0;
@@ -569,18 +638,18 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             mn.u_res = 0.0f;
             mn.on = 0;
             if (k + 1 < nk) mn = meta_at(s_meta, k + 1);
-            nxt = decode_item<Fmt>(a, it + G, mn);
+            nxt = decode_item<Fmt>(a, k + 1 < nk ? sc.item(k + 1) : a.nitems, mn);
             nload = nxt.trow != nullptr;
             // A bonus row whose sequence already stopped here is not read
             // (the current item's outcome is not known yet).
-            if (nload && nxt.bonus && known_rejection_ahead(s_rej, k + 1, a.seq_step)) {
+            if (nload && nxt.bonus && known_rejection_ahead(s_rej, sc, k + 1)) {
                 nload = false;
                 nxt_skip = 1;
             }
         }
         const rsrc_t ntr = make_rsrc(nload ? nxt.trow : a.target, nload ? a.row_bytes : 0u);
         const rsrc_t nsr = make_rsrc(nload && nxt.drow ? nxt.drow : a.target, nload && nxt.drow ? a.row_bytes : 0u);
-        if (k >= 0) cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
+        cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
         // A bonus row is needed only if every proposal of its sequence is
         // accepted.  Besides this workgroup's own outcomes, the decisions
         // that any workgroup has posted so far are consulted (each is
@@ -588,7 +657,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         // is not needed.  Wave 0 reads them (k_b <= 16 lanes); the bonus
         // rows come last, when most are posted.
         bool bonus_stop = false;
-        if (cur.bonus && cur.vkind == kItemLive && !cur_skip && k >= 0) {
+        if (cur.bonus && cur.vkind == kItemLive && !cur_skip) {
             const int t = opaque_tid();  // nothing tid-derived is kept across the loop
             if (t < kWave) {
                 uint32_t d = 0u;
@@ -597,21 +666,41 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 if (t == 0) s_flag[k & 1] = m != 0 ? 1 : 0;
             }
             __syncthreads();
-            bonus_stop = s_flag[k & 1] != 0 || known_rejection(s_rej, k, a.seq_step);
+            bonus_stop = s_flag[k & 1] != 0 || known_rejection(s_rej, sc, k);
         }
         const bool vlive = cur.vkind == kItemLive && !cur_skip && !bonus_stop;
         const bool live = vlive || cur.dist;
         const int ychunk = cur.y / EPC;
-        const rsrc_t gr = make_rsrc(a.grad_out && cur.grow >= 0 && k >= 0
+        const rsrc_t gr = make_rsrc(a.grad_out && cur.grow >= 0
                                         ? static_cast<char*>(a.grad_out) + int64_t(cur.grow) * a.row_bytes
                                         : static_cast<char*>(nullptr),
-                                    a.grad_out && cur.grow >= 0 && k >= 0 ? a.row_bytes : 0u);
+                                    a.grad_out && cur.grow >= 0 ? a.row_bytes : 0u);
         double D = 0.0;
         // ---- statistics pass: consumes the raw chunks and reloads each with
         // the next item's (one load sequence for every item: a branch around
         // the loads would make the compiler wait for all of them) ----
         float kc_t = 0.0f, kc_s = 0.0f;
         double S_t = 0.0, S_s = 0.0;
+        if constexpr (XV) {
+            // JSD caches each element's 2^(x c2 - k) itself, so the thread's
+            // shift k is taken over all its chunks: every cached value is at
+            // most 1 and no sum leaves the fp32 range.
+            if (live) {
+                float mt = kNegInf, ms = kNegInf;
+#pragma unroll
+                for (int r = 0; r < CPT; ++r) {
+                    chunk_t xt = rt[r], xs = rs[r];
+                    if (r == CPT - 1 && !last_ok) {
+                        xt = pad_chunk<Fmt>();
+                        xs = pad_chunk<Fmt>();
+                    }
+                    mt = fmaxf(mt, chunk_max<Fmt>(xt));
+                    ms = fmaxf(ms, chunk_max<Fmt>(xs));
+                }
+                kc_t = shift_of_max(mt, c2);
+                kc_s = shift_of_max(ms, c2);
+            }
+        }
 #pragma unroll
         for (int r = 0; r < CPT; ++r) {
             if (live) {
@@ -624,7 +713,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     s_y[k & 1][0] = Fmt::get(xt, cur.y - ychunk * EPC);
                     s_y[k & 1][1] = Fmt::get(xs, cur.y - ychunk * EPC);
                 }
-                if (r == 0) {
+                if (!XV && r == 0) {
                     kc_t = first_chunk_shift<Fmt>(xt, c2);
                     kc_s = first_chunk_shift<Fmt>(xs, c2);
                 }
@@ -638,18 +727,24 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         const float t = Fmt::get(xt, e), s = Fmt::get(xs, e);
                         const float vt = __builtin_fmaf(t, c2, -kc_t);
                         const float vs = __builtin_fmaf(s, c2, -kc_s);
+                        const float et = exp2_fast(vt), es = exp2_fast(vs);
                         // (the first term starts the sums: 0 + x would cost an add)
-                        st = e == 0 ? exp2_fast(vt) : st + exp2_fast(vt);
-                        ss = e == 0 ? exp2_fast(vs) : ss + exp2_fast(vs);
-                        // Both exponents, for every kind: each side's
-                        // probability is rebuilt from its own exponent, so
-                        // a -inf logit on either side alone gives that side
-                        // 0 and the other its true value.  One floor
-                        // suffices: with the target's exponent finite, a
-                        // draft exponent of -inf still gives q = 0, and two
-                        // -inf exponents give a finite difference.
-                        c0v[j] = fmaxf(vt, kLogFloor);
-                        c1[r][e] = vs;
+                        st = e == 0 ? et : st + et;
+                        ss = e == 0 ? es : ss + es;
+                        if constexpr (XV) {
+                            c0v[j] = et;
+                            c1[r][e] = es;
+                        } else {
+                            // Both exponents: each side's probability is
+                            // rebuilt from its own exponent, so a -inf logit
+                            // on either side alone gives that side 0 and the
+                            // other its true value.  One floor suffices: with
+                            // the target's exponent finite, a draft exponent
+                            // of -inf still gives q = 0, and two -inf
+                            // exponents give a finite difference.
+                            c0v[j] = fmaxf(vt, kLogFloor);
+                            c1[r][e] = vs;
+                        }
                     }
                     lc.store(r, g, f32x4_t{c0v[0], c0v[1], c0v[2], c0v[3]});
                 }
@@ -662,11 +757,6 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             rs[r] = load_chunk<W>(nsr, r);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (k < 0) {  // step -1: stage the item arguments (read after the first rows were requested)
-            const int t = opaque_tid();
-            if (t < nk) s_meta[t] = load_meta(a, int(blockIdx.x) + t * G);
-            __syncthreads();
-        }
         // The record of an item that is not tested (a proposal outside the
         // vocabulary, or a bonus row known to be unneeded); a tested item
         // replaces it below.  Its row may still be distilled.
@@ -678,7 +768,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         if (cur.vkind == kItemBadToken) {
             record = make_rec(kRecBadToken, 0);
             stopped = true;
-            if (opaque_tid() == 0 && k >= 0) __hip_atomic_exchange(dec_at, uint32_t(kDecStop), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (opaque_tid() == 0) __hip_atomic_exchange(dec_at, uint32_t(kDecStop), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         } else if (cur.vkind == kItemLive && !vlive) {
             record = make_rec(kRecBonusSkipped, 0);
             stopped = true;
@@ -693,10 +783,10 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             // Exponent range exceeded by an element far above the first
             // chunk's maximum: rescale exactly from the cache.
             float ks_t = kc_t, ks_s = kc_s;
-            if (S_t >= 1.0e300) {  // (a NaN sum stays NaN: it marks a NaN logit)
+            if (!XV && S_t >= 1.0e300) {  // (a NaN sum stays NaN: it marks a NaN logit)
                 ks_t = kc_t + rescue_sum<CPT, EPC>(S_t, [&](int r, int e) -> float { return lc.load(r, e / 4)[e % 4]; });
             }
-            if (S_s >= 1.0e300) {
+            if (!XV && S_s >= 1.0e300) {
                 ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float { return c1[r][e]; });
             }
             float Kt = ks_t, Ks = ks_s;
@@ -711,12 +801,16 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             // exponents as the sums (so the normalisers and the log-ratios
             // agree: rows with p ~ q keep their small divergence accurate).
             const float dTk = float(dTd - double(kc_t - kc_s));
+            // JSD: p = e_t at and q = e_s as, the cached values times the
+            // thread's scale 2^(k - K) / S (fp64, rounded once).
+            const float at = float(__builtin_ldexp(1.0 / St, int(fmaxf(kc_t - Kt, -2048.0f))));
+            const float as = float(__builtin_ldexp(1.0 / Ss, int(fmaxf(kc_s - Ks, -2048.0f))));
 
             // ---- verification ----
             bool spec = false;  // drew without knowing the earlier positions' outcomes
             if (vlive) {
                 const bool bad = !(St > 0.0 && St < 1.0e300) || (!cur.bonus && !(Ss > 0.0 && Ss < 1.0e300));
-                const bool earlier = known_rejection(s_rej, k, a.seq_step);
+                const bool earlier = known_rejection(s_rej, sc, k);
                 bool want_draw = false;
                 if (bad) {
                     record = make_rec(kRecBadRow, 0);
@@ -768,10 +862,16 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                     // Element masses from the cache; the sums and the walk
                     // evaluate exactly this formula on the same values.
                     auto formula = [&](float c0, float cc1, bool residual) -> float {
-                        const float lp = c0 - ct, lq = cc1 - cs;
-                        const float p = exp2_fast(lp);
-                        if (!residual) return p;
-                        return fmaxf(p - exp2_fast(lq), 0.0f);
+                        if constexpr (XV) {
+                            const float p = c0 * at;
+                            if (!residual) return p;
+                            return fmaxf(p - cc1 * as, 0.0f);
+                        } else {
+                            const float lp = c0 - ct, lq = cc1 - cs;
+                            const float p = exp2_fast(lp);
+                            if (!residual) return p;
+                            return fmaxf(p - exp2_fast(lq), 0.0f);
+                        }
                     };
                     auto mass = [&](int r, int e, bool residual) -> float {
                         return formula(lc.load(r, e / 4)[e % 4], c1[r][e], residual);
@@ -807,7 +907,6 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             const uint32_t rst = record >> 28;
             const bool dist_now = a.erridx ? (rst == kRecReject || rst == kRecRejectSpec) : cur.dist;
             distilled = dist_now;
-            release_rows = a.erridx && spec && dist_now;
 
             // ---- distillation ----
             if (dist_now) {
@@ -823,16 +922,18 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         for (int j = 0; j < 4; ++j) {
                             const int e = 4 * g + j;
                             if constexpr (KIND == 2) {
-                                const float lp = c0v[j] - ct, lq = c1[r][e] - cs;
-                                // log2 m = lp + L, L = log2(beta + (1 - beta) 2^(lq - lp)): the
-                                // mixture's log relative to p, a number near 0 when p ~ q, so the
-                                // rounding of log2 m does not bias every term of a small divergence.
-                                // The ratio is clamped to 2^+-126; both limits stay exact enough
-                                // (the vanishing side carries no weight).
-                                const float d = __builtin_amdgcn_fmed3f(lq - lp, -126.0f, 126.0f);
-                                const float L = log2_fast(__builtin_fmaf(omb, exp2_fast(d), beta));
-                                const float p = exp2_fast(lp), q = exp2_fast(lq);
-                                const float x = q_only ? 0.0f : d - L;  // log2(q/m); m = q at beta = 0
+                                const float p = c0v[j] * at, q = c1[r][e] * as;
+                                // rho = q/p, clamped to 2^+-126 (both limits stay exact enough:
+                                // the vanishing side carries no weight).  log2 m = log2 p + L,
+                                // L = log2(beta + (1 - beta) rho): the mixture's log relative
+                                // to p, a number near 0 when p ~ q, so the rounding of a log
+                                // does not bias every term of a small divergence.  At beta = 0,
+                                // L is d itself (the same log of the same value): x = 0.
+                                const float rho = __builtin_amdgcn_fmed3f(
+                                    q * __builtin_amdgcn_rcpf(fmaxf(p, 0x1p-126f)), 0x1p-126f, 0x1p126f);
+                                const float d = log2_fast(rho);
+                                const float L = log2_fast(__builtin_fmaf(omb, rho, beta));
+                                const float x = d - L;  // log2(q/m)
                                 a0 = __builtin_fmaf(p, -L, a0);
                                 a1 = __builtin_fmaf(q, x, a1);
                                 c0v[j] = x;
@@ -863,15 +964,16 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                 }
                 double A0 = double(acc0), A1 = KIND == 2 ? double(acc1) : 0.0;
                 block_sum2<NW>(A0, A1, s_a);
-                // Terms were accumulated in log2 units.
+                // Terms were accumulated in log2 units.  (ln 2 is read from
+                // LDS here rather than held in registers across the item loop.)
+                const double ln2d = s_ln2;
                 if constexpr (KIND == 2)
-                    D = kLn2 * (a.betad * A0 + a.ombd * A1);
+                    D = ln2d * (a.betad * A0 + a.ombd * A1);
                 else if constexpr (KIND == 0)
-                    D = kLn2 * A0;
+                    D = ln2d * A0;
                 else
-                    D = -kLn2 * A0;
-
-                if (a.grad_out) {
+                    D = -ln2d * A0;
+                if (a.grad_out && distilled) {
                     const float ln2 = float(kLn2);
                     // JSD: (1-beta) ln2/tau * q * (x - KL2);  RKL: ln2/tau * q * (A0 - lr)
                     const float scale = KIND == 2 ? omb * ln2 * a.inv_tau : ln2 * a.inv_tau;
@@ -898,16 +1000,18 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         __builtin_amdgcn_sched_barrier(0);
                     }
                 }
-            } else if (cur.grow >= 0 && a.grad_out) {
+            }
+            if (!distilled && cur.grow >= 0 && a.grad_out) {
 #pragma unroll
                 for (int r = 0; r < CPT; ++r) store_chunk<W>(gr, r, chunk_t{0u, 0u, 0u, 0u});
             }
+            release_rows = a.erridx && spec && distilled;
         }
         if (release_rows) {  // every wave's gradient stores complete before the release below
             wait_memory();
             __syncthreads();
         }
-        if (tid == 0 && k >= 0) {
+        if (tid == 0) {
             if (cur.grow >= 0) {
                 if (a.row_loss_out) a.row_loss_out[cur.grow] = float(D);
                 if (!a.erridx)
@@ -921,7 +1025,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             if (cur.vkind != kItemNone)  // posted at the coherence point; waited for once, at the end
                 __hip_atomic_exchange(&a.records[int64_t(cur.b) * (a.K + 1) + cur.i], record, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
-            if (k < kMaxItems) s_rej[k] = (stopped || known_rejection(s_rej, k, a.seq_step)) ? 1 : 0;
+            if (k < kMaxItems) s_rej[k] = (stopped || known_rejection(s_rej, sc, k)) ? 1 : 0;
         }
         cur_skip = nxt_skip;
     }
@@ -942,9 +1046,11 @@ int blocks_per_cu() {
 template <typename Fmt, int W, int CPT, int KIND>
 hipError_t launch_kind(const FusedLaunch& L, FusedArgs a) {
     int64_t want = int64_t(L.cus) * blocks_per_cu<Fmt, W, CPT, KIND>();
-    const int64_t min_grid = (int64_t(a.nitems) + kMaxItems - 1) / kMaxItems;
+    // Each workgroup stages at most ceil(BK/G) + ceil(B/G) <= nitems/G + 2 items.
+    const int64_t min_grid = (int64_t(a.nitems) + kMaxItems - 3) / (kMaxItems - 2);
     if (want < min_grid) want = min_grid;
-    const unsigned grid = unsigned(want < a.nitems ? want : a.nitems);
+    const int64_t BK = int64_t(a.B) * a.K;
+    const unsigned grid = unsigned(want < BK ? want : BK);
     int g = int(grid), r = a.B;
     while (r != 0) {
         const int t = g % r;
