@@ -30,6 +30,8 @@
 // the records of every sequence into the outputs.
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "osd.h"
 #include "osd_device.hpp"
 #include "osd_internal.hpp"
@@ -277,19 +279,22 @@ __device__ inline int poll_decisions(const uint32_t* dec, int i, int polls) {
     return 0;
 }
 
-// Inverse-CDF draw over the cached row pair.  mass(r, e, residual) gives the
-// fp32 mass of element e of round r (residual: max(0, p - q); else p) and
-// mass_at(rr, e, residual) the same for a round rr known only at run time.
-// Token order is chunk order c = r*W + tid, then element; the cells are
-// (round r, wave w, lane).  Pass A sums each thread's chunks exactly in fixed
-// point and posts each (round, wave) total; one wave scans them
-// (CPT*NW <= 64 cells).  The wave whose cell holds u*Z recomputes that
-// round's chunk sums -- the same fp32 additions of the same values -- finds
-// the lane, and the lane walks its elements.  Returns the token (uniform),
-// or -1 if there is no mass at all.  All threads call it.
-template <int W, int CPT, int EPC, typename MassFn, typename MassAtFn>
-__device__ int draw_cached(MassFn mass, MassAtFn mass_at, bool residual, float u, unsigned long long* s_cell,
-                           unsigned long long* s_z, int* s_tok) {
+// Inverse-CDF draw over the cached row pair.  mass(r, e) gives the fp32
+// mass of element e of round r (RESIDUAL: max(0, p - q); else p) and
+// mass_at(rr, e) the same for a round rr known only at run time.  Token order
+// is chunk order c = r*W + tid, then element; the cells are (round r, wave w,
+// lane).  Masses become 2^-40 fixed point, held as whole numbers in fp64
+// (every sum below stays under 2^53, so each is exact): the chunk sum x, an
+// fp32 sum of at most 8 masses of at most 1, becomes floor(x 2^40).  Pass A
+// posts each (round, wave) total; one wave scans them (CPT*NW <= 64 cells).
+// The wave whose cell holds u*Z recomputes that round's chunk sums -- the
+// same fp32 additions of the same values -- finds the lane, and the lane
+// walks its elements.  Returns the token (uniform), or -1 if there is no mass
+// at all.  All threads call it.
+__device__ inline double fixed40(float x) { return floor(double(x) * 0x1p40); }
+
+template <int W, int CPT, int EPC, bool RESIDUAL, typename MassFn, typename MassAtFn>
+__device__ int draw_cached(MassFn mass, MassAtFn mass_at, float u, double* s_cell, double* s_z, int* s_tok) {
     constexpr int NW = W / kWave, CELLS = CPT * NW;
     static_assert(CELLS <= kWave, "one wave scans the cells");
     const int tid = opaque_tid(), lane = tid & (kWave - 1), wid = tid / kWave;
@@ -297,32 +302,32 @@ __device__ int draw_cached(MassFn mass, MassAtFn mass_at, bool residual, float u
     for (int r = 0; r < CPT; ++r) {
         float sm = 0.0f;
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) sm = sm + mass(r, e, residual);
-        const uint64_t incl = wave_scan_add(to_fixed<kFixedShift>(sm));
+        for (int e = 0; e < EPC; ++e) sm = sm + mass(r, e);
+        const double incl = wave_scan_add(fixed40(sm));
         if (lane == kWave - 1) s_cell[r * NW + wid] = incl;
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
     if (wid == 0) {
-        const uint64_t cv = lane < CELLS ? uint64_t(s_cell[lane]) : 0;
-        const uint64_t ci = wave_scan_add(cv);
+        const double cv = lane < CELLS ? s_cell[lane] : 0.0;
+        const double ci = wave_scan_add(cv);
         if (lane < CELLS) s_cell[lane] = ci - cv;  // exclusive prefix
         if (lane == kWave - 1) *s_z = ci;
         if (lane == 0) *s_tok = -1;
     }
     __syncthreads();
-    const uint64_t Z = *s_z;
+    const double Z = *s_z;
     int tok = -1;
-    if (Z > 0) {
-        uint64_t target = static_cast<uint64_t>(double(u) * double(Z));
-        if (target >= Z) target = Z - 1;
+    if (Z > 0.0) {
+        double target = floor(double(u) * Z);
+        if (target >= Z) target = Z - 1.0;
         // The round whose cell of this wave holds the target (uniform).
         int rr = -1;
-        uint64_t lo = 0;
+        double lo = 0.0;
         for (int r = 0; r < CPT; ++r) {
             const int c = r * NW + wid;
-            const uint64_t l = s_cell[c];
-            const uint64_t h = c + 1 < CELLS ? uint64_t(s_cell[c + 1]) : Z;
+            const double l = s_cell[c];
+            const double h = c + 1 < CELLS ? s_cell[c + 1] : Z;
             if (l <= target && target < h) {
                 rr = r;
                 lo = l;
@@ -333,20 +338,20 @@ __device__ int draw_cached(MassFn mass, MassAtFn mass_at, bool residual, float u
             float sm = 0.0f;
 #pragma unroll
             for (int e = 0; e < EPC; ++e) {
-                m[e] = mass_at(rr, e, residual);
+                m[e] = mass_at(rr, e);
                 sm = sm + m[e];
             }
-            const uint64_t f = to_fixed<kFixedShift>(sm);
-            const uint64_t mylo = lo + wave_scan_add(f) - f;
-            if (f > 0 && mylo <= target && target < mylo + f) {
-                const uint64_t want = target - mylo;
+            const double f = fixed40(sm);
+            const double mylo = lo + (wave_scan_add(f) - f);
+            if (f > 0.0 && mylo <= target && target < mylo + f) {
+                const double want = target - mylo;
                 float racc = 0.0f;
                 int pick = -1, last_pos = -1;
 #pragma unroll
                 for (int e = 0; e < EPC; ++e) {
                     racc = racc + m[e];
                     if (m[e] > 0.0f) last_pos = e;
-                    if (pick < 0 && to_fixed<kFixedShift>(racc) > want) pick = e;
+                    if (pick < 0 && fixed40(racc) > want) pick = e;
                 }
                 if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
                 *s_tok = (rr * W + tid) * EPC + pick;
@@ -537,8 +542,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ uint8_t s_rej[kMaxItems];
     __shared__ int s_flag[2];
     __shared__ float s_y[2][2];
-    __shared__ unsigned long long s_cell[CPT * NW];
-    __shared__ unsigned long long s_z;
+    __shared__ double s_cell[CPT * NW];
+    __shared__ double s_z;
     __shared__ int s_tok;
     __shared__ double s_part[1];
     __shared__ FusedTail s_tail;
@@ -873,28 +878,39 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                             return fmaxf(p - exp2_fast(lq), 0.0f);
                         }
                     };
-                    auto mass = [&](int r, int e, bool residual) -> float {
-                        return formula(lc.load(r, e / 4)[e % 4], c1[r][e], residual);
+                    auto mass = [&](auto res_tag) {
+                        return [&](int r, int e) -> float {
+                            return formula(lc.load(r, e / 4)[e % 4], c1[r][e], decltype(res_tag)::value);
+                        };
                     };
                     // Round rr known at run time: the register half of the
                     // cache is picked with opaque bit masks, so that the
                     // compiler cannot turn the pick into an indexed access
                     // (which would move the whole cache to scratch memory).
-                    auto mass_at = [&](int rr, int e, bool residual) -> float {
-                        uint32_t bits = 0u;
+                    auto mass_at = [&](auto res_tag) {
+                        return [&](int rr, int e) -> float {
+                            uint32_t bits = 0u;
 #pragma unroll
-                        for (int r = 0; r < CPT; ++r) {
-                            uint32_t m = 0u - uint32_t(rr == r);
-                            asm volatile("" : "+v"(m));
-                            bits |= __float_as_uint(c1[r][e]) & m;
-                        }
-                        return formula(lc.load(rr, e / 4)[e % 4], __uint_as_float(bits), residual);
+                            for (int r = 0; r < CPT; ++r) {
+                                uint32_t m = 0u - uint32_t(rr == r);
+                                asm volatile("" : "+v"(m));
+                                bits |= __float_as_uint(c1[r][e]) & m;
+                            }
+                            return formula(lc.load(rr, e / 4)[e % 4], __uint_as_float(bits),
+                                           decltype(res_tag)::value);
+                        };
                     };
                     // No residual mass left after rounding (p = q to fp32
                     // accuracy): draw from p.
+                    using kResidual = std::integral_constant<bool, true>;
+                    using kTarget = std::integral_constant<bool, false>;
                     int tok = -1;
-                    for (int pass = cur.bonus ? 1 : 0; pass < 2 && tok < 0; ++pass)
-                        tok = draw_cached<W, CPT, EPC>(mass, mass_at, pass == 0, cur.u_res, s_cell, &s_z, &s_tok);
+                    if (!cur.bonus)
+                        tok = draw_cached<W, CPT, EPC, true>(mass(kResidual{}), mass_at(kResidual{}), cur.u_res,
+                                                             s_cell, &s_z, &s_tok);
+                    if (tok < 0)
+                        tok = draw_cached<W, CPT, EPC, false>(mass(kTarget{}), mass_at(kTarget{}), cur.u_res,
+                                                              s_cell, &s_z, &s_tok);
                     if (tok < 0 || tok >= a.V)
                         record = make_rec(kRecBadRow, 0);
                     else
