@@ -522,8 +522,10 @@ def main():
     fs = L.osd_sample
     prop_u = [t_(synth.uniforms(synth.rng(100 + r), B)) for r in range(R)]
     prop_out = torch.empty(B, dtype=torch.int32, device=dev)
+    prop_ws = torch.zeros(L.osd_sample_workspace_bytes(B), dtype=torch.uint8, device=dev)
     prop_args = [(None, 0, P(s["draft"]), K * V, binding.OSD_BF16, B, V, ctypes.c_float(T_VERIFY),
-                  ctypes.c_float(0.0), P(prop_u[r]), P(prop_out), hs) for r, s in enumerate(sets)]
+                  ctypes.c_float(0.0), P(prop_u[r]), P(prop_out), P(prop_ws), prop_ws.numel(), hs)
+                 for r, s in enumerate(sets)]
     gen = torch.Generator(device=dev)
     gen.manual_seed(16 + synth.SEED_LOGITS)
     zipf = torch.from_numpy(synth.zipf_bias(MIX_V, 0)).to(dev)
@@ -533,7 +535,7 @@ def main():
     mix_u = t_(synth.uniforms(synth.rng(101), MIX_N))
     mix_out = torch.empty(MIX_N, dtype=torch.int32, device=dev)
     mix_args = (P(mix_p), MIX_V, P(mix_q), MIX_V, binding.OSD_BF16, MIX_N, MIX_V, ctypes.c_float(MIX_T),
-                ctypes.c_float(MIX_BETA), P(mix_u), P(mix_out), hs)
+                ctypes.c_float(MIX_BETA), P(mix_u), P(mix_out), None, 0, hs)
     torch.cuda.synchronize()
 
     # Sharded verification: the whole rows are generated on the device, cut

@@ -315,17 +315,32 @@ int osd_verify_tree(const void* target_logits, const void* draft_logits, int dty
  * out_tokens    out [N] int32: the token, or -1 for a row with weight > 0
  *               that has no finite logit
  *
+ * workspace     NULL, or at least osd_sample_workspace_bytes(N) bytes,
+ *               16-byte aligned, zero before the first call; every call
+ *               leaves it zero.  Calls that may overlap (other streams) need
+ *               their own.  With a workspace, one-row sampling (T > 0, beta
+ *               0 or 1) of fewer rows than two per CU, rows 16-byte aligned
+ *               with 16-byte multiple strides and lengths, splits each row
+ *               over several workgroups that exchange two words each through
+ *               it; every other call (and every call without one) runs one
+ *               workgroup per row.  The token is the same rule's either way;
+ *               the two can differ only where u * sum(pi) lies within fp32
+ *               rounding of a boundary between tokens.
+ *
  * Errors: OSD_ERR_INVALID_ARG for N <= 0, V <= 0, a bad dtype, T < 0, inf
  * or NaN, beta outside [0, 1], T == 0 with 0 < beta < 1, a needed pointer
  * NULL or a row stride < V; OSD_ERR_UNSUPPORTED for V > osd_max_vocab(dtype);
+ * OSD_ERR_WORKSPACE for a workspace that is too small or misaligned;
  * OSD_ERR_DEVICE if the launch fails.  Nothing is enqueued on an error.
- * No workspace; one workgroup per row.  Rows that are 16-byte aligned with
- * 16-byte multiple strides and lengths take 16-byte loads.
+ * Rows that are 16-byte aligned with 16-byte multiple strides and lengths
+ * take 16-byte loads.
  */
+size_t osd_sample_workspace_bytes(int N);
 int osd_sample(const void* p_logits, int64_t p_row_stride,
                const void* q_logits, int64_t q_row_stride,
                int dtype, int N, int V, float temperature, float beta,
-               const float* u, int32_t* out_tokens, void* stream);
+               const float* u, int32_t* out_tokens, void* workspace, size_t workspace_bytes,
+               void* stream);
 
 /*
  * Vocabulary-sharded verification.  When the target and draft LM heads are

@@ -29,7 +29,8 @@ KINDS = {"fkl": OSD_FKL, "rkl": OSD_RKL, "jsd": OSD_JSD}
 
 EXPORTS = ("osd_max_vocab", "osd_status_string", "osd_verify_workspace_bytes", "osd_verify", "osd_verify_noalloc",
            "osd_distill_workspace_bytes", "osd_distill_loss_grad", "osd_verify_distill_workspace_bytes",
-           "osd_verify_distill", "osd_verify_distill_rejected", "osd_verify_tree_workspace_bytes", "osd_verify_tree", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
+           "osd_verify_distill", "osd_verify_distill_rejected", "osd_verify_tree_workspace_bytes", "osd_verify_tree",
+           "osd_sample_workspace_bytes", "osd_sample", "osd_shard_verify_stats", "osd_shard_verify_mass",
            "osd_shard_verify_draw")
 
 _lib = None
@@ -82,7 +83,9 @@ def lib():
             L.osd_verify_tree.restype = i32
             L.osd_verify_tree.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp, sz, vp]
             L.osd_sample.restype = i32
-            L.osd_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f32, vp, vp, vp]
+            L.osd_sample_workspace_bytes.restype = sz
+            L.osd_sample_workspace_bytes.argtypes = [i32]
+            L.osd_sample.argtypes = [vp, i64, vp, i64, i32, i32, i32, f32, f32, vp, vp, vp, sz, vp]
             L.osd_shard_verify_stats.restype = i32
             L.osd_shard_verify_stats.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, f32, vp, vp]
             L.osd_shard_verify_mass.restype = i32
@@ -378,9 +381,11 @@ def osd_sample(p_logits, q_logits, temperature, beta, u=None, out=None):
     if out is None:
         out = torch.empty(N, dtype=torch.int32, device=ref.device)
     stride = lambda t: 0 if t is None else (t.stride(0) if N > 1 else V)
-    st = lib().osd_sample(_ptr(p_logits), stride(p_logits), _ptr(q_logits), stride(q_logits),
-                          _dtype_code(ref), N, V, float(temperature), float(beta), _ptr(u), _ptr(out),
-                          _stream_handle(ref.device))
+    L = lib()
+    ws = workspace("sample", L.osd_sample_workspace_bytes(N), ref.device)
+    st = L.osd_sample(_ptr(p_logits), stride(p_logits), _ptr(q_logits), stride(q_logits),
+                      _dtype_code(ref), N, V, float(temperature), float(beta), _ptr(u), _ptr(out),
+                      _ptr(ws), ws.numel(), _stream_handle(ref.device))
     if st != OSD_OK:
         raise OsdError("osd_sample", st)
     return out

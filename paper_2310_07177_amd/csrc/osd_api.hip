@@ -357,9 +357,14 @@ int osd_verify_distill_rejected(const void* target_logits, const void* draft_log
                                beta, loss_out, row_loss_out, grad_out, workspace, workspace_bytes, stream);
 }
 
+size_t osd_sample_workspace_bytes(int N) {
+    if (N <= 0) return 0;
+    return size_t(N) * osd::kSampleWsPerRow;
+}
+
 int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits, int64_t q_row_stride,
                int dtype, int N, int V, float temperature, float beta, const float* u,
-               int32_t* out_tokens, void* stream) {
+               int32_t* out_tokens, void* workspace, size_t workspace_bytes, void* stream) {
     if (dtype != OSD_F32 && dtype != OSD_BF16) return OSD_ERR_INVALID_ARG;
     if (N <= 0 || V <= 0) return OSD_ERR_INVALID_ARG;
     if (V > osd_max_vocab(dtype)) return OSD_ERR_UNSUPPORTED;
@@ -371,6 +376,9 @@ int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits,
     if (!out_tokens || (!greedy && !u)) return OSD_ERR_INVALID_ARG;
     if (use_p && (!p_logits || p_row_stride < V)) return OSD_ERR_INVALID_ARG;
     if (use_q && (!q_logits || q_row_stride < V)) return OSD_ERR_INVALID_ARG;
+    if (workspace && (workspace_bytes < osd_sample_workspace_bytes(N) ||
+                      (reinterpret_cast<uintptr_t>(workspace) & 15u)))
+        return OSD_ERR_WORKSPACE;
     const int64_t eb = elem_bytes(dtype);
     osd::SampleLaunch L;
     L.p = use_p ? p_logits : nullptr;
@@ -384,6 +392,7 @@ int osd_sample(const void* p_logits, int64_t p_row_stride, const void* q_logits,
     L.beta = beta;
     L.u = u;
     L.out = out_tokens;
+    L.workspace = workspace;
     L.vec = (int64_t(V) * eb) % 16 == 0 && (!use_p || (aligned16(p_logits) && (p_row_stride * eb) % 16 == 0)) &&
             (!use_q || (aligned16(q_logits) && (q_row_stride * eb) % 16 == 0));
     L.stream = static_cast<hipStream_t>(stream);

@@ -182,9 +182,13 @@ struct SampleLaunch {
     int32_t* out;
     bool vec;  // every row 16-byte aligned and V a whole number of chunks
     int cus;
+    void* workspace;  // null, or sample_workspace_bytes(N) zeroed bytes: rows split over workgroups
     hipStream_t stream;
 };
 hipError_t launch_sample(const SampleLaunch& L);
+// Workspace of the split sampling: per row, 16 segment records of 16 bytes
+// and a 16-byte counter slot.
+constexpr size_t kSampleWsPerRow = 16 * 16 + 16;
 
 // Streaming (persistent-workgroup) distillation: rows whose byte length and
 // base are 16-byte multiples and whose V fits one of the streaming tiles.

@@ -12,10 +12,13 @@
 //   mixture:  beta 2^(t c2 - K_p)/S_p + (1 - beta) 2^(d c2 - K_q)/S_q, in
 //             probability units (each element is at most 1, every partial
 //             sum at most 1 + rounding, so 2^-60 fixed point cannot overflow).
+#include <stdlib.h>
+
 #include "osd.h"
 #include "osd_device.hpp"
 #include "osd_internal.hpp"
 #include "row_draw.hpp"
+#include "stream_device.hpp"
 
 namespace osd {
 namespace {
@@ -270,6 +273,322 @@ __global__ __launch_bounds__(kLongW, 1) void sample_mix_long_kernel(SampleArgs a
     if (tid == 0) a.out[n] = s_tok;
 }
 
+// One-row sampling of few rows (fewer than two per CU), each row split over S
+// segment workgroups of 256 threads (CPT chunks per thread, SEG = CPT*256
+// chunks per segment).  The inverse CDF needs no global normaliser: for any
+// common shift K, token j is the first whose running sum of 2^(x c2 - K)
+// exceeds u times the total.  Each segment therefore works alone:
+//   1. shift k_s = ceil(max over the segment * c2); masses 2^(x c2 - k_s);
+//      each thread's chunk sums become 2^-40 fixed point (whole numbers in
+//      fp64, exact below 2^53), summed into cells (round, wave) and the
+//      segment total T_s;
+//   2. it publishes (k_s, T_s) and reads its siblings' (bounded polls; a
+//      workgroup that runs out of polls computes the missing records itself
+//      from the rows in memory, bit for bit as their owners do);
+//   3. every segment combines the S records in segment order, identically:
+//      K = max k_s over segments with a finite logit, weights
+//      W_s = floor(T_s 2^(k_s - K)) (u64), Z = sum W_s, the point
+//      c = floor(u Z), and the segment s* whose weight interval holds c;
+//   4. s* maps c into its own units (an exact shift: the local offset stays
+//      below T_s*) and walks its cells, its lanes and its elements.
+// The cells partition [0, Z) exactly, so the token is always one with mass;
+// it can differ from the one-workgroup kernel's only where u*Z lies within
+// the fp32 rounding of a boundary.  Records are two never-zero words per
+// segment (the shift's bits with the top bit set; the total's bits
+// inverted); each workgroup arrives at its row's counter once it holds all
+// S records, and the last to arrive clears the row's words and counter.
+constexpr int kSegSampleW = 256;
+constexpr int kMaxSampleSegments = 16;
+constexpr int kSamplePolls = 256;
+
+struct SplitSampleArgs {
+    const char* row;   // row 0 of the sampled rows
+    int64_t stride;    // bytes between rows
+    int N, V, nchunks, S, polls;
+    float c2;
+    const float* u;
+    int32_t* out;
+    uint64_t* rec;     // [N, kMaxSampleSegments, 2], zero between calls
+    uint32_t* cnt;     // [N, 4] (word 0: arrivals), zero between calls
+};
+
+__device__ inline double fixed40(float x) { return floor(double(x) * 0x1p40); }
+
+// Statistics of one segment held in x (chunk r of this thread is segment
+// chunk r*W + tid): the shift, the cell totals (s_cell[r*NW + w], when
+// cells), the total and whether the segment has any finite logit.  All
+// threads call it; it ends with the totals visible to every thread.
+template <typename Fmt, int CPT>
+__device__ void segment_stats(const chunk_t (&x)[CPT], float c2, float* s_mx, double* s_cell, double* s_tot,
+                              float& k, double& T, bool& empty) {
+    constexpr int W = kSegSampleW, NW = W / kWave, EPC = Fmt::kPerChunk;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    float m = chunk_max<Fmt>(x[0]);
+#pragma unroll
+    for (int r = 1; r < CPT; ++r) m = fmaxf(m, chunk_max<Fmt>(x[r]));
+    m = wave_max_u(m);
+    if (lane == 0) s_mx[wid] = m;
+    __syncthreads();
+    m = s_mx[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) m = fmaxf(m, s_mx[w]);
+    empty = !(m > kNegInf);
+    k = shift_of_max(m, c2);
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        float sm = exp2_fast(__builtin_fmaf(Fmt::get(x[r], 0), c2, -k));
+#pragma unroll
+        for (int e = 1; e < EPC; ++e) sm = sm + exp2_fast(__builtin_fmaf(Fmt::get(x[r], e), c2, -k));
+        const double t = wave_scan_add(fixed40(sm));
+        if (lane == kWave - 1) s_cell[r * NW + wid] = t;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    if (wid == 0) {
+        const double t = wave_sum(lane < CPT * NW ? s_cell[lane] : 0.0);
+        if (lane == 0) *s_tot = t;
+    }
+    __syncthreads();
+    T = *s_tot;
+}
+
+template <typename Fmt, int CPT>
+__global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleArgs a) {
+    constexpr int W = kSegSampleW, NW = W / kWave, EPC = Fmt::kPerChunk, SEG = CPT * W, CELLS = CPT * NW;
+    static_assert(CELLS <= kWave, "one wave scans the cells");
+    __shared__ float s_mx[NW];
+    __shared__ double s_cell[CELLS];
+    __shared__ double s_tot;
+    __shared__ float s_k[kMaxSampleSegments];
+    __shared__ double s_T[kMaxSampleSegments];
+    __shared__ int s_ok;
+    __shared__ int s_tok;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int S = a.S, n = blockIdx.x / S, s = blockIdx.x - n * S;
+    const char* row = a.row + int64_t(n) * a.stride;
+    uint64_t* rec = a.rec + int64_t(n) * kMaxSampleSegments * 2;
+    const float c2 = a.c2;
+
+    // The row's uniform is read with the chunks (a load after the exchange
+    // would wait for the exchange's own memory operations).
+    const float un = a.u[n];
+    chunk_t x[CPT];
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) x[r] = stream_chunk<Fmt, true>(row, s * SEG + r * W + tid, a.nchunks, a.V);
+    float k;
+    double T;
+    bool empty;
+    segment_stats<Fmt, CPT>(x, c2, s_mx, s_cell, &s_tot, k, T, empty);
+    if (tid == 0) {
+        s_k[s] = empty ? kNegInf : k;
+        s_T[s] = T;
+        // Both words issued before either completion is waited for.
+        const uint64_t o0 = __hip_atomic_exchange(&rec[2 * s], (1ull << 63) | __float_as_uint(empty ? kNegInf : k),
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t o1 = __hip_atomic_exchange(&rec[2 * s + 1], ~uint64_t(__double_as_longlong(T)),
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("" ::"v"(o0), "v"(o1));
+    }
+    // The siblings' records: wave 0, lane j reads segment j's two words.
+    if (wid == 0) {
+        const bool mine = lane < S && lane != s;
+        bool ok = false;
+        uint64_t w0 = 0, w1 = 0;
+        for (int p = 0; p < a.polls; ++p) {
+            if (p > 0) __builtin_amdgcn_s_sleep(4);
+            bool ready = true;
+            if (mine) {
+                w0 = poll_u64(&rec[2 * lane]);
+                w1 = poll_u64(&rec[2 * lane + 1]);
+                ready = w0 != 0 && w1 != 0;
+            }
+            if (__ballot(!ready) == 0) {
+                ok = true;
+                break;
+            }
+        }
+        if (ok && mine) {
+            s_k[lane] = __uint_as_float(uint32_t(w0));
+            s_T[lane] = __longlong_as_double(~w1);
+        }
+        if (lane == 0) s_ok = ok;
+    }
+    __syncthreads();
+    if (!s_ok) {
+        // Out of polls: every other segment's record from the row itself.
+        __shared__ double s_cellx[CELLS];
+        for (int j = 0; j < S; ++j) {
+            if (j == s) continue;
+            chunk_t y[CPT];
+#pragma unroll
+            for (int r = 0; r < CPT; ++r) y[r] = stream_chunk<Fmt, true>(row, j * SEG + r * W + tid, a.nchunks, a.V);
+            float kj;
+            double Tj;
+            bool ej;
+            segment_stats<Fmt, CPT>(y, c2, s_mx, s_cellx, &s_tot, kj, Tj, ej);
+            if (tid == 0) {
+                s_k[j] = ej ? kNegInf : kj;
+                s_T[j] = Tj;
+            }
+        }
+        __syncthreads();
+    }
+    // Arrival at the row's counter, once this workgroup holds every record:
+    // issued here, its count awaited only at the end (s* walks meanwhile);
+    // the last to arrive leaves the row's words zero.  (This workgroup's
+    // records went out before its polls, whose waits covered them.)
+    uint32_t prev = 0;
+    if (tid == 0) prev = __hip_atomic_fetch_add(&a.cnt[int64_t(n) * 4], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    auto arrive_row = [&]() {
+        if (tid == 0 && prev == uint32_t(S - 1)) {
+            for (int j = 0; j < S; ++j) {
+                take_u64(&rec[2 * j]);
+                take_u64(&rec[2 * j + 1]);
+            }
+            take_u32(&a.cnt[int64_t(n) * 4]);
+        }
+    };
+    // The combine, identical in every segment and every wave (no barrier):
+    // lane j holds segment j's record; the shift K is their maximum, the
+    // weights are scanned in segment order, and s* is the lane whose weight
+    // interval holds c.
+    const bool have = lane < S;
+    const float kj = have ? s_k[lane] : kNegInf;
+    const double Tj = have ? s_T[lane] : 0.0;
+    const bool bad = __ballot(have && !(Tj >= 0.0 && Tj < 0x1p60)) != 0;
+    const float K = wave_max_u(kj);
+    uint64_t wj = 0;
+    if (have && kj > kNegInf && !bad) wj = uint64_t(floor(__builtin_ldexp(Tj, int(fmaxf(kj - K, -2048.0f)))));
+    const uint64_t incl = wave_scan_add(wj);
+    const uint64_t Z = readlane_u64(incl, kWave - 1);
+    if (bad || Z == 0) {
+        if (s == 0 && tid == 0) a.out[n] = -1;
+        arrive_row();
+        return;
+    }
+    uint64_t c = uint64_t(double(un) * double(Z));
+    if (c >= Z) c = Z - 1;
+    const uint64_t hit = __ballot(wj > 0 && incl - wj <= c && c < incl);
+    const int sstar = hit ? __builtin_ctzll(hit) : -1;
+    if (s != sstar) {
+        arrive_row();
+        return;
+    }
+    const uint64_t lo = readlane_u64(incl - wj, sstar);
+    // This segment holds the point: its offset in the segment's own units.
+    const double target = __builtin_ldexp(double(c - lo), int(K - k));
+    if (wid == 0) {
+        const double cv = lane < CELLS ? s_cell[lane] : 0.0;
+        const double ci = wave_scan_add(cv);
+        if (lane < CELLS) s_cell[lane] = ci - cv;  // exclusive prefix
+        if (lane == 0) s_tok = -1;
+    }
+    __syncthreads();
+    int rr = -1;
+    double clo = 0.0;
+    for (int r = 0; r < CPT; ++r) {
+        const int ci = r * NW + wid;
+        const double l = s_cell[ci];
+        const double h = ci + 1 < CELLS ? s_cell[ci + 1] : T;
+        if (l <= target && target < h) {
+            rr = r;
+            clo = l;
+        }
+    }
+    if (rr >= 0) {
+        // The chunk of round rr, picked with opaque bit masks (no indexed
+        // register access), and its masses exactly as in the first sweep.
+        uint32_t b[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int r = 0; r < CPT; ++r) {
+            uint32_t msk = 0u - uint32_t(rr == r);
+            asm volatile("" : "+v"(msk));
+            b[0] |= x[r].x & msk;
+            b[1] |= x[r].y & msk;
+            b[2] |= x[r].z & msk;
+            b[3] |= x[r].w & msk;
+        }
+        const chunk_t xc{b[0], b[1], b[2], b[3]};
+        float m[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) m[e] = exp2_fast(__builtin_fmaf(Fmt::get(xc, e), c2, -k));
+        float sm = m[0];
+#pragma unroll
+        for (int e = 1; e < EPC; ++e) sm = sm + m[e];
+        const double f = fixed40(sm);
+        const double mylo = clo + (wave_scan_add(f) - f);
+        if (f > 0.0 && mylo <= target && target < mylo + f) {
+            const double want = target - mylo;
+            float racc = m[0];
+            int pick = fixed40(racc) > want ? 0 : -1, last_pos = m[0] > 0.0f ? 0 : -1;
+#pragma unroll
+            for (int e = 1; e < EPC; ++e) {
+                racc = racc + m[e];
+                if (m[e] > 0.0f) last_pos = e;
+                if (pick < 0 && fixed40(racc) > want) pick = e;
+            }
+            if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+            s_tok = ((s * SEG + rr * W + tid) * EPC) + pick;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) a.out[n] = s_tok;
+    arrive_row();
+}
+
+// kSamplePolls, or the value of OSD_SAMPLE_POLLS (read once; 0 makes every
+// workgroup compute its siblings' records itself).
+int sample_polls() {
+    static const int v = [] {
+        const char* e = getenv("OSD_SAMPLE_POLLS");
+        if (e == nullptr || *e == 0) return kSamplePolls;
+        const int k = atoi(e);
+        return k < 0 ? kSamplePolls : (k > 65536 ? 65536 : k);
+    }();
+    return v;
+}
+
+template <typename Fmt, int CPT>
+hipError_t launch_split(const SampleLaunch& L, const SampleArgs& a, int nchunks, int S) {
+    SplitSampleArgs sa{};
+    sa.row = a.p;
+    sa.stride = a.p_stride;
+    sa.N = a.N;
+    sa.V = a.V;
+    sa.nchunks = nchunks;
+    sa.S = S;
+    sa.polls = sample_polls();
+    sa.c2 = a.c2;
+    sa.u = a.u;
+    sa.out = a.out;
+    char* w = static_cast<char*>(L.workspace);
+    sa.rec = reinterpret_cast<uint64_t*>(w);
+    sa.cnt = reinterpret_cast<uint32_t*>(w + size_t(L.N) * kMaxSampleSegments * 16);
+    return launch_kernel(&sample_split_kernel<Fmt, CPT>, dim3(unsigned(L.N) * unsigned(S)), dim3(kSegSampleW), 0,
+                         L.stream, sa);
+}
+
+// The split applies to one-row sampling (T > 0, beta 0 or 1) of 16-byte rows
+// when one workgroup per row would leave most CUs idle.
+template <typename Fmt>
+bool try_split(const SampleLaunch& L, const SampleArgs& a, hipError_t* e) {
+    if (!L.workspace || !L.vec || !(L.temperature > 0.0f) || (L.beta > 0.0f && L.beta < 1.0f)) return false;
+    if (L.N >= 2 * L.cus) return false;
+    const int nchunks = (L.V + Fmt::kPerChunk - 1) / Fmt::kPerChunk;
+    const int s2 = (nchunks + 2 * kSegSampleW - 1) / (2 * kSegSampleW);
+    const int s4 = (nchunks + 4 * kSegSampleW - 1) / (4 * kSegSampleW);
+    if (s2 >= 2 && s2 <= kMaxSampleSegments && int64_t(L.N) * s2 <= 4 * int64_t(L.cus)) {
+        *e = launch_split<Fmt, 2>(L, a, nchunks, s2);
+        return true;
+    }
+    if (s4 >= 2 && s4 <= kMaxSampleSegments && int64_t(L.N) * s4 <= 4 * int64_t(L.cus)) {
+        *e = launch_split<Fmt, 4>(L, a, nchunks, s4);
+        return true;
+    }
+    return false;
+}
+
 template <typename Fmt, int W, int CPT>
 hipError_t launch_tile(const SampleLaunch& L, const SampleArgs& a) {
     if (L.temperature == 0.0f) return launch_mode<Fmt, W, CPT, kModeGreedy>(L, a);
@@ -279,6 +598,8 @@ hipError_t launch_tile(const SampleLaunch& L, const SampleArgs& a) {
 
 template <typename Fmt>
 hipError_t launch_fmt(const SampleLaunch& L, const SampleArgs& a) {
+    hipError_t se;
+    if (try_split<Fmt>(L, a, &se)) return se;
     RowTile t;
     if (!pick_tile(L.V, Fmt::kPerChunk, &t)) {
         // Longer rows: a mixture streams its row pair; one row (or an

@@ -50,6 +50,7 @@ def test_workspace_sizes():
 
 
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+FAKE_MISALIGNED = ctypes.c_void_p(0x1004)
 
 
 def verify(**kw):
@@ -140,10 +141,10 @@ def test_fused_workspace_covers_both_entry_points():
 
 def sample(**kw):
     a = dict(p=FAKE, ps=64, q=FAKE, qs=64, dtype=1, N=4, V=64, T=0.8, beta=0.5, u=FAKE, out=FAKE,
-             stream=None)
+             ws=None, wsb=0, stream=None)
     a.update(kw)
     return osd.lib().osd_sample(a["p"], a["ps"], a["q"], a["qs"], a["dtype"], a["N"], a["V"], a["T"],
-                                a["beta"], a["u"], a["out"], a["stream"])
+                                a["beta"], a["u"], a["out"], a["ws"], a["wsb"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -154,9 +155,16 @@ def sample(**kw):
     (dict(p=None), -1), (dict(q=None), -1), (dict(u=None), -1), (dict(out=None), -1),
     (dict(ps=63), -1), (dict(qs=10), -1),
     (dict(beta=1.0, p=None), -1), (dict(beta=0.0, q=None), -1),
+    (dict(ws=FAKE, wsb=4 * 272 - 1), -4), (dict(ws=FAKE_MISALIGNED, wsb=4 * 272), -4),
 ])
 def test_sample_rejects_bad_arguments(kw, status):
     assert sample(**kw) == status
+
+
+def test_sample_workspace_size():
+    L = osd.lib()
+    assert L.osd_sample_workspace_bytes(4) == 4 * 272
+    assert L.osd_sample_workspace_bytes(0) == 0
 
 
 def test_binding_sample_fails_loudly_without_gpu_tensors():
@@ -166,7 +174,6 @@ def test_binding_sample_fails_loudly_without_gpu_tensors():
 
 
 # Vocabulary-sharded verification (three phases, one call per rank each).
-FAKE_MISALIGNED = ctypes.c_void_p(0x1004)
 
 
 def shard_stats(**kw):

@@ -122,8 +122,9 @@ def test_sample_and_tree_outputs_stay_in_bounds(L, V, dtype):
     p, q, u = to_device(x["p"]), to_device(x["q"]), to_device(x["u"])
     for beta, T in ((0.5, 1.0), (0.0, 0.8), (1.0, 0.0)):
         out = Guarded(4 * 9, 4)
+        ws = zeros_ws(L.osd_sample_workspace_bytes(9))
         assert L.osd_sample(ptr(p), V, ptr(q), V, dt, 9, V, ctypes.c_float(T), ctypes.c_float(beta), ptr(u),
-                            out.ptr, stream()) == 0
+                            out.ptr, ptr(ws), ws.numel(), stream()) == 0
         torch.cuda.synchronize()
         out.check(f"sample V={V} beta={beta} T={T}")
     if V > 32768:

@@ -161,3 +161,120 @@ def test_sample_deterministic(osd):
     a = run(osd, x["p"], x["q"], 1.0, 0.5, x["u"])
     b = run(osd, x["p"], x["q"], 1.0, 0.5, x["u"])
     assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# One-row sampling of few rows with a workspace: each row split over several
+# workgroups that exchange (shift, total) records through the workspace.
+
+def raw_sample(osd, p, q, T, beta, u, ws):
+    """osd_sample through ctypes with the workspace tensor ws (or none):
+    p/q/u are device tensors, rows contiguous."""
+    import ctypes
+    import torch
+    from paper_2310_07177_amd import binding
+    L = osd.lib()
+    ref_t = p if p is not None else q
+    N, V = ref_t.shape
+    out = torch.empty(N, dtype=torch.int32, device=ref_t.device)
+    P = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())
+    st = L.osd_sample(P(p), V if p is not None else 0, P(q), V if q is not None else 0,
+                      binding._dtype_code(ref_t), N, V, ctypes.c_float(T), ctypes.c_float(beta), P(u), P(out),
+                      P(ws), 0 if ws is None else ws.numel(), binding._stream_handle(ref_t.device))
+    assert st == 0
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def split_case(osd, N, V, dtype, T, seed, q=None):
+    import torch
+    x = synth.sample_inputs(N, V, dtype, seed=seed, p_std=2.5)
+    q = x["q"] if q is None else q
+    qd, ud = to_device(q), to_device(x["u"])
+    ws = torch.zeros(osd.lib().osd_sample_workspace_bytes(N), dtype=torch.uint8, device=qd.device)
+    split = raw_sample(osd, None, qd, T, 0.0, ud, ws)
+    split2 = raw_sample(osd, None, qd, T, 0.0, ud, ws)
+    one = raw_sample(osd, None, qd, T, 0.0, ud, None)
+    assert int(ws.count_nonzero()) == 0, "the workspace is left zero"
+    assert np.array_equal(split, split2)
+    r = ref.sample(None, q, T, 0.0, x["u"])
+    close = np.nan_to_num(r["margin"], nan=np.inf) < MARGIN
+    for got, name in ((split, "split"), (one, "one workgroup")):
+        bad = np.nonzero((got != r["tokens"]) & ~close)[0]
+        assert bad.size == 0, (f"{name} N={N} V={V} {dtype}: {bad.size} rows differ from the oracle, first "
+                               f"n={bad[0]}: {got[bad[0]]} vs {r['tokens'][bad[0]]}")
+    assert close.sum() <= max(2, N // 10)
+    return split, r
+
+
+@pytest.mark.parametrize("N,V,dtype,T", [(64, 32128, "bf16", 0.7),   # 8 segments of 512 chunks
+                                         (8, 4104, "bf16", 1.0),     # 2 segments, the second one chunk
+                                         (16, 131072, "bf16", 0.8),  # 16 segments of 1024 chunks
+                                         (4, 65536, "f32", 1.0),     # 16 segments, fp32
+                                         (1, 32000, "bf16", 0.5)])   # one row
+def test_sample_split_rows_match_oracle_and_one_workgroup(osd, N, V, dtype, T):
+    split_case(osd, N, V, dtype, T, seed=V % 97 + N)
+
+
+def test_sample_split_segments_without_finite_logits(osd):
+    """Whole segments of -inf (their records carry no shift), a row with one
+    finite logit, and a row with none (-1)."""
+    N, V = 8, 32000
+    x = synth.sample_inputs(N, V, "bf16", seed=31, p_std=2.5)
+    q = x["q"].copy()
+    neg = 0xFF80
+    q[0, :16384] = neg           # segments 0..3 empty
+    q[1, :] = neg
+    q[1, 20000] = x["q"][1, 20000]  # one finite logit
+    q[2, :] = neg                # no finite logit: -1
+    q[3, :28672] = neg           # only the last segment has mass
+    q[4, ::2] = neg              # every other token masked
+    got, r = split_case(osd, N, V, "bf16", 0.9, seed=31, q=q)
+    assert got[1] == 20000 and got[2] == -1
+    assert got[0] >= 16384 and got[3] >= 28672 and got[4] % 2 == 1
+
+
+SAMPLE_FALLBACK = r'''
+import sys
+import numpy as np
+import torch
+sys.path.insert(0, ".")
+import paper_2310_07177_amd as osd
+from paper_2310_07177_amd import synth
+from tests._helpers import to_device
+from tests.test_sample_gpu import raw_sample
+out = {}
+for N, V, dtype in ((64, 32128, "bf16"), (4, 65536, "f32")):
+    x = synth.sample_inputs(N, V, dtype, seed=5, p_std=2.5)
+    qd, ud = to_device(x["q"]), to_device(x["u"])
+    ws = torch.zeros(osd.lib().osd_sample_workspace_bytes(N), dtype=torch.uint8, device=qd.device)
+    out[f"{N}_{V}"] = raw_sample(osd, None, qd, 0.8, 0.0, ud, ws)
+    assert int(ws.count_nonzero()) == 0
+np.savez(sys.argv[1], **out)
+print("FALLBACK_OK", flush=True)
+'''
+
+
+def test_sample_split_fallback_is_bit_identical(osd, tmp_path):
+    """With the bound on a segment's waits set to 0 (OSD_SAMPLE_POLLS, read
+    once per process, so in a child process), every segment computes its
+    siblings' records itself from memory; the tokens must be the exchanging
+    path's, bit for bit."""
+    import os
+    import subprocess
+    import sys
+    import torch
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    path = str(tmp_path / "sample_fallback.npz")
+    env = dict(os.environ, OSD_SAMPLE_POLLS="0")
+    r = subprocess.run([sys.executable, "-u", "-c", SAMPLE_FALLBACK, path], cwd=root, env=env,
+                       capture_output=True, text=True, timeout=150)
+    print(r.stdout[-3000:], r.stderr[-3000:], flush=True)
+    assert r.returncode == 0 and "FALLBACK_OK" in r.stdout
+    got = np.load(path)
+    for N, V, dtype in ((64, 32128, "bf16"), (4, 65536, "f32")):
+        x = synth.sample_inputs(N, V, dtype, seed=5, p_std=2.5)
+        qd, ud = to_device(x["q"]), to_device(x["u"])
+        ws = torch.zeros(osd.lib().osd_sample_workspace_bytes(N), dtype=torch.uint8, device=qd.device)
+        want = raw_sample(osd, None, qd, 0.8, 0.0, ud, ws)
+        assert np.array_equal(got[f"{N}_{V}"], want), f"N={N} V={V} {dtype}"
