@@ -51,6 +51,62 @@ __device__ inline float rescue_sum(double& S, VFn v) {
     return o;
 }
 
+// A row pair's merged softmax statistics and the row-uniform values derived
+// from them (fp64), computed once per row pair by wave 0 and read from LDS by
+// every thread: K, S of each row, T_t - T_s (T = K + log2 S, the log2
+// normalisers), 1/S and log2 S.
+struct RowPair {
+    float kt, ks;
+    double st, ss, dtd, ist, iss, lt, ls;
+};
+
+// Every wave merges its lanes' (K, S) pairs and posts them; after one
+// barrier wave 0 merges the waves' pairs and derives the row values; after a
+// second, every thread reads them.  The values are those of block_merge2
+// followed by the same formulas, bit for bit.
+template <int NW>
+__device__ inline RowPair merge_row_pair(float Kt, double St, float Ks, double Ss, float* s_k, double* s_s,
+                                         RowPair* s_r) {
+    static_assert(NW <= 16, "the posted pairs fit one DPP row");
+    const int t = opaque_tid(), lane = t & (kWave - 1), wid = t / kWave;
+    wave_merge_stats_u(Kt, St);
+    wave_merge_stats_u(Ks, Ss);
+    if (lane == 0) {
+        s_k[wid] = Kt;
+        s_k[NW + wid] = Ks;
+        s_s[wid] = St;
+        s_s[NW + wid] = Ss;
+    }
+    __syncthreads();
+    if (wid == 0) {
+        float k0 = kNegInf, k1 = kNegInf;
+        double t0 = 0.0, t1 = 0.0;
+        if (lane < NW) {
+            k0 = s_k[lane];
+            k1 = s_k[NW + lane];
+            t0 = s_s[lane];
+            t1 = s_s[NW + lane];
+        }
+        row0_merge_stats_u(k0, t0);
+        row0_merge_stats_u(k1, t1);
+        if (lane == 0) {
+            RowPair r;
+            r.kt = k0;
+            r.ks = k1;
+            r.st = t0;
+            r.ss = t1;
+            r.dtd = double(k0 - k1) + (t0 == t1 ? 0.0 : log2_pos(t0 / t1));
+            r.ist = 1.0 / t0;
+            r.iss = 1.0 / t1;
+            r.lt = log2_pos(t0);
+            r.ls = log2_pos(t1);
+            *s_r = r;
+        }
+    }
+    __syncthreads();
+    return *s_r;
+}
+
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // The LDS half of the cache: element e of chunk r of this thread, in float4

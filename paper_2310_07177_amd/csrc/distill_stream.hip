@@ -86,6 +86,7 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
     constexpr bool XV = KIND == 2;
     __shared__ float s_k[2 * NW];
     __shared__ double s_s[2 * NW];
+    __shared__ RowPair s_rp;
     __shared__ double s_a[2 * NW];
     __shared__ uint8_t s_on[W];
     __shared__ double s_part[1];  // sum of this workgroup's row divergences
@@ -238,22 +239,21 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             if (!XV && S_s >= 1.0e300) {
                 ks_s = kc_s + rescue_sum<CPT, EPC>(S_s, [&](int r, int e) -> float { return c1[r][e]; });
             }
-            float Kt = ks_t, Ks = ks_s;
-            double St = S_t, Ss = S_s;
-            block_merge2<NW>(Kt, St, Ks, Ss, s_k, s_s);
+            const RowPair rp = merge_row_pair<NW>(ks_t, S_t, ks_s, S_s, s_k, s_s, &s_rp);
+            const float Kt = rp.kt, Ks = rp.ks;
             // log2 p_j = (t_j c2 - K_t) - (K_row_t - K_t + log2 S_t) = c - ct, likewise q.
             // T = K + log2 S, the rows' log2 normalisers; only their
             // difference is needed in fp64 (from the ratio of the sums).
-            const double dTd = double(Kt - Ks) + (St == Ss ? 0.0 : log2_pos(St / Ss));
-            const float ct = float(double(Kt - kc_t) + log2_pos(St)), cs = float(double(Ks - kc_s) + log2_pos(Ss));
+            const double dTd = rp.dtd;
+            const float ct = float(double(Kt - kc_t) + rp.lt), cs = float(double(Ks - kc_s) + rp.ls);
             // FKL/RKL: log2(p/q) = (v_t - v_s) - dTk, from the same rounded
             // exponents as the sums (so the normalisers and the log-ratios
             // agree: rows with p ~ q keep their small divergence accurate).
             const float dTk = float(dTd - double(kc_t - kc_s));
             // JSD: p = e_t at and q = e_s as, the cached values times the
             // thread's scale 2^(k - K) / S (fp64, rounded once).
-            const float at = float(__builtin_ldexp(1.0 / St, int(fmaxf(kc_t - Kt, -2048.0f))));
-            const float as = float(__builtin_ldexp(1.0 / Ss, int(fmaxf(kc_s - Ks, -2048.0f))));
+            const float at = float(__builtin_ldexp(rp.ist, int(fmaxf(kc_t - Kt, -2048.0f))));
+            const float as = float(__builtin_ldexp(rp.iss, int(fmaxf(kc_s - Ks, -2048.0f))));
 
             // ---- loss pass (from the cache) ----
             float acc0 = 0.0f, acc1 = 0.0f;

@@ -13,10 +13,62 @@
 
 namespace osd {
 
+// x 2^SH as a whole number held in fp64: for masses of at most 1 per element
+// (chunk sums at most 8) and SH <= 44, every chunk value is below 2^47 and
+// every wave sum at most 2^53, so each is exact -- and equal to
+// mass_to_fixed<SH>(x), which takes more instructions.
+template <int SH>
+__device__ inline double fixed_f64(float x) {
+    static_assert(SH <= 44, "exact below 2^53 only for SH <= 44");
+    return floor(double(x) * double(1ull << SH));
+}
+
 struct DrawShared {
     int cell_round, cell_wave;
     unsigned long long target;  // offset of u*Z inside the winning cell
 };
+
+// The winning wave's last step (both draws): this lane's chunk of round
+// nstar has masses m[] (sum s, added left to right from 0); target is the
+// point's offset inside the wave's cell.  The lanes' fixed-point chunk sums
+// are scanned to find the lane holding the target, which walks its elements
+// with the same left-to-right fp32 sums.  Returns the token on that lane and
+// -1 on the others.
+template <int SH, int W, int EPC>
+__device__ inline int walk_chunk(const float (&m)[EPC], float s, uint64_t target, int nstar) {
+    const int tid = threadIdx.x;
+    int pick = -1, last_pos = -1;
+    if constexpr (SH <= 44) {
+        // Offsets inside one cell stay below 2^53: exact in fp64.
+        const double v = fixed_f64<SH>(s);
+        const double incl = wave_scan_add(v);
+        const double lo = incl - v, t = double(target);
+        if (!(v > 0.0 && lo <= t && t < incl)) return -1;
+        const double want = t - lo;
+        float run = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+            run = run + m[e];
+            if (m[e] > 0.0f) last_pos = e;
+            if (pick < 0 && fixed_f64<SH>(run) > want) pick = e;
+        }
+    } else {
+        const uint64_t v = mass_to_fixed<SH>(s);
+        const uint64_t incl = wave_inclusive_scan(v);
+        const uint64_t lo = incl - v;
+        if (!(v > 0 && lo <= target && target < incl)) return -1;
+        const uint64_t want = target - lo;
+        float run = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+            run = run + m[e];
+            if (m[e] > 0.0f) last_pos = e;
+            if (pick < 0 && mass_to_fixed<SH>(run) > want) pick = e;
+        }
+    }
+    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+    return (nstar * W + tid) * EPC + pick;
+}
 
 // Inverse-CDF draw over a register-resident row pair.  mass(t, d, e) returns
 // the non-negative fp32 mass of element e of the chunks t, d (0 for padding).
@@ -45,7 +97,11 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
         float s = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) s = s + mass(tv[n], dv[n], e);
-        const uint64_t t = wave_sum(mass_to_fixed<SH>(s));
+        uint64_t t;
+        if constexpr (SH <= 44)
+            t = uint64_t(wave_sum(fixed_f64<SH>(s)));
+        else
+            t = wave_sum(mass_to_fixed<SH>(s));
         if (lane == 0) s_tot[n * NW + wid] = t;
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -97,23 +153,7 @@ __device__ int draw_inverse_cdf(const chunk_t (&tv)[CPT], const chunk_t (&dv)[CP
         m[e] = mass(tc, dc, e);
         s = s + m[e];
     }
-    const uint64_t v = mass_to_fixed<SH>(s);
-    const uint64_t incl = wave_inclusive_scan(v);
-    const uint64_t lo = incl - v;
-    const uint64_t target = s_draw->target;
-    if (!(v > 0 && lo <= target && target < incl)) return -1;
-    // Walk the chunk with the same left-to-right fp32 sum.
-    const uint64_t want = target - lo;
-    float run = 0.0f;
-    int pick = -1, last_pos = -1;
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-        run = run + m[e];
-        if (m[e] > 0.0f) last_pos = e;
-        if (pick < 0 && mass_to_fixed<SH>(run) > want) pick = e;
-    }
-    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
-    return (nstar * W + tid) * EPC + pick;
+    return walk_chunk<SH, W, EPC>(m, s, s_draw->target, nstar);
 }
 
 }  // namespace osd
@@ -148,7 +188,11 @@ __device__ int draw_inverse_cdf_streamed(int R, MassFn masses, float u, unsigned
         float s = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) s = s + m[e];
-        const uint64_t t = wave_sum(mass_to_fixed<SH>(s));
+        uint64_t t;
+        if constexpr (SH <= 44)
+            t = uint64_t(wave_sum(fixed_f64<SH>(s)));
+        else
+            t = wave_sum(mass_to_fixed<SH>(s));
         if (lane == 0) s_tot[r * NW + wid] = t;
     }
     __syncthreads();
@@ -184,22 +228,7 @@ __device__ int draw_inverse_cdf_streamed(int R, MassFn masses, float u, unsigned
     float s = 0.0f;
 #pragma unroll
     for (int e = 0; e < EPC; ++e) s = s + m[e];
-    const uint64_t v = mass_to_fixed<SH>(s);
-    const uint64_t incl = wave_inclusive_scan(v);
-    const uint64_t lo = incl - v;
-    const uint64_t target = s_draw->target;
-    if (!(v > 0 && lo <= target && target < incl)) return -1;
-    const uint64_t want = target - lo;
-    float run = 0.0f;
-    int pick = -1, last_pos = -1;
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-        run = run + m[e];
-        if (m[e] > 0.0f) last_pos = e;
-        if (pick < 0 && mass_to_fixed<SH>(run) > want) pick = e;
-    }
-    if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
-    return (nstar * W + tid) * EPC + pick;
+    return walk_chunk<SH, W, EPC>(m, s, s_draw->target, nstar);
 }
 
 }  // namespace osd
