@@ -152,17 +152,8 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
             // shift k is taken over all its chunks: every cached value is at
             // most 1 and no sum leaves the fp32 range.
             if (live) {
-                float mt = kNegInf, ms = kNegInf;
-#pragma unroll
-                for (int r = 0; r < CPT; ++r) {
-                    chunk_t xt = rt[r], xs = rs[r];
-                    if (r == CPT - 1 && !last_ok) {
-                        xt = pad_chunk<Fmt>();
-                        xs = pad_chunk<Fmt>();
-                    }
-                    mt = fmaxf(mt, chunk_max<Fmt>(xt));
-                    ms = fmaxf(ms, chunk_max<Fmt>(xs));
-                }
+                const float mt = chunks_max<Fmt, CPT>(rt, !last_ok);
+                const float ms = chunks_max<Fmt, CPT>(rs, !last_ok);
                 kc_t = shift_of_max(mt, c2);
                 kc_s = shift_of_max(ms, c2);
             }

@@ -95,6 +95,50 @@ __device__ inline float first_chunk_shift(const chunk_t& c, float c2) {
     return shift_of_max(chunk_max<Fmt>(c), c2);
 }
 
+// The largest element of a thread's CPT chunks of one row (pad_last: the
+// last chunk is padding), element by element.
+template <typename Fmt, int CPT>
+__device__ inline float chunks_max_exact(const chunk_t (&x)[CPT], bool pad_last) {
+    float m = kNegInf;
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        const chunk_t c = (r == CPT - 1 && pad_last) ? pad_chunk<Fmt>() : x[r];
+        m = fmaxf(m, chunk_max<Fmt>(c));
+    }
+    return m;
+}
+
+// The same maximum.  For bf16 the chunks' 16-bit patterns are first compared
+// as f16 numbers, two per packed instruction with three operands: both
+// formats are sign-magnitude with the exponent above the mantissa, so the
+// two orders agree wherever the f16 reading is finite, that is for bf16
+// magnitudes below 2^121, and the winning pattern is the bf16 maximum.  The
+// f16 maximum propagates NaN, so a thread holding a pattern outside that
+// range (an infinity, a NaN, a magnitude of 2^121 or more) or only padding
+// (f16 -inf) gets an unusable result and is decided element by element.
+// Either way the value is the exact maximum.
+template <typename Fmt, int CPT>
+__device__ inline float chunks_max(const chunk_t (&x)[CPT], bool pad_last) {
+    if constexpr (Fmt::kPerChunk == 8) {
+        typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+        constexpr uint32_t kNegInfPair = 0xFC00FC00u;  // f16 -inf in both halves
+        const auto H = [](uint32_t w) { return __builtin_bit_cast(h2_t, w); };
+        const auto mx = [](h2_t u, h2_t v) { return __builtin_elementwise_maximum(u, v); };
+        h2_t m = H(kNegInfPair);
+#pragma unroll
+        for (int r = 0; r < CPT - 1; ++r)
+            m = mx(mx(mx(m, H(x[r].x)), mx(H(x[r].y), H(x[r].z))), H(x[r].w));
+        // The last chunk joins unless it is padding (one select).
+        const chunk_t& l = x[CPT - 1];
+        const h2_t ml = mx(mx(mx(m, H(l.x)), mx(H(l.y), H(l.z))), H(l.w));
+        m = pad_last ? m : ml;
+        const uint32_t b = __builtin_bit_cast(uint32_t, m);
+        const float lo = __uint_as_float(b << 16), hi = __uint_as_float(b & 0xFFFF0000u);
+        if (__builtin_fabsf(lo) < 0x1p121f && __builtin_fabsf(hi) < 0x1p121f) return fmaxf(lo, hi);
+    }
+    return chunks_max_exact<Fmt, CPT>(x, pad_last);
+}
+
 // The thread index through an opaque copy: lane and wave numbers derived from
 // it are recomputed where they are used instead of being kept alive (or
 // spilled) across a long loop.

@@ -156,21 +156,11 @@ __device__ inline Meta finish_meta(const FusedArgs& a, const MetaLoads& r) {
     return m;
 }
 
-__device__ inline Meta meta_at(const Meta* s_meta, int k) {
-    const Meta v = s_meta[k];
-    Meta m;
-    m.kb = __builtin_amdgcn_readfirstlane(v.kb);
-    m.y = __builtin_amdgcn_readfirstlane(v.y);
-    m.u = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v.u)));
-    m.u_res = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v.u_res)));
-    m.on = __builtin_amdgcn_readfirstlane(v.on);
-    return m;
-}
-
 enum : int { kItemNone = 0, kItemBadToken = 1, kItemLive = 2 };
 
 struct Item {
-    int b, i;
+    int row;      // b*(K+1) + i: the target row, and the item's decision and record slot
+    int i;        // position (k_b for a bonus row)
     bool bonus;
     int vkind;    // verification: none, bad token or live
     bool dist;    // distillation row with mask 1 (error-index mode: decided after the test)
@@ -197,21 +187,21 @@ __device__ inline Item decode_item(const FusedArgs& a, int it, const Meta& m) {
     const int BK = a.B * a.K;
     t.bonus = it >= BK;
     const int i = t.bonus ? 0 : it / a.B;
-    t.b = t.bonus ? it - BK : it - i * a.B;
+    const int b = t.bonus ? it - BK : it - i * a.B;
     t.i = t.bonus ? m.kb : i;
+    t.row = b * (a.K + 1) + t.i;
     if (it < 0 || it >= a.nitems) return t;
     const bool kb_ok = m.kb >= 1 && m.kb <= a.K;
     if (!t.bonus) {
-        t.grow = t.b * a.K + i;
+        t.grow = b * a.K + i;
         t.dist = !a.erridx && m.on != 0;
         if (kb_ok && i < m.kb) t.vkind = (m.y < 0 || m.y >= a.V) ? kItemBadToken : kItemLive;
     } else if (kb_ok) {
         t.vkind = kItemLive;
     }
     if (t.vkind == kItemLive || t.dist) {
-        t.trow = static_cast<const char*>(a.target) + (int64_t(t.b) * (a.K + 1) + t.i) * int64_t(a.V) * Fmt::kBytes;
-        if (!t.bonus)
-            t.drow = static_cast<const char*>(a.draft) + (int64_t(t.b) * a.K + t.i) * int64_t(a.V) * Fmt::kBytes;
+        t.trow = static_cast<const char*>(a.target) + int64_t(t.row) * int64_t(a.V) * Fmt::kBytes;
+        if (!t.bonus) t.drow = static_cast<const char*>(a.draft) + int64_t(t.grow) * int64_t(a.V) * Fmt::kBytes;
     }
     return t;
 }
@@ -250,20 +240,76 @@ __device__ inline Schedule make_schedule(const FusedArgs& a, int g, int G) {
 
 // s_rej[k] = 1 if item k of this workgroup or an earlier item of the same
 // sequence ended the test (or could not be tested).  Read after a barrier of
-// item k (every item has one), the entries up to k - 1 are visible.
-__device__ inline bool known_rejection(const uint8_t* s_rej, const Schedule& sc, int k) {
-    const int kk = sc.prev_same(k);
-    return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
-}
-// The same, asked at the start of item k - 1 (to decide whether item k's
-// rows are read).  Items end without a workgroup barrier, so only entries up
-// to k - 3 are certainly visible to every wave then (entry j is written by
-// thread 0 at the end of item j, before it reaches a barrier of item j + 1).
-__device__ inline bool known_rejection_ahead(const uint8_t* s_rej, const Schedule& sc, int k) {
+// item k (every item has one), the entries up to k - 1 are visible.  Items
+// end without a workgroup barrier, so when item k - 1 starts only the entries
+// up to k - 3 are certainly visible to every wave (entry j is written by
+// thread 0 at the end of item j, before it reaches a barrier of item j + 1):
+// the link consulted there, to decide whether item k's rows are read, is the
+// latest earlier item of the sequence at or below k - 3.
+
+// An item as the prologue stages it in LDS (thread k decodes item k of its
+// workgroup, once), so that the item loop takes each item's fields from two
+// uniform LDS reads instead of recomputing them from the schedule and the
+// arguments in scalar code.  links holds the entries of the workgroup's
+// outcome flags consulted for the item: its latest earlier item of the same
+// sequence (bits 0-15) and the one consulted a step ahead (bits 16-31), each
+// -1 if none.
+struct ItemRec {
+    int row, i, y;
+    float u, u_res;
+    int grow;
+    uint32_t flags;  // bit 0 bonus, bits 1-2 vkind, bit 3 dist, bit 4 seq_ok, bit 5 target row read, bit 6 draft row read
+    int links;
+};
+static_assert(sizeof(ItemRec) == 32, "two 16-byte LDS reads per item");
+
+__device__ inline int link_of(int kk) { return kk >= 0 && kk < kMaxItems ? kk : -1; }
+
+template <typename Fmt>
+__device__ inline ItemRec encode_item(const FusedArgs& a, const Schedule& sc, int k, const Meta& m) {
+    const Item t = decode_item<Fmt>(a, sc.item(k), m);
+    ItemRec r;
+    r.row = t.row;
+    r.i = t.i;
+    r.y = t.y;
+    r.u = t.u;
+    r.u_res = t.u_res;
+    r.grow = t.grow;
+    r.flags = (t.bonus ? 1u : 0u) | (uint32_t(t.vkind) << 1) | (t.dist ? 8u : 0u) | (t.seq_ok ? 16u : 0u) |
+              (t.trow != nullptr ? 32u : 0u) | (t.drow != nullptr ? 64u : 0u);
     int kk = sc.prev_same(k);
+    const int prev = link_of(kk);
     while (kk > k - 3) kk = sc.prev_same(kk);
-    return kk >= 0 && kk < kMaxItems && s_rej[kk] != 0;
+    r.links = (prev & 0xFFFF) | (link_of(kk) << 16);
+    return r;
 }
+
+// Item k from the staged records (uniform); prev and ahead receive its links.
+template <typename Fmt>
+__device__ inline Item item_at(const FusedArgs& a, const ItemRec* s_items, int k, int* prev, int* ahead) {
+    const ItemRec v = s_items[k];
+    const auto rfl = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
+    Item t;
+    t.row = rfl(v.row);
+    t.i = rfl(v.i);
+    t.y = rfl(v.y);
+    t.u = __int_as_float(rfl(__float_as_int(v.u)));
+    t.u_res = __int_as_float(rfl(__float_as_int(v.u_res)));
+    t.grow = rfl(v.grow);
+    const uint32_t f = uint32_t(rfl(int(v.flags)));
+    const int l = rfl(v.links);
+    t.bonus = (f & 1u) != 0;
+    t.vkind = int((f >> 1) & 3u);
+    t.dist = (f & 8u) != 0;
+    t.seq_ok = (f & 16u) != 0;
+    t.trow = (f & 32u) ? static_cast<const char*>(a.target) + int64_t(t.row) * a.row_bytes : nullptr;
+    t.drow = (f & 64u) ? static_cast<const char*>(a.draft) + int64_t(t.grow) * a.row_bytes : nullptr;
+    *prev = int(int16_t(l & 0xFFFF));
+    *ahead = l >> 16;
+    return t;
+}
+
+__device__ inline bool rejected_at(const uint8_t* s_rej, int link) { return link >= 0 && s_rej[link] != 0; }
 
 // Wave 0: the decisions of positions 0..i-1 of one sequence (lane j:
 // position j).  2 if one of them stopped the test, 1 if all accepted, 0 if
@@ -539,7 +585,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ double s_s[2][2 * NW];
     __shared__ RowPair s_rp[2];
     __shared__ double s_a[2 * NW];
-    __shared__ Meta s_meta[kMaxItems];
+    __shared__ ItemRec s_items[kMaxItems];
     __shared__ uint8_t s_rej[kMaxItems];
     __shared__ int s_flag[2];
     __shared__ float s_y[2][2];
@@ -615,14 +661,14 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             rs[r] = load_chunk<W>(fsr, r);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (t < nk) s_meta[t] = finish_meta(a, ml);
+        if (t < nk) s_items[t] = encode_item<Fmt>(a, sc, t, finish_meta(a, ml));
         __syncthreads();
     }
     Item cur;
     cur.vkind = kItemNone;
     cur.dist = false;
     cur.bonus = false;
-    cur.b = 0;
+    cur.row = 0;
     cur.i = 0;
     cur.y = 0;
     cur.u = 0.0f;
@@ -632,30 +678,26 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     cur.grow = -1;
     int cur_skip = 0;
     for (int k = 0; k < nk; ++k) {
-        const int it = sc.item(k);
         Item nxt;
-        bool nload;
+        nxt.bonus = false;
+        nxt.trow = nullptr;
+        nxt.drow = nullptr;
         int nxt_skip = 0;
-        {
-            Meta mn;
-            mn.kb = 0;
-            mn.y = 0;
-            mn.u = 0.0f;
-            mn.u_res = 0.0f;
-            mn.on = 0;
-            if (k + 1 < nk) mn = meta_at(s_meta, k + 1);
-            nxt = decode_item<Fmt>(a, k + 1 < nk ? sc.item(k + 1) : a.nitems, mn);
-            nload = nxt.trow != nullptr;
+        if (k + 1 < nk) {
+            int nprev, nahead;
+            nxt = item_at<Fmt>(a, s_items, k + 1, &nprev, &nahead);
             // A bonus row whose sequence already stopped here is not read
             // (the current item's outcome is not known yet).
-            if (nload && nxt.bonus && known_rejection_ahead(s_rej, sc, k + 1)) {
-                nload = false;
+            if (nxt.trow != nullptr && nxt.bonus && rejected_at(s_rej, nahead)) {
+                nxt.trow = nullptr;
                 nxt_skip = 1;
             }
         }
+        const bool nload = nxt.trow != nullptr;
         const rsrc_t ntr = make_rsrc(nload ? nxt.trow : a.target, nload ? a.row_bytes : 0u);
         const rsrc_t nsr = make_rsrc(nload && nxt.drow ? nxt.drow : a.target, nload && nxt.drow ? a.row_bytes : 0u);
-        cur = decode_item<Fmt>(a, it, meta_at(s_meta, k));
+        int cprev, cahead;
+        cur = item_at<Fmt>(a, s_items, k, &cprev, &cahead);
         // A bonus row is needed only if every proposal of its sequence is
         // accepted.  Besides this workgroup's own outcomes, the decisions
         // that any workgroup has posted so far are consulted (each is
@@ -667,12 +709,12 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             const int t = opaque_tid();  // nothing tid-derived is kept across the loop
             if (t < kWave) {
                 uint32_t d = 0u;
-                if (t < cur.i) d = load_relaxed(&a.dec[int64_t(cur.b) * (a.K + 1) + t]);
+                if (t < cur.i) d = load_relaxed(&a.dec[int64_t(cur.row - cur.i) + t]);
                 const uint64_t m = __ballot(d == kDecStop);
                 if (t == 0) s_flag[k & 1] = m != 0 ? 1 : 0;
             }
             __syncthreads();
-            bonus_stop = s_flag[k & 1] != 0 || known_rejection(s_rej, sc, k);
+            bonus_stop = s_flag[k & 1] != 0 || rejected_at(s_rej, cprev);
         }
         const bool vlive = cur.vkind == kItemLive && !cur_skip && !bonus_stop;
         const bool live = vlive || cur.dist;
@@ -692,17 +734,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             // shift k is taken over all its chunks: every cached value is at
             // most 1 and no sum leaves the fp32 range.
             if (live) {
-                float mt = kNegInf, ms = kNegInf;
-#pragma unroll
-                for (int r = 0; r < CPT; ++r) {
-                    chunk_t xt = rt[r], xs = rs[r];
-                    if (r == CPT - 1 && !last_ok) {
-                        xt = pad_chunk<Fmt>();
-                        xs = pad_chunk<Fmt>();
-                    }
-                    mt = fmaxf(mt, chunk_max<Fmt>(xt));
-                    ms = fmaxf(ms, chunk_max<Fmt>(xs));
-                }
+                const float mt = chunks_max<Fmt, CPT>(rt, !last_ok);
+                const float ms = chunks_max<Fmt, CPT>(rs, !last_ok);
                 kc_t = shift_of_max(mt, c2);
                 kc_s = shift_of_max(ms, c2);
             }
@@ -770,7 +803,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
         bool stopped = false;  // this item ended the test (or could not be tested)
         bool distilled = false;
         bool release_rows = false;  // error-index mode: this item's outputs may be cleared by the last workgroup
-        uint32_t* const dec_at = a.dec + int64_t(cur.b) * (a.K + 1) + cur.i;
+        uint32_t* const dec_at = a.dec + cur.row;
         if (cur.vkind == kItemBadToken) {
             record = make_rec(kRecBadToken, 0);
             stopped = true;
@@ -816,7 +849,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             bool spec = false;  // drew without knowing the earlier positions' outcomes
             if (vlive) {
                 const bool bad = !(St > 0.0 && St < 1.0e300) || (!cur.bonus && !(Ss > 0.0 && Ss < 1.0e300));
-                const bool earlier = known_rejection(s_rej, sc, k);
+                const bool earlier = rejected_at(s_rej, cprev);
                 bool want_draw = false;
                 if (bad) {
                     record = make_rec(kRecBadRow, 0);
@@ -851,7 +884,7 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
                         // in the error-index mode, is distilled): wave 0
                         // looks at the earlier positions' decisions.
                         if (opaque_tid() < kWave) {
-                            const int st = poll_decisions(a.dec + int64_t(cur.b) * (a.K + 1), cur.i, a.max_polls);
+                            const int st = poll_decisions(a.dec + (cur.row - cur.i), cur.i, a.max_polls);
                             if (opaque_tid() == 0) s_flag[k & 1] = st;
                         }
                         __syncthreads();
@@ -1040,9 +1073,8 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             // its record says so: the last workgroup may overwrite them.
             if (release_rows) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
             if (cur.vkind != kItemNone)  // posted at the coherence point; waited for once, at the end
-                __hip_atomic_exchange(&a.records[int64_t(cur.b) * (a.K + 1) + cur.i], record, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-            if (k < kMaxItems) s_rej[k] = (stopped || known_rejection(s_rej, sc, k)) ? 1 : 0;
+                __hip_atomic_exchange(&a.records[cur.row], record, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (k < kMaxItems) s_rej[k] = (stopped || rejected_at(s_rej, cprev)) ? 1 : 0;
         }
         cur_skip = nxt_skip;
     }
