@@ -75,23 +75,30 @@ constexpr int kMaxItems = 256;
 constexpr int kMaxPolls = 32;
 
 struct FusedArgs {
-    const void* target;  // [B, K+1, V]
-    const void* draft;   // [B, K, V]
-    int B, K, V;
+    // What the prologue needs comes first: the kernel requests these words
+    // at once on entry (one round trip to the argument buffer).
+    const void* target;        // [B, K+1, V]
+    const void* draft;         // [B, K, V]
     const int32_t* tokens;     // [B, K]
     const int32_t* draft_len;  // [B] or null
     const float* u_accept;     // [B, K]
     const float* u_resample;   // [B]
     const uint8_t* mask;       // [B, K] distillation mask or null (all rows)
-    float c2;                  // log2(e) / T
-    double c2d;
-    double betad, ombd;        // beta and 1 - beta in fp64 (scalar operands of the JSD combination)
-    float inv_tau;             // 1 / T
-    float beta;
-    uint32_t* records;         // [B, K+1], zero between calls
-    uint32_t* dec;             // [B, K+1] decisions, zero between calls
+    int B, K, V;
+    int G;                     // workgroups in the grid
+    int nitems;                // B*K + B
+    int nchunks;
+    uint32_t row_bytes;
+    int seq_step;              // items k and k - seq_step of a workgroup share a sequence
     int erridx;                // distil the first rejected row of each sequence (not `mask`)
     int max_polls;             // looks at the earlier decisions before drawing speculatively
+    float c2;                  // log2(e) / T
+    float inv_tau;             // 1 / T
+    float beta;
+    double c2d;
+    double betad, ombd;        // beta and 1 - beta in fp64 (scalar operands of the JSD combination)
+    uint32_t* records;         // [B, K+1], zero between calls
+    uint32_t* dec;             // [B, K+1] decisions, zero between calls
     int32_t* accepted_len;
     int32_t* out_tokens;
     uint8_t* reject_mask;
@@ -100,10 +107,6 @@ struct FusedArgs {
     double* part_ws;           // [G] loss partials ([B*K] row losses in the error-index mode), zero between calls
     uint32_t* done;            // workgroups finished, zero between calls
     float* loss_out;
-    int nitems;                // B*K + B
-    int nchunks;
-    uint32_t row_bytes;
-    int seq_step;              // items k and k - seq_step of a workgroup share a sequence
 };
 
 // Per-item arguments, loaded once per workgroup (thread j: its j-th item)
@@ -410,7 +413,7 @@ __device__ int draw_cached(MassFn mass, MassAtFn mass_at, float u, double* s_cel
     return tok;
 }
 
-// What the last workgroup needs, staged in LDS at kernel start so that none
+// What the last workgroup needs, staged in LDS by the prologue so that none
 // of it stays in registers across the item loop.
 struct FusedTail {
     double* part_ws;
@@ -430,6 +433,7 @@ struct FusedTail {
     uint32_t row_bytes;
     int erridx;
     int B, K;
+    int G;
 };
 
 // Rows whose gradient the last workgroup clears (error-index mode): rows
@@ -467,7 +471,7 @@ __device__ inline void finish_fused(const FusedTail& a, const double* s_part) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int lane = tid & (kWave - 1), wid = tid / kWave;
-    const int G = gridDim.x;
+    const int G = a.G;
     __syncthreads();
     if (tid == 0) {
         if (!a.erridx)
@@ -598,8 +602,16 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ double s_ln2;
     const LdsCache<W, EPC> lc{s_c0};
 
+    // Every argument word the prologue reads, requested together (each
+    // dependent request would cost a round trip to the argument buffer).
+    asm volatile("" ::"s"(a.target), "s"(a.draft), "s"(a.tokens), "s"(a.draft_len), "s"(a.u_accept),
+                 "s"(a.u_resample), "s"(a.mask));
+    asm volatile("" ::"s"(a.B), "s"(a.K), "s"(a.V), "s"(a.G), "s"(a.nitems), "s"(a.nchunks), "s"(a.row_bytes),
+                 "s"(a.seq_step), "s"(a.erridx), "s"(a.max_polls), "s"(a.c2), "s"(a.inv_tau), "s"(a.beta));
+    asm volatile("" ::"s"(a.c2d), "s"(a.betad), "s"(a.ombd), "s"(a.records), "s"(a.dec), "s"(a.row_loss_out),
+                 "s"(a.grad_out), "s"(a.part_ws));
     const int tid = threadIdx.x;
-    const int G = gridDim.x;
+    const int G = a.G;
     const float c2 = a.c2;
     const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
     const float beta = a.beta, omb = 1.0f - a.beta;
@@ -613,24 +625,6 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     if (tid == 0) {
         s_ln2 = kLn2;     // ordered before any read by the prologue's barrier
         s_part[0] = 0.0;  // read and written by thread 0 only
-        s_tail.part_ws = a.part_ws;
-        s_tail.done = a.done;
-        s_tail.loss_out = a.loss_out;
-        s_tail.mask = a.mask;
-        s_tail.nrows = a.B * a.K;
-        s_tail.records = a.records;
-        s_tail.dec = a.dec;
-        s_tail.row_loss_out = a.row_loss_out;
-        s_tail.grad_out = a.grad_out;
-        s_tail.row_bytes = a.row_bytes;
-        s_tail.erridx = a.erridx;
-        s_tail.draft_len = a.draft_len;
-        s_tail.tokens = a.tokens;
-        s_tail.accepted_len = a.accepted_len;
-        s_tail.out_tokens = a.out_tokens;
-        s_tail.reject_mask = a.reject_mask;
-        s_tail.B = a.B;
-        s_tail.K = a.K;
     }
     // Prologue: the item arguments are requested first (a few words per
     // item), then the first item's rows, so that waiting for the arguments
@@ -660,6 +654,36 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             rt[r] = load_chunk<W>(ftr, r);
             rs[r] = load_chunk<W>(fsr, r);
             __builtin_amdgcn_sched_barrier(0);
+        }
+        // What the last workgroup needs, staged while the item arguments and
+        // the first rows are in flight: read through an opaque copy of the
+        // argument buffer's address, so that these reads (and the wait for
+        // them) cannot move ahead of the row loads.
+        __builtin_amdgcn_sched_barrier(0);
+        if (tid == 0) {
+            typedef const __attribute__((address_space(4))) FusedArgs* ArgPtr;
+            ArgPtr ap = (ArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
+            asm volatile("" : "+s"(ap));
+            const __attribute__((address_space(4))) FusedArgs& a = *ap;
+            s_tail.part_ws = a.part_ws;
+            s_tail.done = a.done;
+            s_tail.loss_out = a.loss_out;
+            s_tail.mask = a.mask;
+            s_tail.nrows = a.B * a.K;
+            s_tail.records = a.records;
+            s_tail.dec = a.dec;
+            s_tail.row_loss_out = a.row_loss_out;
+            s_tail.grad_out = a.grad_out;
+            s_tail.row_bytes = a.row_bytes;
+            s_tail.erridx = a.erridx;
+            s_tail.draft_len = a.draft_len;
+            s_tail.tokens = a.tokens;
+            s_tail.accepted_len = a.accepted_len;
+            s_tail.out_tokens = a.out_tokens;
+            s_tail.reject_mask = a.reject_mask;
+            s_tail.B = a.B;
+            s_tail.K = a.K;
+            s_tail.G = a.G;
         }
         if (t < nk) s_items[t] = encode_item<Fmt>(a, sc, t, finish_meta(a, ml));
         __syncthreads();
@@ -1107,6 +1131,7 @@ hipError_t launch_kind(const FusedLaunch& L, FusedArgs a) {
         r = t;
     }
     a.seq_step = a.B / g;
+    a.G = int(grid);
     const hipError_t e = launch_kernel(&verify_distill_kernel<Fmt, W, CPT, KIND>, dim3(grid), dim3(W), 0, L.stream, a);
     return e;
 }
