@@ -89,17 +89,26 @@ __device__ inline RowPair merge_row_pair(float Kt, double St, float Ks, double S
         }
         row0_merge_stats_u(k0, t0);
         row0_merge_stats_u(k1, t1);
+        // The three quotients and the three logarithms are taken side by side
+        // in lanes 0-2 (one division and one log2_pos in sequence instead of
+        // three and three): lane 0 t0/t1, lane 1 1/t0, lane 2 1/t1, then the
+        // log2 of t0/t1, t0 and t1.  Each value is the one the scalar formula
+        // gives.
+        const double qv = (lane == 0 ? t0 : 1.0) / (lane == 1 ? t0 : t1);
+        const double lv = log2_pos(lane == 0 ? qv : (lane == 1 ? t0 : t1));
+        const double l_q = readlane_f64(lv, 0), l_t = readlane_f64(lv, 1), l_s = readlane_f64(lv, 2);
+        const double i_t = readlane_f64(qv, 1), i_s = readlane_f64(qv, 2);
         if (lane == 0) {
             RowPair r;
             r.kt = k0;
             r.ks = k1;
             r.st = t0;
             r.ss = t1;
-            r.dtd = double(k0 - k1) + (t0 == t1 ? 0.0 : log2_pos(t0 / t1));
-            r.ist = 1.0 / t0;
-            r.iss = 1.0 / t1;
-            r.lt = log2_pos(t0);
-            r.ls = log2_pos(t1);
+            r.dtd = double(k0 - k1) + (t0 == t1 ? 0.0 : l_q);
+            r.ist = i_t;
+            r.iss = i_s;
+            r.lt = l_t;
+            r.ls = l_s;
             *s_r = r;
         }
     }
