@@ -413,7 +413,7 @@ __device__ int draw_cached(MassFn mass, MassAtFn mass_at, float u, double* s_cel
     return tok;
 }
 
-// What the last workgroup needs, staged in LDS by the prologue so that none
+// What the last workgroup needs, staged in LDS at kernel start so that none
 // of it stays in registers across the item loop.
 struct FusedTail {
     double* part_ws;
@@ -602,14 +602,16 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     __shared__ double s_ln2;
     const LdsCache<W, EPC> lc{s_c0};
 
-    // Every argument word the prologue reads, requested together (each
-    // dependent request would cost a round trip to the argument buffer).
+    // Every argument word the kernel reads, requested together: each
+    // dependent request would cost a round trip to the argument buffer
+    // (about a microsecond), and no argument is read again later.
     asm volatile("" ::"s"(a.target), "s"(a.draft), "s"(a.tokens), "s"(a.draft_len), "s"(a.u_accept),
                  "s"(a.u_resample), "s"(a.mask));
     asm volatile("" ::"s"(a.B), "s"(a.K), "s"(a.V), "s"(a.G), "s"(a.nitems), "s"(a.nchunks), "s"(a.row_bytes),
                  "s"(a.seq_step), "s"(a.erridx), "s"(a.max_polls), "s"(a.c2), "s"(a.inv_tau), "s"(a.beta));
     asm volatile("" ::"s"(a.c2d), "s"(a.betad), "s"(a.ombd), "s"(a.records), "s"(a.dec), "s"(a.row_loss_out),
                  "s"(a.grad_out), "s"(a.part_ws));
+    asm volatile("" ::"s"(a.accepted_len), "s"(a.out_tokens), "s"(a.reject_mask), "s"(a.done), "s"(a.loss_out));
     const int tid = threadIdx.x;
     const int G = a.G;
     const float c2 = a.c2;
@@ -625,6 +627,26 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
     if (tid == 0) {
         s_ln2 = kLn2;     // ordered before any read by the prologue's barrier
         s_part[0] = 0.0;  // read and written by thread 0 only
+        // What the last workgroup needs (from the arguments already read).
+        s_tail.part_ws = a.part_ws;
+        s_tail.done = a.done;
+        s_tail.loss_out = a.loss_out;
+        s_tail.mask = a.mask;
+        s_tail.nrows = a.B * a.K;
+        s_tail.records = a.records;
+        s_tail.dec = a.dec;
+        s_tail.row_loss_out = a.row_loss_out;
+        s_tail.grad_out = a.grad_out;
+        s_tail.row_bytes = a.row_bytes;
+        s_tail.erridx = a.erridx;
+        s_tail.draft_len = a.draft_len;
+        s_tail.tokens = a.tokens;
+        s_tail.accepted_len = a.accepted_len;
+        s_tail.out_tokens = a.out_tokens;
+        s_tail.reject_mask = a.reject_mask;
+        s_tail.B = a.B;
+        s_tail.K = a.K;
+        s_tail.G = a.G;
     }
     // Prologue: the item arguments are requested first (a few words per
     // item), then the first item's rows, so that waiting for the arguments
@@ -654,36 +676,6 @@ __global__ __launch_bounds__(W, 1) void verify_distill_kernel(FusedArgs a) {
             rt[r] = load_chunk<W>(ftr, r);
             rs[r] = load_chunk<W>(fsr, r);
             __builtin_amdgcn_sched_barrier(0);
-        }
-        // What the last workgroup needs, staged while the item arguments and
-        // the first rows are in flight: read through an opaque copy of the
-        // argument buffer's address, so that these reads (and the wait for
-        // them) cannot move ahead of the row loads.
-        __builtin_amdgcn_sched_barrier(0);
-        if (tid == 0) {
-            typedef const __attribute__((address_space(4))) FusedArgs* ArgPtr;
-            ArgPtr ap = (ArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
-            asm volatile("" : "+s"(ap));
-            const __attribute__((address_space(4))) FusedArgs& a = *ap;
-            s_tail.part_ws = a.part_ws;
-            s_tail.done = a.done;
-            s_tail.loss_out = a.loss_out;
-            s_tail.mask = a.mask;
-            s_tail.nrows = a.B * a.K;
-            s_tail.records = a.records;
-            s_tail.dec = a.dec;
-            s_tail.row_loss_out = a.row_loss_out;
-            s_tail.grad_out = a.grad_out;
-            s_tail.row_bytes = a.row_bytes;
-            s_tail.erridx = a.erridx;
-            s_tail.draft_len = a.draft_len;
-            s_tail.tokens = a.tokens;
-            s_tail.accepted_len = a.accepted_len;
-            s_tail.out_tokens = a.out_tokens;
-            s_tail.reject_mask = a.reject_mask;
-            s_tail.B = a.B;
-            s_tail.K = a.K;
-            s_tail.G = a.G;
         }
         if (t < nk) s_items[t] = encode_item<Fmt>(a, sc, t, finish_meta(a, ml));
         __syncthreads();
