@@ -140,6 +140,7 @@ struct LossTail {
     float* loss_out;
     const uint8_t* mask;
     int nrows;
+    int G;  // workgroups in the grid
 };
 
 template <int W>
@@ -151,7 +152,7 @@ __device__ inline void finish_loss(const LossTail& a, const double* s_part) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int lane = tid & (kWave - 1), wid = tid / kWave;
-    const int G = gridDim.x;
+    const int G = a.G;
     __syncthreads();
     if (tid == 0) {
         __hip_atomic_exchange(&a.row_ws[blockIdx.x], s_part[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -56,6 +56,7 @@ struct StreamDistillArgs {
     int nrows;
     int nchunks;
     uint32_t row_bytes;
+    int G;  // workgroups in the grid
 };
 
 struct Row {
@@ -94,8 +95,14 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
     __shared__ f32x4_t s_c0[CPT * NG * W];
     const LdsCache<W, EPC> lc{s_c0};
 
+    // Every argument word, requested together: each dependent request would
+    // cost a round trip to the argument buffer (about a microsecond).
+    asm volatile("" ::"s"(a.teacher), "s"(a.tstride), "s"(a.student), "s"(a.sstride), "s"(a.B), "s"(a.K), "s"(a.V),
+                 "s"(a.mask), "s"(a.beta), "s"(a.c2), "s"(a.inv_tau));
+    asm volatile("" ::"s"(a.row_loss_out), "s"(a.grad_out), "s"(a.row_ws), "s"(a.done), "s"(a.loss_out), "s"(a.nrows),
+                 "s"(a.nchunks), "s"(a.row_bytes), "s"(a.G));
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-    const int G = gridDim.x;
+    const int G = a.G;
     const float c2 = a.c2;
     const bool last_ok = (CPT - 1) * W + tid < a.nchunks;
     const float beta = a.beta, omb = 1.0f - a.beta;
@@ -116,6 +123,7 @@ __global__ __launch_bounds__(W, 1) void distill_stream_kernel(StreamDistillArgs 
         s_tail.loss_out = a.loss_out;
         s_tail.mask = a.mask;
         s_tail.nrows = a.nrows;
+        s_tail.G = a.G;
     }
     uint32_t mine = 1u;
     if (a.mask && tid < nk) mine = a.mask[int(blockIdx.x) + tid * G];
@@ -365,7 +373,9 @@ hipError_t launch_kind(const DistillLaunch& L, const StreamDistillArgs& a) {
     const int64_t min_grid = (int64_t(a.nrows) + W - 1) / W;
     if (want < min_grid) want = min_grid;
     const unsigned grid = unsigned(want < a.nrows ? want : a.nrows);
-    const hipError_t e = launch_kernel(&distill_stream_kernel<Fmt, W, CPT, KIND>, dim3(grid), dim3(W), 0, L.stream, a);
+    StreamDistillArgs ag = a;
+    ag.G = int(grid);
+    const hipError_t e = launch_kernel(&distill_stream_kernel<Fmt, W, CPT, KIND>, dim3(grid), dim3(W), 0, L.stream, ag);
     return e;
 }
 

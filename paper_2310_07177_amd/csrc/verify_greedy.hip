@@ -63,12 +63,21 @@ __device__ inline void pad_segment(chunk_t (&x)[CPT], const SegArgs& a, int s) {
 
 __device__ inline int seq_k(const SegArgs& a, int b) { return a.draft_len ? scalar_load(a.draft_len + b) : a.K; }
 
+// Every argument word, requested together on entry: each dependent request
+// would cost a round trip to the argument buffer (about a microsecond).
+__device__ inline void request_args(const SegArgs& a) {
+    asm volatile("" ::"s"(a.target), "s"(a.B), "s"(a.K), "s"(a.V), "s"(a.tokens), "s"(a.draft_len), "s"(a.nseg),
+                 "s"(a.nchunks), "s"(a.row_bytes), "s"(a.first), "s"(a.stats));
+    asm volatile("" ::"s"(a.accepted_len), "s"(a.out_tokens), "s"(a.reject_mask));
+}
+
 template <typename Fmt, int CPT>
 __global__ __launch_bounds__(kW) void verify_greedy_stats(SegArgs a) {
     constexpr int EPC = Fmt::kPerChunk;
     __shared__ float s_k[kNW];
     __shared__ int s_i[kNW];
 
+    request_args(a);
     const int tid = threadIdx.x;
     const int64_t unit = a.first + blockIdx.x;
     const int s = int(unit % a.nseg);
@@ -156,6 +165,7 @@ __device__ inline void clear_stats(const SegArgs& a, int b, int kb) {
 template <typename Fmt>
 __global__ __launch_bounds__(kW) void verify_greedy_decide(SegArgs a) {
     __shared__ SegStats s_st[(OSD_MAX_K + 1) * kMaxSeg];
+    request_args(a);
     const int tid = threadIdx.x;
     const int b = int(a.first + blockIdx.x);
     const int K = a.K;
