@@ -458,3 +458,19 @@ def test_rejected_speculative_rows_are_cleared(osd):
                        timeout=150)
     print(r.stdout[-3000:], r.stderr[-3000:], flush=True)
     assert r.returncode == 0 and "SPECULATIVE_OK" in r.stdout
+
+
+@pytest.mark.parametrize("V", [4096, 32128])
+def test_fused_extreme_finite_logits(osd, V):
+    """The fused step on bf16 rows with logits at the edges of the f16 range
+    and beyond, and rows of denormals (both branches of the thread maxima),
+    against the oracle."""
+    from tests.test_parity_gpu import extreme_rows
+    B, K = 4, 3
+    x = synth.verify_inputs(B, K, V, "bf16", T=0.9, seed=43)
+    t, s = extreme_rows(B, K, V, 47)
+    x["target"], x["draft"] = synth.to_bf16(t), synth.to_bf16(s)
+    # One-hot and tied rows put many decisions exactly on their boundaries
+    # (such sequences are excluded from the token comparison by the margin
+    # rule); losses and gradients are compared on every row.
+    check_fused(osd, x, "jsd", 0.5, np.ones((B, K), np.uint8), f"extreme fused V={V}", max_excluded_frac=1.0)

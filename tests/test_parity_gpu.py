@@ -552,3 +552,51 @@ def test_distill_long_rows_fallback_is_bit_identical(osd, tmp_path):
         for name, v in (("loss", loss), ("rows", rows), ("grad", g)):
             w = got[f"{kind}{V}{dtype}{name}"]
             assert np.array_equal(v.view(np.uint8), w.view(np.uint8)), f"{kind} V={V} {dtype} {name}"
+
+
+def extreme_rows(B, K, V, seed):
+    """Teacher [B, K+1, V] and student [B, K, V] float32 rows (to be rounded
+    to bf16) whose per-thread maxima hit both branches of the kernels' bf16
+    maximum: blocks of very negative logits whose 16-bit patterns read as
+    finite f16 numbers (magnitudes below 2^121, compared as f16) or not
+    (2^121 and more, decided element by element), bf16 denormals and signed
+    zeros, and rows whose maximum is a large logit within the supported
+    range (|logit| c2 below 2^23, where the integer shifts are exact)."""
+    g = np.random.default_rng(seed)
+    t = g.normal(0, 2, (B, K + 1, V)).astype(np.float32)
+    s = (t[:, :K] + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    rows = [(b, i) for b in range(B) for i in range(K)]
+    for n, (b, i) in enumerate(rows):
+        kind = n % 6
+        j = g.choice(V, size=64, replace=False)
+        if kind == 0:    # f16-finite patterns, both sides (probability 0)
+            t[b, i, j] = -1.5 * 2.0 ** 119
+            s[b, i, j] = -1.5 * 2.0 ** 119
+        elif kind == 1:  # patterns beyond the f16 range, teacher only
+            t[b, i, j] = -(2.0 ** 125)
+        elif kind == 2:  # beyond the f16 range on the student side, next to a large maximum
+            s[b, i, j[1:]] = -(2.0 ** 123)
+            t[b, i, j[0]] = 4096.0
+        elif kind == 3:  # tiny values only: denormals and signed zeros
+            t[b, i] = g.choice(np.array([1e-39, -1e-39, 0.0, -0.0, 3e-39], np.float32), V)
+            s[b, i] = g.choice(np.array([1e-39, -1e-39, 0.0, -0.0, 2e-39], np.float32), V)
+        elif kind == 4:  # a large shared maximum (one-hot rows on both sides)
+            t[b, i, j[:8]] = 60000.0
+            s[b, i, j[:8]] = 60000.0
+        # kind 5: ordinary rows
+    return t, s
+
+
+@pytest.mark.parametrize("V", [4096, 32128])
+def test_distill_jsd_extreme_finite_logits(osd, V):
+    """bf16 rows with logits at the edges of the f16 range and beyond, and
+    rows of denormals: the thread maxima of JSD's statistics (packed f16
+    comparisons with an element-by-element fallback) give the oracle's
+    losses and gradients.  (JSD stays bounded on such rows; the KL
+    divergences of a row whose probabilities underflow on one side are
+    beyond the log-ratio clamp and are not compared here.)"""
+    B, K = 2, 6
+    t, s = extreme_rows(B, K, V, 41)
+    mask = np.ones((B, K), np.uint8)
+    tt, ss = synth.to_bf16(t[:, :K].copy()), synth.to_bf16(s)
+    check_distill(osd, tt, ss, "jsd", 0.5, 0.9, mask, f"extreme jsd V={V}")
