@@ -315,38 +315,50 @@ struct SplitSampleArgs {
 __device__ inline double fixed40(float x) { return floor(double(x) * 0x1p40); }
 
 // Statistics of one segment held in x (chunk r of this thread is segment
-// chunk r*W + tid): the shift, the cell totals (s_cell[r*NW + w], when
-// cells), the total and whether the segment has any finite logit.  All
-// threads call it; it ends with the totals visible to every thread.
+// chunk r*W + tid): the shift, the cell totals (s_cell[r*NW + w]) and their
+// exclusive prefix in segment order (s_excl), the total and whether the
+// segment has any finite logit.  Each thread also keeps what a walk to a
+// point inside its chunks needs: the chunk masses m, their fixed-point sums
+// f and the sum of the lower lanes' sums in the same cell (off).  All
+// threads call it; it ends with the cell values visible to every thread.
 template <typename Fmt, int CPT>
-__device__ void segment_stats(const chunk_t (&x)[CPT], float c2, float* s_mx, double* s_cell, double* s_tot,
-                              float& k, double& T, bool& empty) {
-    constexpr int W = kSegSampleW, NW = W / kWave, EPC = Fmt::kPerChunk;
+__device__ void segment_stats(const chunk_t (&x)[CPT], float c2, float* s_mx, double* s_cell, double* s_excl,
+                              double* s_tot, float& k, double& T, bool& empty, float (&m)[CPT][Fmt::kPerChunk],
+                              double (&f)[CPT], double (&off)[CPT]) {
+    constexpr int W = kSegSampleW, NW = W / kWave, EPC = Fmt::kPerChunk, CELLS = CPT * NW;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-    float m = chunk_max<Fmt>(x[0]);
+    float mx = chunk_max<Fmt>(x[0]);
 #pragma unroll
-    for (int r = 1; r < CPT; ++r) m = fmaxf(m, chunk_max<Fmt>(x[r]));
-    m = wave_max_u(m);
-    if (lane == 0) s_mx[wid] = m;
+    for (int r = 1; r < CPT; ++r) mx = fmaxf(mx, chunk_max<Fmt>(x[r]));
+    mx = wave_max_u(mx);
+    if (lane == 0) s_mx[wid] = mx;
     __syncthreads();
-    m = s_mx[0];
+    mx = s_mx[0];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) m = fmaxf(m, s_mx[w]);
-    empty = !(m > kNegInf);
-    k = shift_of_max(m, c2);
+    for (int w = 1; w < NW; ++w) mx = fmaxf(mx, s_mx[w]);
+    empty = !(mx > kNegInf);
+    k = shift_of_max(mx, c2);
 #pragma unroll
     for (int r = 0; r < CPT; ++r) {
-        float sm = exp2_fast(__builtin_fmaf(Fmt::get(x[r], 0), c2, -k));
+        m[r][0] = exp2_fast(__builtin_fmaf(Fmt::get(x[r], 0), c2, -k));
+        float sm = m[r][0];
 #pragma unroll
-        for (int e = 1; e < EPC; ++e) sm = sm + exp2_fast(__builtin_fmaf(Fmt::get(x[r], e), c2, -k));
-        const double t = wave_scan_add(fixed40(sm));
+        for (int e = 1; e < EPC; ++e) {
+            m[r][e] = exp2_fast(__builtin_fmaf(Fmt::get(x[r], e), c2, -k));
+            sm = sm + m[r][e];
+        }
+        f[r] = fixed40(sm);
+        const double t = wave_scan_add(f[r]);
+        off[r] = t - f[r];
         if (lane == kWave - 1) s_cell[r * NW + wid] = t;
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
     if (wid == 0) {
-        const double t = wave_sum(lane < CPT * NW ? s_cell[lane] : 0.0);
-        if (lane == 0) *s_tot = t;
+        const double cv = lane < CELLS ? s_cell[lane] : 0.0;
+        const double ci = wave_scan_add(cv);
+        if (lane < CELLS) s_excl[lane] = ci - cv;
+        if (lane == kWave - 1) *s_tot = ci;
     }
     __syncthreads();
     T = *s_tot;
@@ -358,6 +370,7 @@ __global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleAr
     static_assert(CELLS <= kWave, "one wave scans the cells");
     __shared__ float s_mx[NW];
     __shared__ double s_cell[CELLS];
+    __shared__ double s_excl[CELLS];
     __shared__ double s_tot;
     __shared__ float s_k[kMaxSampleSegments];
     __shared__ double s_T[kMaxSampleSegments];
@@ -376,10 +389,13 @@ __global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleAr
     chunk_t x[CPT];
 #pragma unroll
     for (int r = 0; r < CPT; ++r) x[r] = stream_chunk<Fmt, true>(row, s * SEG + r * W + tid, a.nchunks, a.V);
+    if (tid == 0) s_tok = -1;  // ordered before the walk by the statistics' barriers
     float k;
     double T;
     bool empty;
-    segment_stats<Fmt, CPT>(x, c2, s_mx, s_cell, &s_tot, k, T, empty);
+    float mass[CPT][EPC];
+    double fx[CPT], off[CPT];
+    segment_stats<Fmt, CPT>(x, c2, s_mx, s_cell, s_excl, &s_tot, k, T, empty, mass, fx, off);
     if (tid == 0) {
         s_k[s] = empty ? kNegInf : k;
         s_T[s] = T;
@@ -417,7 +433,7 @@ __global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleAr
     __syncthreads();
     if (!s_ok) {
         // Out of polls: every other segment's record from the row itself.
-        __shared__ double s_cellx[CELLS];
+        __shared__ double s_cellx[CELLS], s_exclx[CELLS];
         for (int j = 0; j < S; ++j) {
             if (j == s) continue;
             chunk_t y[CPT];
@@ -426,7 +442,9 @@ __global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleAr
             float kj;
             double Tj;
             bool ej;
-            segment_stats<Fmt, CPT>(y, c2, s_mx, s_cellx, &s_tot, kj, Tj, ej);
+            float mj[CPT][EPC];
+            double fj[CPT], oj[CPT];
+            segment_stats<Fmt, CPT>(y, c2, s_mx, s_cellx, s_exclx, &s_tot, kj, Tj, ej, mj, fj, oj);
             if (tid == 0) {
                 s_k[j] = ej ? kNegInf : kj;
                 s_T[j] = Tj;
@@ -477,59 +495,28 @@ __global__ __launch_bounds__(kSegSampleW) void sample_split_kernel(SplitSampleAr
     }
     const uint64_t lo = readlane_u64(incl - wj, sstar);
     // This segment holds the point: its offset in the segment's own units.
+    // The cell (round r of this wave) and the lane that hold it, from the
+    // prefixes prepared before the exchange; that lane walks its chunk with
+    // the same fp32 sums of the same masses.
     const double target = __builtin_ldexp(double(c - lo), int(K - k));
-    if (wid == 0) {
-        const double cv = lane < CELLS ? s_cell[lane] : 0.0;
-        const double ci = wave_scan_add(cv);
-        if (lane < CELLS) s_cell[lane] = ci - cv;  // exclusive prefix
-        if (lane == 0) s_tok = -1;
-    }
-    __syncthreads();
-    int rr = -1;
-    double clo = 0.0;
+#pragma unroll
     for (int r = 0; r < CPT; ++r) {
-        const int ci = r * NW + wid;
-        const double l = s_cell[ci];
-        const double h = ci + 1 < CELLS ? s_cell[ci + 1] : T;
-        if (l <= target && target < h) {
-            rr = r;
-            clo = l;
-        }
-    }
-    if (rr >= 0) {
-        // The chunk of round rr, picked with opaque bit masks (no indexed
-        // register access), and its masses exactly as in the first sweep.
-        uint32_t b[4] = {0u, 0u, 0u, 0u};
+        const double cl = s_excl[r * NW + wid];
+        if (cl <= target && target < cl + s_cell[r * NW + wid]) {
+            const double mylo = cl + off[r];
+            if (fx[r] > 0.0 && mylo <= target && target < mylo + fx[r]) {
+                const double want = target - mylo;
+                float racc = mass[r][0];
+                int pick = fixed40(racc) > want ? 0 : -1, last_pos = mass[r][0] > 0.0f ? 0 : -1;
 #pragma unroll
-        for (int r = 0; r < CPT; ++r) {
-            uint32_t msk = 0u - uint32_t(rr == r);
-            asm volatile("" : "+v"(msk));
-            b[0] |= x[r].x & msk;
-            b[1] |= x[r].y & msk;
-            b[2] |= x[r].z & msk;
-            b[3] |= x[r].w & msk;
-        }
-        const chunk_t xc{b[0], b[1], b[2], b[3]};
-        float m[EPC];
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) m[e] = exp2_fast(__builtin_fmaf(Fmt::get(xc, e), c2, -k));
-        float sm = m[0];
-#pragma unroll
-        for (int e = 1; e < EPC; ++e) sm = sm + m[e];
-        const double f = fixed40(sm);
-        const double mylo = clo + (wave_scan_add(f) - f);
-        if (f > 0.0 && mylo <= target && target < mylo + f) {
-            const double want = target - mylo;
-            float racc = m[0];
-            int pick = fixed40(racc) > want ? 0 : -1, last_pos = m[0] > 0.0f ? 0 : -1;
-#pragma unroll
-            for (int e = 1; e < EPC; ++e) {
-                racc = racc + m[e];
-                if (m[e] > 0.0f) last_pos = e;
-                if (pick < 0 && fixed40(racc) > want) pick = e;
+                for (int e = 1; e < EPC; ++e) {
+                    racc = racc + mass[r][e];
+                    if (mass[r][e] > 0.0f) last_pos = e;
+                    if (pick < 0 && fixed40(racc) > want) pick = e;
+                }
+                if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
+                s_tok = ((s * SEG + r * W + tid) * EPC) + pick;
             }
-            if (pick < 0) pick = last_pos >= 0 ? last_pos : 0;
-            s_tok = ((s * SEG + rr * W + tid) * EPC) + pick;
         }
     }
     __syncthreads();
