@@ -75,8 +75,8 @@ constexpr int kMaxItems = 256;
 constexpr int kMaxPolls = 32;
 
 struct FusedArgs {
-    // What the prologue needs comes first: the kernel requests these words
-    // at once on entry (one round trip to the argument buffer).
+    // Every word is requested at once on entry (one round trip to the
+    // argument buffer); those the prologue needs come first.
     const void* target;        // [B, K+1, V]
     const void* draft;         // [B, K, V]
     const int32_t* tokens;     // [B, K]
@@ -283,7 +283,7 @@ __device__ inline ItemRec encode_item(const FusedArgs& a, const Schedule& sc, in
     int kk = sc.prev_same(k);
     const int prev = link_of(kk);
     while (kk > k - 3) kk = sc.prev_same(kk);
-    r.links = (prev & 0xFFFF) | (link_of(kk) << 16);
+    r.links = int((uint32_t(prev) & 0xFFFFu) | (uint32_t(link_of(kk)) << 16));
     return r;
 }
 
