@@ -278,8 +278,9 @@ int osd_verify_distill_rejected(const void* target_logits, const void* draft_log
  * workspace     osd_verify_tree_workspace_bytes(B, N) zero-initialised bytes
  *
  * N <= OSD_MAX_TREE_NODES; V up to 32768 (bf16) or 16384 (fp32), otherwise
- * OSD_ERR_UNSUPPORTED.  One workgroup per (sequence, node): every node's
- * rows are read once, whether or not the walk reaches it.
+ * OSD_ERR_UNSUPPORTED.  Every node's rows are read once, whether or not the
+ * walk reaches it: one workgroup per (sequence, node), or, for 16-byte
+ * aligned rows at T > 0, about one workgroup per CU walking the nodes.
  */
 #define OSD_MAX_TREE_NODES 64
 size_t osd_verify_tree_workspace_bytes(int B, int N);

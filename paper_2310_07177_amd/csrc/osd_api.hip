@@ -639,6 +639,7 @@ int osd_verify_tree(const void* target_logits, const void* draft_logits, int dty
     L.vec = (int64_t(V) * elem_bytes(dtype)) % 16 == 0 && aligned16(target_logits) &&
             (greedy || aligned16(draft_logits));
     L.stream = static_cast<hipStream_t>(stream);
+    L.cus = device_cus(L.stream);
     return osd::launch_verify_tree(L) == hipSuccess ? OSD_OK : OSD_ERR_DEVICE;
 }
 

@@ -161,6 +161,7 @@ struct TreeLaunch {
     uint32_t* records;   // [B*N] zero on entry and exit
     uint32_t* counters;  // [B]   zero on entry and exit
     bool vec;
+    int cus;  // compute units of the device
     hipStream_t stream;
 };
 bool pick_tree_tile(int V, int per_chunk, RowTile* t);
