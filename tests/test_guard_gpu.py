@@ -4,7 +4,8 @@ Each output is a window inside a larger allocation filled with a canary byte;
 after the call, the bytes before and after every window must be untouched.
 The shapes are the ones most likely to write past an end: ragged proposal
 lengths, row lengths that are not a multiple of a chunk (V = 1, 7, 1001),
-outputs that are not 16-byte aligned, long streamed rows, and trees.  The
+outputs that are not 16-byte aligned, long streamed rows, and trees (both
+layouts of the tree kernel: V = 4096 bf16 takes the streaming one).  The
 calls go through the C ABI directly, with raw pointers into the windows.
 """
 import ctypes
@@ -114,7 +115,7 @@ def test_verify_and_distill_outputs_stay_in_bounds(L, V, dtype, shift):
         g.check(f"verify_distill_rejected V={V} {dtype} output {j}")
 
 
-@pytest.mark.parametrize("V,dtype", [(7, "bf16"), (1001, "f32"), (70001, "bf16")])
+@pytest.mark.parametrize("V,dtype", [(7, "bf16"), (1001, "f32"), (4096, "bf16"), (70001, "bf16")])
 def test_sample_and_tree_outputs_stay_in_bounds(L, V, dtype):
     import torch
     dt = binding.OSD_BF16 if dtype == "bf16" else binding.OSD_F32
