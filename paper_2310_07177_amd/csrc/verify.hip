@@ -53,10 +53,15 @@ __device__ inline bool rejects(uint32_t s) {
 // exponentials), where every element is at most about 1: chunk sums stay
 // below 16 and row totals below 2^17, so a 2^-44 fixed point never overflows.
 constexpr int kFixedShift = 44;
-// Polls of the earlier positions' records before a rejecting workgroup draws
-// speculatively.  Each poll is one device-coherent round trip plus a short
-// sleep; the bound keeps every wait finite whatever the dispatch order.
-constexpr int kMaxPolls = 24;
+// Looks at the earlier positions' records before a rejecting workgroup draws
+// speculatively (a speculative draw is always correct: the finalizer takes
+// the first rejection's token).  Each look is one device-coherent round trip.
+// The row-resident kernel looks once: its draw works on registers it already
+// holds, and waiting for a late earlier row costs more than drawing (a
+// measured 0.4 us at B = 64, k = 8).  The streamed kernel, whose draw reads
+// the row pair again, waits longer (24 looks with a short sleep).
+constexpr int kMaxPolls = 1;
+constexpr int kMaxLongPolls = 24;
 
 struct VerifyArgs {
     const void* target;
@@ -536,12 +541,12 @@ __global__ __launch_bounds__(kLongW, 1) void verify_long_kernel(VerifyArgs a) {
                 publish(a, b, i, kb, make_rec(kRecAccept, 0));
             } else {
                 if (lane == 0) publish_u32(a.records + int64_t(b) * (K + 1) + i, make_rec(kRecRejectPending, 0));
-                if (i > 0 && poll_earlier(a, b, i, kMaxPolls) == 2) {
+                if (i > 0 && poll_earlier(a, b, i, kMaxLongPolls) == 2) {
                     flag = 0;
                     publish(a, b, i, kb, make_rec(kRecRejectSkipped, 0));
                 }
             }
-        } else if (poll_earlier(a, b, i, kMaxPolls) == 2) {
+        } else if (poll_earlier(a, b, i, kMaxLongPolls) == 2) {
             flag = 0;
             publish(a, b, i, kb, make_rec(kRecBonusSkipped, 0));
         }
