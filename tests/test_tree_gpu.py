@@ -69,11 +69,13 @@ def test_tree_medusa_shape_full_batch(osd):
         check_tree(osd, synth.config_medusa_tree(seed), f"medusa tree seed={seed}")
 
 
-@pytest.mark.parametrize("V,dtype", [(5, "bf16"), (1001, "bf16"), (4096, "bf16"), (16384, "bf16"),
-                                     (32768, "bf16"), (4100, "f32"), (16384, "f32")])
+@pytest.mark.parametrize("V,dtype", [(5, "bf16"), (1001, "bf16"), (4096, "bf16"), (8000, "bf16"), (16384, "bf16"),
+                                     (24000, "bf16"), (32768, "bf16"), (4100, "f32"), (16384, "f32")])
 def test_tree_random_shapes_and_vocabularies(osd, V, dtype):
     """Random trees (node n's parent uniform over 0..n-1) of up to 40 nodes,
-    every tile of the kernel, aligned and unaligned rows."""
+    every tile of both layouts (unaligned rows take one workgroup per node;
+    V = 8000 and 24000 bf16 end in a partial round of the streaming
+    layout's 1024x1 and 1024x3 tiles)."""
     g = synth.rng(V)
     for k, N in enumerate((2, 9, 40)):
         par = np.stack([synth.random_tree_parents(g, N) for _ in range(6)])
