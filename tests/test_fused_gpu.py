@@ -106,11 +106,12 @@ def test_fused_tiny_fp32(osd):
     check_fused(osd, x, "fkl", 0.5, x["mask"], "fused tiny fp32")
 
 
-@pytest.mark.parametrize("V,dtype", [(8192, "bf16"), (8200, "bf16"), (4100, "f32"), (1001, "bf16"),
-                                     (40000, "bf16")])
+@pytest.mark.parametrize("V,dtype", [(1000, "bf16"), (8192, "bf16"), (8200, "bf16"), (20000, "bf16"), (4100, "f32"),
+                                     (1001, "bf16"), (40000, "bf16")])
 def test_fused_vocab_sizes(osd, V, dtype):
-    """Streaming tiles of several sizes, an unaligned row length and a
-    vocabulary above the streaming tiles (the last two take the two-call
+    """Streaming tiles of several sizes (256x1, 1024x1, 1024x2, 1024x3, the
+    partial ones ending in a part-filled round), an unaligned row length and
+    a vocabulary above the streaming tiles (the last two take the two-call
     path inside the entry point)."""
     x = synth.verify_inputs(6, 4, V, dtype, T=0.9, seed=V % 97, target_std=2.5, draft_noise=0.8)
     mask = (np.random.default_rng(V).random((6, 4)) < 0.7).astype(np.uint8)
