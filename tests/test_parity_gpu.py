@@ -269,6 +269,23 @@ def test_distill_shapes_and_settings(osd, kind, beta, tau, V):
     check_distill(osd, t, s, kind, beta, tau, mask, f"{kind} beta={beta} tau={tau} V={V}")
 
 
+@pytest.mark.parametrize("kind", ["jsd", "fkl"])
+@pytest.mark.parametrize("V,dtype", [(2000, "bf16"), (12000, "bf16"), (20000, "bf16"), (1000, "f32"), (6000, "f32"),
+                                     (10000, "f32")])
+def test_distill_stream_tiles(osd, kind, V, dtype):
+    """The streaming kernel's 256x1, 1024x2 and 1024x3 tiles, each ending in
+    a part-filled round."""
+    g = np.random.default_rng(V + 3)
+    B, K = 3, 4
+    t = g.normal(0, 2.5, (B, K, V)).astype(np.float32)
+    s = (t + g.normal(0, 1, (B, K, V))).astype(np.float32)
+    if dtype == "bf16":
+        t = synth.to_bf16(t)
+        s = synth.to_bf16((synth.bf16_to_f32(t) + g.normal(0, 1, (B, K, V))).astype(np.float32))
+    mask = (g.random((B, K)) < 0.7).astype(np.uint8)
+    check_distill(osd, t, s, kind, 0.5, 0.9, mask, f"{kind} tile V={V} {dtype}")
+
+
 def test_distill_identical_rows_zero(osd):
     x = synth.config_t5_vocab(1, B=8)
     K, V = x["K"], x["V"]
